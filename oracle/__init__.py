@@ -1,0 +1,175 @@
+"""Plain fp64 CPU oracle for the multi-step GRPO loss (AsyncWebRL, Eq. 1 and Eq. 2).
+
+TEST INFRASTRUCTURE ONLY: the test suite, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package; the product
+library never does.  It shares no code with the HIP path.  The arithmetic lives
+in ``grpo_oracle.c`` (built with gcc into ``liboracle.so`` next to it); this
+module only marshals numpy arrays.  The fused LM-head oracle in ``fused.py``
+adds fp64 matrix products around the same per-row definition.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "grpo_oracle.c")
+_SO = os.path.join(_HERE, "liboracle.so")
+
+ERR_ACTION = 1
+ERR_OFFSETS = 2
+ERR_NONFINITE = 4
+NORM_TRAJ_STEPS = 0
+NORM_CONST_K = 1
+
+DT_F32, DT_BF16, DT_F64 = 0, 1, 2
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compiles grpo_oracle.c with gcc (-O2, OpenMP over rows)."""
+    if force or not os.path.exists(_SO) or os.path.getmtime(_SO) < os.path.getmtime(_SRC):
+        tmp = _SO + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _SO)
+    return _SO
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_SO)
+        P = ctypes.c_void_p
+        I32, I64, D = ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        lib.oracle_segments.argtypes = [I64, I32, P, I32, P, P, P, P]
+        lib.oracle_segments.restype = ctypes.c_int
+        lib.oracle_advantages.argtypes = [P, I32, I32, I32, D, P]
+        lib.oracle_advantages.restype = None
+        lib.oracle_loss_rows.argtypes = [P, ctypes.c_int, I64, I64, P, P, P, P, P, P, I32, I32, D,
+                                         ctypes.c_int, D, D, D, D, D, I64, I64, P, P, P, P, P]
+        lib.oracle_loss_rows.restype = ctypes.c_int
+        lib.oracle_reduce.argtypes = [P, P, I64, I32, P]
+        lib.oracle_reduce.restype = D
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+@dataclass
+class Segments:
+    traj_tok_off: np.ndarray  # int32 [n_traj+1]
+    tok_traj: np.ndarray      # int32 [T]
+    traj_steps: np.ndarray    # int32 [n_traj]  (|tau_i|)
+    flags: int
+
+
+def segments(T: int, step_tok_off, traj_step_off) -> Segments:
+    """Token/step/trajectory bookkeeping of Eq. 1's triple sum (see grpo_oracle.c)."""
+    lib = _load()
+    sto = _c(step_tok_off, np.int32)
+    tso = _c(traj_step_off, np.int32)
+    n_steps, n_traj = len(sto) - 1, len(tso) - 1
+    tto = np.empty(n_traj + 1, np.int32)
+    tt = np.empty(T, np.int32)
+    ts = np.empty(n_traj, np.int32)
+    f = lib.oracle_segments(T, n_steps, _ptr(sto), n_traj, _ptr(tso), _ptr(tto), _ptr(tt), _ptr(ts))
+    return Segments(tto, tt, ts, int(f))
+
+
+def gather_index(T: int, ld: int, actions) -> np.ndarray:
+    """Flat element index t*ld + a_t of each token's action logit."""
+    return np.arange(T, dtype=np.int64) * np.int64(ld) + np.asarray(actions, dtype=np.int64)
+
+
+def advantages(rewards, group_size: int, ddof: int = 1, std_eps: float = 0.0) -> np.ndarray:
+    """Group-relative advantage of Sec. 3.2, fp64."""
+    lib = _load()
+    r = _c(rewards, np.float32)
+    out = np.empty(len(r), np.float64)
+    lib.oracle_advantages(_ptr(r), len(r), group_size, ddof, float(std_eps), _ptr(out))
+    return out
+
+
+@dataclass
+class LossResult:
+    loss: float
+    traj_loss: np.ndarray      # [n_traj] fp64
+    token_logp: np.ndarray     # [rows]   fp64
+    token_contrib: np.ndarray  # [rows]   fp64, -w_i * s_t
+    token_g: np.ndarray        # [rows]   fp64, dloss/dl_t * grad_scale
+    token_state: np.ndarray    # [rows]   int32: bit0 eps-clip cut, bit1 dual clip cut
+    dlogits: np.ndarray | None  # [rows, V] fp64
+    flags: int
+
+
+def _logits_dtype(logits: np.ndarray) -> int:
+    if logits.dtype == np.float32:
+        return DT_F32
+    if logits.dtype == np.uint16:  # bfloat16 bit patterns
+        return DT_BF16
+    if logits.dtype == np.float64:
+        return DT_F64
+    raise TypeError(f"oracle: unsupported logits dtype {logits.dtype}")
+
+
+def loss_rows(logits: np.ndarray, actions, behave_logp, prox_logp, adv, seg: Segments, group_size: int, *,
+              V: int | None = None, norm: int = NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2,
+              eps_high: float = 0.2, dual_clip_c: float = 0.0, grad_scale: float = 1.0,
+              n_groups_total: float = 0.0, row_begin: int = 0, row_end: int | None = None,
+              want_dlogits: bool = True, row_offset: int = 0) -> LossResult:
+    """Per-token quantities and dlogits for token rows [row_begin, row_end).
+
+    ``logits`` is [rows_held, ld] (float32, bfloat16 bit patterns as uint16, or
+    float64) and holds token rows starting at token ``row_offset``; V (default
+    ld) is the vocabulary size.  Per-token inputs (actions, log-probs) are
+    indexed by absolute token number; per-row outputs by t - row_begin.  The
+    loss and traj_loss fields sum only the rows computed.
+    """
+    lib = _load()
+    logits = np.ascontiguousarray(logits)
+    dt = _logits_dtype(logits)
+    ld = logits.shape[1]
+    V = ld if V is None else int(V)
+    assert 1 <= V <= ld
+    T = len(seg.tok_traj)
+    n_traj = len(seg.traj_steps)
+    if row_end is None:
+        row_end = T
+    n_rows = row_end - row_begin
+    assert row_begin >= row_offset and row_end - row_offset <= logits.shape[0]
+    a = _c(actions, np.int32)
+    b = _c(behave_logp, np.float32)
+    p = _c(prox_logp, np.float32)
+    A = _c(adv, np.float64)
+    n_groups = float(n_groups_total) if n_groups_total else n_traj / group_size
+    logp = np.empty(n_rows, np.float64)
+    contrib = np.empty(n_rows, np.float64)
+    g = np.empty(n_rows, np.float64)
+    st = np.empty(n_rows, np.int32)
+    dl = np.empty((n_rows, V), np.float64) if want_dlogits else None
+    # The C routine addresses token row t at element t*ld of its base pointer:
+    # shift the base back by row_offset rows so absolute token numbers work.
+    base = logits.ctypes.data - row_offset * ld * logits.itemsize
+    f = lib.oracle_loss_rows(ctypes.c_void_p(base), dt, V, ld, _ptr(a), _ptr(b), _ptr(p), _ptr(A),
+                             _ptr(seg.tok_traj), _ptr(seg.traj_steps), seg.flags, group_size, n_groups,
+                             norm, float(k), float(eps_low), float(eps_high), float(dual_clip_c),
+                             float(grad_scale), row_begin, row_end, _ptr(logp), _ptr(contrib), _ptr(g),
+                             _ptr(st), _ptr(dl))
+    traj = np.zeros(n_traj, np.float64)
+    tt = np.ascontiguousarray(seg.tok_traj[row_begin:row_end])
+    total = lib.oracle_reduce(_ptr(contrib), _ptr(tt), n_rows, n_traj, _ptr(traj))
+    return LossResult(float(total), traj, logp, contrib, g, st, dl, int(f))
