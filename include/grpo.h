@@ -1,0 +1,191 @@
+/*
+ * grpo.h -- C ABI of libgrpo, the MI355X (gfx950) library for the multi-step
+ * GRPO token loss of AsyncWebRL (arXiv 2606.05597) and its gradient.
+ *
+ * The objective (Eq. 1, Sec. 3.2), per task group of G trajectories:
+ *   J = 1/(G k) sum_i sum_{j<=|tau_i|} sum_{t in step j}
+ *         min( rho_t A_i , omega_t clip(r_t, 1-eps_low, 1+eps_high) A_i )
+ *   rho = pi/pi_behave, r = pi/pi_prox, omega = pi_prox/pi_behave,
+ *   A_i = (r_i - mean r)/std r over the group (Sec. 3.2),
+ *   1/k replaced by 1/|tau_i| for the paper's baseline normaliser (Sec. 3.2),
+ *   and, when dual_clip_c > 0 and A_i < 0, the per-token term floored at
+ *   c*A_i (Eq. 2, Appendix B.2).  pi is the softmax of the policy's
+ *   vocabulary logits at the token's position; importance sampling is per
+ *   token (Table 5).
+ * The library returns loss = -J averaged over groups,
+ *   loss = -sum_t w_{i(t)} s_t,  w_i = 1/(n_groups*G*|tau_i|)  or  1/(n_groups*G*k),
+ * and dlogits = grad_scale * dloss/dz, i.e. row t is
+ *   g_t * (softmax(z_t) - onehot(a_t)),  g_t = grad_scale * w_i * ds_t/dl_t.
+ * pi_behave and pi_prox are constants (no gradient).
+ *
+ * Conventions for every entry point:
+ *  - Pointers named "device" are device memory owned by the caller; the
+ *    library never allocates, frees or synchronises.  All work is enqueued on
+ *    the caller's stream `s` (0 = the null stream) in stream order.
+ *  - Scalars and the structs below are read on the host during the call;
+ *    the structs may live on the caller's stack.
+ *  - The return value is a grpo_status.  Argument errors are detected on the
+ *    host before anything is enqueued; nothing is launched when the status is
+ *    negative.  GRPO_ERR_HIP means a HIP launch failed (work enqueued before
+ *    it may have run).
+ *  - Errors in device data (action ids, offsets, non-finite values) cannot be
+ *    seen by the host without a sync: they are reported through
+ *    grpo_aux.error_flags and handled as documented there.
+ *  - The ragged batch (Eq. 1's triple sum) is CSR: trajectory i owns steps
+ *    [traj_step_off[i], traj_step_off[i+1]), step j owns action tokens
+ *    [step_tok_off[j], step_tok_off[j+1]) of the packed token axis.  Groups are
+ *    G consecutive trajectories.  Only loss-mask (action) tokens are packed.
+ */
+#ifndef GRPO_H_
+#define GRPO_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GRPO_OK = 0,
+  GRPO_ERR_ARG = -1,       /* a required pointer is NULL or a scalar is out of range */
+  GRPO_ERR_SHAPE = -2,     /* sizes inconsistent (ld < V, n_traj % group_size, ...)  */
+  GRPO_ERR_DTYPE = -3,     /* unsupported dtype                                      */
+  GRPO_ERR_WORKSPACE = -4, /* workspace NULL or smaller than the size query         */
+  GRPO_ERR_ALIGN = -5,     /* a device pointer is not aligned as documented          */
+  GRPO_ERR_HIP = -6        /* a HIP launch returned an error                         */
+} grpo_status;
+
+typedef enum { GRPO_F32 = 0, GRPO_BF16 = 1 } grpo_dtype;
+
+typedef enum {
+  GRPO_NORM_TRAJ_STEPS = 0, /* 1/|tau_i|: the multi-step GRPO baseline (Sec. 3.2) */
+  GRPO_NORM_CONST_K = 1     /* 1/k: the paper's constant normaliser (Sec. 3.2)    */
+} grpo_norm;
+
+/* Bits of grpo_aux.error_flags (device int32, overwritten by every call). */
+#define GRPO_FLAG_ACTION 1    /* some a_t outside [0, V): that row adds 0 and gets a zero dlogits row  */
+#define GRPO_FLAG_OFFSETS 2   /* malformed offsets: every dlogits row is zero and the loss is NaN     */
+#define GRPO_FLAG_NONFINITE 4 /* a non-finite log-prob, input log-prob or advantage; values propagate */
+
+/* The ragged batch.  Offsets are device int32 arrays.  Valid offsets:
+ * step_tok_off[0] = 0, non-decreasing, step_tok_off[n_steps] = T (a step may
+ * hold no action token); traj_step_off[0] = 0, strictly increasing (every
+ * trajectory has >= 1 step, so |tau_i| >= 1), traj_step_off[n_traj] = n_steps. */
+typedef struct {
+  int32_t n_traj;               /* N >= 1, a multiple of group_size              */
+  int32_t group_size;           /* G >= 1 (Table 5: 8)                           */
+  int32_t n_steps;              /* >= n_traj                                     */
+  const int32_t* step_tok_off;  /* device [n_steps + 1]                          */
+  const int32_t* traj_step_off; /* device [n_traj + 1]                           */
+} grpo_segments;
+
+/* Loss hyper-parameters (Table 5 values in brackets). */
+typedef struct {
+  int32_t norm;          /* grpo_norm                                                      */
+  float k;               /* constant normaliser, > 0 when norm = GRPO_NORM_CONST_K [10]    */
+  float eps_low;         /* clip range [1 - eps_low, 1 + eps_high], 0 <= eps_low < 1 [0.2] */
+  float eps_high;        /* >= 0 [0.2]                                                     */
+  float dual_clip_c;     /* 0 disables the dual clip; otherwise > 1 (Eq. 2) [3.0]          */
+  float grad_scale;      /* upstream d(objective)/d(loss), folded into dlogits [1]        */
+  double n_groups_total; /* groups in the global batch for the normaliser; 0 = N/G        */
+} grpo_loss_params;
+
+/* Optional outputs; every field may be NULL (device pointers unless noted). */
+typedef struct {
+  float* token_logp;     /* [T] new log-prob l_t of each action token (fp32)               */
+  int32_t* tok_traj;     /* [T] trajectory of each token                                   */
+  int32_t* traj_tok_off; /* [n_traj + 1] first token of each trajectory, then T            */
+  int64_t* gather_idx;   /* [T] flat element index t*ld + a_t of each action logit         */
+  double* traj_loss;     /* [n_traj] -sum over the trajectory's tokens of w_i s_t          */
+  int64_t* clip_counts;  /* [2] tokens whose gradient the eps clip / the dual clip cut     */
+  int32_t* error_flags;  /* [1] GRPO_FLAG_* bits seen by this call                         */
+  hipEvent_t hot_begin;  /* host handles: when both are set, recorded on `s` right before  */
+  hipEvent_t hot_end;    /*   and after the dominant kernel (for timing)                   */
+} grpo_aux;
+
+/*
+ * Group-relative advantage (Sec. 3.2): for each group of `group_size`
+ * consecutive trajectories, A_i = (r_i - mean)/(std + std_eps), with the std
+ * taken with `ddof` degrees of freedom removed (1 = the unbiased estimate).
+ * A group whose denominator is 0 gets A = 0.  Sums run in fp64 in index
+ * order; the result is stored as fp32.
+ *   rewards  device fp32 [n_traj]      adv_out  device fp32 [n_traj]
+ * Errors: GRPO_ERR_ARG (NULL pointer, ddof not in {0, 1}, std_eps < 0),
+ *         GRPO_ERR_SHAPE (n_traj < 1, group_size < 1, n_traj % group_size).
+ */
+int grpo_advantages(const float* rewards, int32_t n_traj, int32_t group_size, int32_t ddof, float std_eps,
+                    float* adv_out, hipStream_t s);
+
+/* Bytes of device workspace grpo_loss_fwd_bwd needs for T tokens and n_traj trajectories. */
+size_t grpo_loss_workspace_bytes(int64_t T, int32_t n_traj);
+
+/*
+ * The logits path: loss and dlogits of Eq. 1 (+ Eq. 2) from the policy's
+ * vocabulary logits at every action token.
+ *   logits       device [T, ld] of `dt`, row t = token t; columns >= V unread
+ *   dt           GRPO_BF16 or GRPO_F32 (dlogits has the same dtype)
+ *   T >= 0, 1 <= V <= ld
+ *   actions      device int32 [T]  sampled token ids a_t
+ *   behave_logp  device fp32 [T]   log pi_behave(a_t), recorded at rollout
+ *   prox_logp    device fp32 [T]   log pi_prox(a_t); NULL = behave_logp (the
+ *                                  coupled ratio, Sec. 4.3)
+ *   adv          device fp32 [n_traj]  A_i (e.g. from grpo_advantages)
+ *   seg, p       host structs (above)
+ *   loss_out     device fp64 [1]   the loss (not multiplied by grad_scale)
+ *   dlogits      device [T, ld] of `dt`; columns >= V are not written; NULL =
+ *                forward only.  It may alias `logits` (each row is read in
+ *                full before any of it is written).
+ *   aux          host struct of optional outputs, or NULL
+ *   ws, ws_bytes device workspace of at least grpo_loss_workspace_bytes(T, n_traj)
+ * The loss and traj_loss are reduced in a fixed order (bitwise reproducible).
+ * Errors: GRPO_ERR_ARG (NULL required pointer; k <= 0 under CONST_K;
+ *   eps_low not in [0,1); eps_high < 0; dual_clip_c in (0, 1] or < 0;
+ *   non-finite grad_scale; n_groups_total < 0), GRPO_ERR_SHAPE (T < 0, V < 1,
+ *   ld < V, n_traj < 1, group_size < 1, n_traj % group_size, n_steps < n_traj,
+ *   T >= 2^31), GRPO_ERR_DTYPE, GRPO_ERR_WORKSPACE, GRPO_ERR_ALIGN (logits or
+ *   dlogits not aligned to the element size), GRPO_ERR_HIP.
+ */
+int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                      const int32_t* actions, const float* behave_logp, const float* prox_logp,
+                      const float* adv, const grpo_segments* seg, const grpo_loss_params* p, double* loss_out,
+                      void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
+
+/* Bytes of device workspace fused_lmhead_grpo needs. */
+size_t fused_lmhead_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t vocab_chunk, int32_t n_traj);
+
+/*
+ * The fused LM-head path: the same loss computed from the final hidden states
+ * h [T, H] and the LM-head weight W [H, V], with z = h W formed on the matrix
+ * cores in vocabulary chunks of `vocab_chunk` columns and never stored whole.
+ * Emits the loss, dhidden = dloss/dh = D W^T and dW = dloss/dW = h^T D, where
+ * D = grad_scale * dloss/dz (bf16-rounded per chunk before the two products).
+ *   hidden       device bf16 [T, H] row-major       w_lm device bf16 [H, V] row-major
+ *   T >= 0, H >= 1 and a multiple of 64, V >= 1 and a multiple of 8,
+ *   vocab_chunk  a positive multiple of 256 (8192 is the tuned value)
+ *   actions, behave_logp, prox_logp, adv, seg, p, loss_out, aux: as above
+ *   (aux->gather_idx uses ld = V)
+ *   dhidden      device bf16 [T, H]  (written)
+ *   dw_lm        device fp32 [H, V]; written, or accumulated into when
+ *                accumulate_dw != 0
+ *   ws, ws_bytes device workspace of at least fused_lmhead_workspace_bytes(...)
+ * hidden, w_lm, dhidden and dw_lm must be 16-byte aligned (GRPO_ERR_ALIGN).
+ * Errors: as grpo_loss_fwd_bwd, plus GRPO_ERR_SHAPE for H, V or vocab_chunk
+ *   outside the ranges above.
+ */
+int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V, int32_t vocab_chunk,
+                      const int32_t* actions, const float* behave_logp, const float* prox_logp, const float* adv,
+                      const grpo_segments* seg, const grpo_loss_params* p, double* loss_out, void* dhidden,
+                      float* dw_lm, int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
+                      hipStream_t s);
+
+/* A static, human-readable name for a grpo_status value. */
+const char* grpo_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRPO_H_ */

@@ -1,0 +1,234 @@
+"""MI355X (gfx950) library for the multi-step GRPO token loss of AsyncWebRL.
+
+Thin torch-facing binding of libgrpo's C ABI (include/grpo.h): every function
+here marshals tensors into pointers and calls the entry point of the same
+name; all arithmetic runs in the HIP kernels.  torch provides device memory
+and the current stream only.  There is no CPU fallback: the functions raise
+if the library is not built or a tensor is not on a GPU.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass, field
+
+import torch
+
+from . import _lib
+from ._lib import (GRPO_BF16, GRPO_F32, GRPO_FLAG_ACTION, GRPO_FLAG_NONFINITE, GRPO_FLAG_OFFSETS,  # noqa: F401
+                   GRPO_NORM_CONST_K, GRPO_NORM_TRAJ_STEPS, GrpoError)
+
+__all__ = ["grpo_advantages", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
+           "fused_lmhead_grpo", "grpo_status_str", "LossAux", "GrpoError"]
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (no CPU path)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(status, what):
+    if status != _lib.GRPO_OK:
+        raise GrpoError(status, what)
+
+
+def grpo_status_str(status: int) -> str:
+    return _lib.status_str(status)
+
+
+def grpo_advantages(rewards: torch.Tensor, group_size: int, ddof: int = 1, std_eps: float = 0.0,
+                    out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Group-relative advantages A_i (fp32 [N]) from rewards (fp32 [N])."""
+    _dev(rewards, "rewards")
+    if rewards.dtype != torch.float32:
+        raise TypeError("rewards must be float32")
+    out = torch.empty_like(rewards) if out is None else _dev(out, "out")
+    st = _lib.load().grpo_advantages(_ptr(rewards), rewards.numel(), int(group_size), int(ddof), float(std_eps),
+                                     _ptr(out), _stream(stream))
+    _check(st, "grpo_advantages")
+    return out
+
+
+def grpo_loss_workspace_bytes(T: int, n_traj: int) -> int:
+    return int(_lib.load().grpo_loss_workspace_bytes(int(T), int(n_traj)))
+
+
+def fused_lmhead_workspace_bytes(T: int, H: int, V: int, vocab_chunk: int, n_traj: int) -> int:
+    return int(_lib.load().fused_lmhead_workspace_bytes(int(T), int(H), int(V), int(vocab_chunk), int(n_traj)))
+
+
+@dataclass
+class LossAux:
+    """Optional outputs of the loss entry points (allocate with ``LossAux.alloc``)."""
+    token_logp: torch.Tensor | None = None
+    tok_traj: torch.Tensor | None = None
+    traj_tok_off: torch.Tensor | None = None
+    gather_idx: torch.Tensor | None = None
+    traj_loss: torch.Tensor | None = None
+    clip_counts: torch.Tensor | None = None
+    error_flags: torch.Tensor | None = None
+    hot_events: tuple | None = field(default=None)  # (begin, end) raw hipEvent_t handles
+
+    @staticmethod
+    def alloc(T: int, n_traj: int, device, which=("token_logp", "tok_traj", "traj_tok_off", "gather_idx",
+                                                   "traj_loss", "clip_counts", "error_flags")) -> "LossAux":
+        mk = {
+            "token_logp": lambda: torch.empty(T, dtype=torch.float32, device=device),
+            "tok_traj": lambda: torch.empty(T, dtype=torch.int32, device=device),
+            "traj_tok_off": lambda: torch.empty(n_traj + 1, dtype=torch.int32, device=device),
+            "gather_idx": lambda: torch.empty(T, dtype=torch.int64, device=device),
+            "traj_loss": lambda: torch.empty(n_traj, dtype=torch.float64, device=device),
+            "clip_counts": lambda: torch.empty(2, dtype=torch.int64, device=device),
+            "error_flags": lambda: torch.empty(1, dtype=torch.int32, device=device),
+        }
+        return LossAux(**{k: mk[k]() for k in which})
+
+    def _c(self):
+        a = _lib.Aux()
+        for name in ("token_logp", "tok_traj", "traj_tok_off", "gather_idx", "traj_loss", "clip_counts",
+                     "error_flags"):
+            t = getattr(self, name)
+            setattr(a, name, None if t is None else _dev(t, name).data_ptr())
+        if self.hot_events is not None:
+            a.hot_begin, a.hot_end = self.hot_events
+        return a
+
+
+def _segments(step_tok_off, traj_step_off, group_size):
+    _dev(step_tok_off, "step_tok_off")
+    _dev(traj_step_off, "traj_step_off")
+    if step_tok_off.dtype != torch.int32 or traj_step_off.dtype != torch.int32:
+        raise TypeError("offsets must be int32")
+    seg = _lib.Segments()
+    seg.n_traj = traj_step_off.numel() - 1
+    seg.group_size = int(group_size)
+    seg.n_steps = step_tok_off.numel() - 1
+    seg.step_tok_off = step_tok_off.data_ptr()
+    seg.traj_step_off = traj_step_off.data_ptr()
+    return seg
+
+
+def _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total):
+    p = _lib.LossParams()
+    p.norm = int(norm)
+    p.k = float(k)
+    p.eps_low = float(eps_low)
+    p.eps_high = float(eps_high)
+    p.dual_clip_c = float(dual_clip_c)
+    p.grad_scale = float(grad_scale)
+    p.n_groups_total = float(n_groups_total)
+    return p
+
+
+def _f32(t, name):
+    if t is None:
+        return None
+    _dev(t, name)
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+    return t
+
+
+def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: torch.Tensor, adv: torch.Tensor,
+                      step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *,
+                      V: int | None = None, prox_logp: torch.Tensor | None = None, norm: int = GRPO_NORM_CONST_K,
+                      k: float = 10.0, eps_low: float = 0.2, eps_high: float = 0.2, dual_clip_c: float = 0.0,
+                      grad_scale: float = 1.0, n_groups_total: float = 0.0, dlogits=True,
+                      aux: LossAux | None = None, workspace: torch.Tensor | None = None,
+                      loss_out: torch.Tensor | None = None, stream=None):
+    """Loss (fp64 device scalar) and dlogits of Eq. 1 from logits [T, ld].
+
+    ``dlogits``: True allocates a [T, ld] tensor like ``logits``; None/False is
+    forward only; a tensor is written in place (it may be ``logits`` itself).
+    Returns (loss [1] fp64, dlogits or None).
+    """
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be [T, ld] with unit column stride")
+    if not logits.is_cuda:
+        raise ValueError("logits must be a GPU tensor (no CPU path)")
+    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
+    if dt is None:
+        raise TypeError("logits must be bfloat16 or float32")
+    T = logits.shape[0]
+    ld = logits.stride(0) if T > 0 else logits.shape[1]
+    Vv = logits.shape[1] if V is None else int(V)
+    _dev(actions, "actions")
+    if actions.dtype != torch.int32:
+        raise TypeError("actions must be int32")
+    seg = _segments(step_tok_off, traj_step_off, group_size)
+    par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
+    if dlogits is True:
+        dlogits = torch.empty_like(logits)
+    elif dlogits is False:
+        dlogits = None
+    if dlogits is not None and (dlogits.shape != logits.shape or dlogits.stride() != logits.stride()
+                                or dlogits.dtype != logits.dtype):
+        raise ValueError("dlogits must match logits in shape, stride and dtype")
+    need = grpo_loss_workspace_bytes(T, seg.n_traj)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=logits.device)
+    if loss_out is None:
+        loss_out = torch.empty(1, dtype=torch.float64, device=logits.device)
+    ca = aux._c() if aux is not None else None
+    st = _lib.load().grpo_loss_fwd_bwd(
+        _ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
+        _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
+        _ptr(loss_out), _ptr(dlogits), ctypes.byref(ca) if ca is not None else None, _ptr(workspace),
+        workspace.numel(), _stream(stream))
+    _check(st, "grpo_loss_fwd_bwd")
+    return loss_out, dlogits
+
+
+def fused_lmhead_grpo(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.Tensor, behave_logp: torch.Tensor,
+                      adv: torch.Tensor, step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *,
+                      vocab_chunk: int = 8192, prox_logp: torch.Tensor | None = None,
+                      norm: int = GRPO_NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2, eps_high: float = 0.2,
+                      dual_clip_c: float = 0.0, grad_scale: float = 1.0, n_groups_total: float = 0.0,
+                      dhidden: torch.Tensor | None = None, dw_lm: torch.Tensor | None = None,
+                      accumulate_dw: bool = False, aux: LossAux | None = None,
+                      workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None, stream=None):
+    """Loss, dhidden (bf16 [T, H]) and dW (fp32 [H, V]) from hidden [T, H] and W [H, V] (bf16).
+
+    Returns (loss [1] fp64, dhidden, dw_lm).
+    """
+    _dev(hidden, "hidden")
+    _dev(w_lm, "w_lm")
+    if hidden.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
+        raise TypeError("hidden and w_lm must be bfloat16")
+    T, H = hidden.shape
+    H2, V = w_lm.shape
+    if H2 != H:
+        raise ValueError("hidden and w_lm disagree on H")
+    _dev(actions, "actions")
+    seg = _segments(step_tok_off, traj_step_off, group_size)
+    par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
+    if dhidden is None:
+        dhidden = torch.empty_like(hidden)
+    if dw_lm is None:
+        dw_lm = torch.empty((H, V), dtype=torch.float32, device=hidden.device)
+    _dev(dhidden, "dhidden")
+    _dev(dw_lm, "dw_lm")
+    need = fused_lmhead_workspace_bytes(T, H, V, vocab_chunk, seg.n_traj)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    if loss_out is None:
+        loss_out = torch.empty(1, dtype=torch.float64, device=hidden.device)
+    ca = aux._c() if aux is not None else None
+    st = _lib.load().fused_lmhead_grpo(
+        _ptr(hidden), _ptr(w_lm), T, H, V, int(vocab_chunk), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
+        _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
+        _ptr(loss_out), _ptr(dhidden), _ptr(dw_lm), int(bool(accumulate_dw)),
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "fused_lmhead_grpo")
+    return loss_out, dhidden, dw_lm

@@ -1,0 +1,230 @@
+// Batch bookkeeping kernels: segment validation, group advantages, and the
+// deterministic loss reduction.  All are small next to the row pass.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "device.h"
+#include "launch.h"
+
+namespace grpo {
+
+// ---- segments ----------------------------------------------------------------
+// One workgroup.  Checks the CSR offsets of Eq. 1's trajectory/step/token
+// sums, writes traj_tok_off[i] = step_tok_off[traj_step_off[i]] and the
+// per-trajectory weight w_i = 1/(n_groups * G * |tau_i| or k).
+struct SegArgs {
+  const int32_t* sto;  // [n_steps+1]
+  const int32_t* tso;  // [n_traj+1]
+  int32_t n_steps, n_traj, G, norm;
+  int64_t T;
+  double n_groups, k;
+  WsHeader* hdr;
+  int32_t* traj_tok_off;  // ws [n_traj+1]
+  double* w;              // ws [n_traj]
+  int32_t* aux_traj_tok_off;
+};
+
+__global__ __launch_bounds__(256) void k_segments(const SegArgs a) {
+  const int tid = threadIdx.x;
+  int bad = 0;
+  for (int j = tid; j < a.n_steps; j += 256)
+    if (a.sto[j + 1] < a.sto[j]) bad = 1;
+  for (int i = tid; i < a.n_traj; i += 256)
+    if (a.tso[i + 1] <= a.tso[i]) bad = 1;
+  if (tid == 0) {
+    if (a.sto[0] != 0 || (int64_t)a.sto[a.n_steps] != a.T) bad = 1;
+    if (a.tso[0] != 0 || a.tso[a.n_traj] != a.n_steps) bad = 1;
+  }
+  bad = __syncthreads_or(bad);
+  for (int i = tid; i <= a.n_traj; i += 256) {
+    int off;
+    if (i == a.n_traj) {
+      off = (int)a.T;
+    } else {
+      int st = min(max(a.tso[i], 0), a.n_steps);  // clamped: offsets may be malformed
+      off = a.sto[st];
+      int steps = a.tso[i + 1] - a.tso[i];
+      double den = (a.norm == GRPO_NORM_CONST_K) ? a.k : (double)steps;
+      a.w[i] = 1.0 / (a.n_groups * (double)a.G * den);
+    }
+    a.traj_tok_off[i] = off;
+    if (a.aux_traj_tok_off) a.aux_traj_tok_off[i] = bad ? -1 : off;
+  }
+  if (tid == 0) {
+    a.hdr->flags = bad ? GRPO_FLAG_OFFSETS : 0;
+    a.hdr->done = 0;
+    a.hdr->counts[0] = 0;
+    a.hdr->counts[1] = 0;
+  }
+}
+
+hipError_t launch_segments(const grpo_segments* seg, int64_t T, const grpo_loss_params* p, char* ws,
+                           const LossWs& L, int32_t* aux_traj_tok_off, hipStream_t s) {
+  SegArgs a;
+  a.sto = seg->step_tok_off;
+  a.tso = seg->traj_step_off;
+  a.n_steps = seg->n_steps;
+  a.n_traj = seg->n_traj;
+  a.G = seg->group_size;
+  a.norm = p->norm;
+  a.T = T;
+  a.n_groups = n_groups_of(seg, p);
+  a.k = (double)p->k;
+  a.hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+  a.traj_tok_off = reinterpret_cast<int32_t*>(ws + L.traj_tok_off);
+  a.w = reinterpret_cast<double*>(ws + L.w);
+  a.aux_traj_tok_off = aux_traj_tok_off;
+  hipLaunchKernelGGL(k_segments, dim3(1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---- reduction -----------------------------------------------------------------
+// One workgroup per trajectory sums its tokens' contributions in a fixed
+// order; the last workgroup to finish sums the trajectories in index order.
+struct ReduceArgs {
+  int64_t T;
+  int32_t n_traj;
+  WsHeader* hdr;
+  const int32_t* traj_tok_off;
+  const double* contrib;
+  const int8_t* state;
+  double* traj_loss;  // ws
+  double* loss_out;
+  double* aux_traj_loss;
+  int64_t* aux_clip_counts;
+  int32_t* aux_error_flags;
+};
+
+template <int NT>
+__device__ __forceinline__ double block_sum(double v, double* sh) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) sh[wv] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0)
+    for (int q = 0; q < NT / 64; ++q) r += sh[q];
+  __syncthreads();
+  return r;  // valid in thread 0
+}
+
+__global__ __launch_bounds__(256) void k_reduce(const ReduceArgs a) {
+  __shared__ double sh[4];
+  __shared__ int is_last;
+  const int i = blockIdx.x, tid = threadIdx.x;
+  const int64_t t0 = min(max((int64_t)a.traj_tok_off[i], (int64_t)0), a.T);
+  const int64_t t1 = min(max((int64_t)a.traj_tok_off[i + 1], t0), a.T);
+  double acc = 0.0;
+  int64_t c_eps = 0, c_dual = 0;
+  for (int64_t t = t0 + tid; t < t1; t += 256) {
+    acc += a.contrib[t];
+    const int st = a.state[t];
+    c_eps += st & 1;
+    c_dual += (st >> 1) & 1;
+  }
+  const double tot = block_sum<256>(acc, sh);
+  c_eps = wave_sum_i64(c_eps);
+  c_dual = wave_sum_i64(c_dual);
+  if ((tid & 63) == 0 && (c_eps | c_dual)) {
+    atomicAdd((unsigned long long*)&a.hdr->counts[0], (unsigned long long)c_eps);
+    atomicAdd((unsigned long long*)&a.hdr->counts[1], (unsigned long long)c_dual);
+  }
+  __syncthreads();  // every wave's counter update is performed before the block reports done
+  if (tid == 0) {
+    a.traj_loss[i] = tot;
+    __threadfence();
+    const unsigned prev = atomicAdd(&a.hdr->done, 1u);
+    is_last = (prev == (unsigned)gridDim.x - 1);
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  double part = 0.0;
+  for (int q = tid; q < a.n_traj; q += 256)
+    part += __hip_atomic_load(&a.traj_loss[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const double loss = block_sum<256>(part, sh);
+  const int flags = __hip_atomic_load(&a.hdr->flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const bool bad = flags & GRPO_FLAG_OFFSETS;
+  if (a.aux_traj_loss)
+    for (int q = tid; q < a.n_traj; q += 256)
+      a.aux_traj_loss[q] =
+          bad ? (double)NAN : __hip_atomic_load(&a.traj_loss[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) {
+    *a.loss_out = bad ? (double)NAN : loss;
+    if (a.aux_clip_counts) {
+      a.aux_clip_counts[0] = __hip_atomic_load(&a.hdr->counts[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      a.aux_clip_counts[1] = __hip_atomic_load(&a.hdr->counts[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (a.aux_error_flags) *a.aux_error_flags = flags;
+  }
+}
+
+hipError_t launch_reduce(int64_t T, int32_t n_traj, char* ws, const LossWs& L, double* loss_out,
+                         const grpo_aux* aux, hipStream_t s) {
+  ReduceArgs a;
+  a.T = T;
+  a.n_traj = n_traj;
+  a.hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+  a.traj_tok_off = reinterpret_cast<const int32_t*>(ws + L.traj_tok_off);
+  a.contrib = reinterpret_cast<const double*>(ws + L.contrib);
+  a.state = reinterpret_cast<const int8_t*>(ws + L.state);
+  a.traj_loss = reinterpret_cast<double*>(ws + L.traj_loss);
+  a.loss_out = loss_out;
+  a.aux_traj_loss = aux ? aux->traj_loss : nullptr;
+  a.aux_clip_counts = aux ? aux->clip_counts : nullptr;
+  a.aux_error_flags = aux ? aux->error_flags : nullptr;
+  hipLaunchKernelGGL(k_reduce, dim3(n_traj), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---- group advantages (Sec. 3.2) -------------------------------------------------
+// One workgroup per group; the moments are summed serially in fp64 so the
+// result does not depend on the launch shape.
+__global__ __launch_bounds__(64) void k_advantages(const float* __restrict__ r, int G, int ddof, double std_eps,
+                                                   float* __restrict__ adv) {
+  __shared__ double sh_mean, sh_den;
+  const int64_t base = (int64_t)blockIdx.x * G;
+  if (threadIdx.x == 0) {
+    double mean = 0.0;
+    for (int q = 0; q < G; ++q) mean += (double)r[base + q];
+    mean /= (double)G;
+    double ss = 0.0;
+    for (int q = 0; q < G; ++q) {
+      const double d = (double)r[base + q] - mean;
+      ss += d * d;
+    }
+    const double sd = (G - ddof > 0) ? sqrt(ss / (double)(G - ddof)) : 0.0;
+    sh_mean = mean;
+    sh_den = sd + std_eps;
+  }
+  __syncthreads();
+  const double mean = sh_mean, den = sh_den;
+  for (int q = threadIdx.x; q < G; q += 64)
+    adv[base + q] = (den == 0.0) ? 0.f : (float)(((double)r[base + q] - mean) / den);
+}
+
+}  // namespace grpo
+
+extern "C" int grpo_advantages(const float* rewards, int32_t n_traj, int32_t group_size, int32_t ddof,
+                               float std_eps, float* adv_out, hipStream_t s) {
+  if (!rewards || !adv_out) return GRPO_ERR_ARG;
+  if (ddof != 0 && ddof != 1) return GRPO_ERR_ARG;
+  if (!(std_eps >= 0.f) || !isfinite(std_eps)) return GRPO_ERR_ARG;
+  if (n_traj < 1 || group_size < 1 || n_traj % group_size != 0) return GRPO_ERR_SHAPE;
+  hipLaunchKernelGGL(grpo::k_advantages, dim3(n_traj / group_size), dim3(64), 0, s, rewards, group_size, ddof,
+                     (double)std_eps, adv_out);
+  return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+}
+
+extern "C" const char* grpo_status_str(int status) {
+  switch (status) {
+    case GRPO_OK: return "GRPO_OK";
+    case GRPO_ERR_ARG: return "GRPO_ERR_ARG: a required pointer is NULL or a scalar is out of range";
+    case GRPO_ERR_SHAPE: return "GRPO_ERR_SHAPE: inconsistent sizes";
+    case GRPO_ERR_DTYPE: return "GRPO_ERR_DTYPE: unsupported dtype";
+    case GRPO_ERR_WORKSPACE: return "GRPO_ERR_WORKSPACE: workspace missing or too small";
+    case GRPO_ERR_ALIGN: return "GRPO_ERR_ALIGN: a device pointer is misaligned";
+    case GRPO_ERR_HIP: return "GRPO_ERR_HIP: a HIP launch failed";
+    default: return "unknown grpo status";
+  }
+}

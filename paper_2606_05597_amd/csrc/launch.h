@@ -1,0 +1,22 @@
+// Launchers shared by the logits path and the fused LM-head path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "grpo.h"
+#include "host.h"
+
+namespace grpo {
+
+// Validates the offsets on the device and writes the per-trajectory tables:
+// first token of each trajectory and its normaliser weight w_i.  Resets the
+// workspace header (flags, counters).  One workgroup.
+hipError_t launch_segments(const grpo_segments* seg, int64_t T, const grpo_loss_params* p, char* ws,
+                           const LossWs& L, int32_t* aux_traj_tok_off, hipStream_t s);
+
+// Reduces the per-token loss contributions: per trajectory, then over
+// trajectories, both in a fixed order; writes loss_out and the aux outputs.
+hipError_t launch_reduce(int64_t T, int32_t n_traj, char* ws, const LossWs& L, double* loss_out,
+                         const grpo_aux* aux, hipStream_t s);
+
+}  // namespace grpo
