@@ -1,0 +1,195 @@
+#!/usr/bin/env python3
+"""Benchmark of the GRPO loss hot path on one MI355X.
+
+A step is one pass of the whole logits path over one batch resident in HBM:
+group advantages (grpo_advantages), then grpo_loss_fwd_bwd (segment pass,
+row pass with dlogits, loss reduction).  Workload: 16 task groups x G = 8
+trajectories, T = 120,000 action tokens, V = 151,936, bf16 logits (the
+realistic-vocabulary rollout batch), synthetic and seeded.
+
+Prints one JSON line.  ``value`` is tokens/s of the whole step.  ``roofline``
+reports the dominant kernel (the row pass): algorithmic bytes per launch,
+T * (4V + 16), over its average duration from HIP events recorded around it
+on its stream; ``traffic`` is the HBM traffic measured with rocprofv3 counters
+(FETCH_SIZE, WRITE_SIZE) scaled by a plain copy's reading, when the committed
+measurement matches the current kernel source, else null.  ``cpu_baseline``
+times the fp64 oracle on the host on a bounded sample of the same batch.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GRPO loss fwd+bwd tokens/s at V=151,936 bf16; % of HBM (or MFMA) roofline"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rows_resident_v152k_traffic.md")
+KERNEL_SOURCES = ["paper_2606_05597_amd/csrc/loss.hip", "paper_2606_05597_amd/csrc/device.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(T: int):
+    """HBM bytes per launch of the row kernel from the committed counter summary, if it is current."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = dict(re.findall(r"^- (\w+): (\S+)", open(TRAFFIC_FILE).read(), re.M))
+    if kv.get("kernel_source_sha256") != kernel_source_hash() or int(kv.get("T", -1)) != T:
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (0 = skip)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain device copy of known size (for counter calibration)")
+    return ap.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 8 << 30  # 8 GiB
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "copies": 2}))
+
+
+def cpu_baseline(b: dict, adv64, budget_s: float) -> dict:
+    """The fp64 oracle on host cores, on the first rows of the same batch, cycled for ~budget_s."""
+    import numpy as np
+    import torch
+
+    import oracle
+    st = b["structure"]
+    R = min(st.T, 16384)
+    zl = b["logits"][:R].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    seg = oracle.segments(st.T, st.step_tok_off, st.traj_step_off)
+    actions = b["actions"].cpu().numpy()
+    behave = b["behave"].cpu().numpy()
+    cfg = b["cfg"]
+    chunk = 256
+    rows = 0
+    t0 = time.perf_counter()
+    r0 = 0
+    while True:
+        r1 = min(R, r0 + chunk)
+        oracle.loss_rows(zl[r0:r1], actions, behave, None, adv64, seg, cfg.G, norm=oracle.NORM_CONST_K, k=cfg.k,
+                         dual_clip_c=3.0, row_begin=r0, row_end=r1, row_offset=r0)
+        rows += r1 - r0
+        r0 = 0 if r1 == R else r1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": rows / el, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"first {R} token rows of the same batch (loss + fp64 dlogits), cycled in blocks of "
+                      f"{chunk}; {rows} rows in {el:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+              "the path shards by whole task groups, see the design notes", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    import numpy as np
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    from synth import make_batch
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    b = make_batch("v152k", dev)
+    cfg, st = b["cfg"], b["structure"]
+    T, V = b["logits"].shape
+    N = len(st.rewards)
+    sto = torch.from_numpy(st.step_tok_off).to(dev)
+    tso = torch.from_numpy(st.traj_step_off).to(dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    dlogits = torch.empty_like(b["logits"])
+    ws = torch.empty(grpo.grpo_loss_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    n_ev = args.steps
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+    for e in ev0 + ev1:
+        e.record(stream)  # creates the underlying hipEvent_t
+    torch.cuda.synchronize()
+
+    def step(i=None):
+        grpo.grpo_advantages(b["rewards"], cfg.G, out=adv)
+        aux = None
+        if i is not None:
+            aux = grpo.LossAux(hot_events=(ev0[i].cuda_event, ev1[i].cuda_event))
+        grpo.grpo_loss_fwd_bwd(b["logits"], b["actions"], b["behave"], adv, sto, tso, cfg.G,
+                               norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, eps_low=0.2, eps_high=0.2, dual_clip_c=3.0,
+                               dlogits=dlogits, aux=aux, workspace=ws, loss_out=loss)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    ms = el * 1e3 / args.steps
+    hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(args.steps)) / args.steps
+    alg_bytes = T * (4.0 * V + 16.0)
+    achieved = alg_bytes / (hot_ms * 1e-3) / 1e9
+    traffic = measured_traffic(T)
+    out = {
+        "metric": METRIC,
+        "value": T / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "v152k: 16 groups x G=8 rollouts, T=120,000 action tokens, V=151,936, bf16 logits",
+                   "T": T, "V": V, "n_traj": N, "n_steps": int(st.step_tok_off.shape[0] - 1),
+                   "normalizer": "1/k (k=10)", "eps": 0.2, "dual_clip_c": 3.0, "loss": float(loss.item())},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_rows_resident<bf16, 1024, 19>", "kernel_ms": hot_ms,
+                     "algorithmic_bytes_per_launch": alg_bytes},
+    }
+    if args.cpu_seconds > 0:
+        import oracle
+        A = oracle.advantages(st.rewards, cfg.G).astype(np.float32).astype(np.float64)
+        del dlogits
+        out["cpu_baseline"] = cpu_baseline(b, A, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -57,8 +57,15 @@ def _load():
         lib.oracle_loss_rows.restype = ctypes.c_int
         lib.oracle_reduce.argtypes = [P, P, I64, I32, P]
         lib.oracle_reduce.restype = D
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's row loop uses."""
+    return int(_load().oracle_threads())
 
 
 def _ptr(a):

@@ -29,6 +29,7 @@
  * when s < c*A strictly.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -250,3 +251,6 @@ double oracle_reduce(const double* token_contrib, const int32_t* tok_traj, int64
   }
   return total;
 }
+
+/* Threads the row loop runs on (for reporting the oracle's timing). */
+int oracle_threads(void) { return omp_get_max_threads(); }

@@ -78,6 +78,32 @@ hipError_t launch_segments(const grpo_segments* seg, int64_t T, const grpo_loss_
   return hipGetLastError();
 }
 
+TokenArgs make_token_args(int64_t V, int64_t ld, const int32_t* actions, const float* behave, const float* prox,
+                          const float* adv, const grpo_segments* seg, const grpo_loss_params* p, char* ws,
+                          const LossWs& L, const grpo_aux* aux) {
+  TokenArgs a;
+  a.V = V;
+  a.ld = ld;
+  a.n_traj = seg->n_traj;
+  a.actions = actions;
+  a.behave = behave;
+  a.prox = prox;
+  a.adv = adv;
+  a.traj_tok_off = reinterpret_cast<const int32_t*>(ws + L.traj_tok_off);
+  a.w = reinterpret_cast<const double*>(ws + L.w);
+  a.hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
+  a.contrib = reinterpret_cast<double*>(ws + L.contrib);
+  a.state = reinterpret_cast<int8_t*>(ws + L.state);
+  a.token_logp = aux ? aux->token_logp : nullptr;
+  a.tok_traj = aux ? aux->tok_traj : nullptr;
+  a.gather_idx = aux ? aux->gather_idx : nullptr;
+  a.lo = 1.0 - (double)p->eps_low;
+  a.hi = 1.0 + (double)p->eps_high;
+  a.c = (double)p->dual_clip_c;
+  a.grad_scale = (double)p->grad_scale;
+  return a;
+}
+
 // ---- reduction -----------------------------------------------------------------
 // One workgroup per trajectory sums its tokens' contributions in a fixed
 // order; the last workgroup to finish sums the trajectories in index order.

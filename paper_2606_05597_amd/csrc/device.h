@@ -8,6 +8,13 @@
 
 namespace grpo {
 
+// Header block at the start of every loss workspace.
+struct WsHeader {
+  int32_t flags;      // GRPO_FLAG_* of this call (set by the segment pass, OR-ed by the row pass)
+  uint32_t done;      // reduction workgroups finished (last-block pattern)
+  int64_t counts[2];  // eps-clip / dual-clip cut counts
+};
+
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr double kLn2 = 0.69314718055994530942;
 
@@ -99,6 +106,73 @@ __device__ __forceinline__ int find_traj(const int32_t* __restrict__ traj_tok_of
     else hi = mid - 1;
   }
   return lo;
+}
+
+// ---- the per-token epilogue shared by the logits and fused paths -------------
+struct TokenArgs {
+  int64_t V, ld;
+  int32_t n_traj;
+  const int32_t* actions;
+  const float* behave;
+  const float* prox;            // nullable: coupled ratio
+  const float* adv;
+  const int32_t* traj_tok_off;  // ws
+  const double* w;              // ws: per-trajectory normaliser weight
+  WsHeader* hdr;                // ws
+  double* contrib;              // ws [T]
+  int8_t* state;                // ws [T]
+  float* token_logp;            // aux, nullable
+  int32_t* tok_traj;            // aux, nullable
+  int64_t* gather_idx;          // aux, nullable
+  double lo, hi, c, grad_scale;
+};
+
+// How the dlogits row is formed: d_v = sign * 2^(z_v*log2e + nc) for v != a_t
+// (nc folds -lse*log2e + log2|g|), and d_a for the action column.  act < 0
+// means the row is zero.
+struct RowScale {
+  float nc, sign, d_a;
+  int act;
+};
+
+// Runs once per token after the row's log-sum-exp is known.  z_a is the
+// action's logit (ignored when the action is out of range).  Writes the
+// token's loss contribution, clip state and optional outputs.
+__device__ inline RowScale token_finish(const TokenArgs& a, int t, int act, double lse, double z_a) {
+  RowScale rs;
+  const int flags = __hip_atomic_load(&a.hdr->flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const bool bad_off = flags & GRPO_FLAG_OFFSETS;
+  const bool bad_act = act < 0 || (int64_t)act >= a.V;
+  const int i = find_traj(a.traj_tok_off, a.n_traj, t);
+  if (a.tok_traj) a.tok_traj[t] = bad_off ? -1 : i;
+  if (a.gather_idx) a.gather_idx[t] = (int64_t)t * a.ld + act;
+  rs.act = act;
+  if (bad_off || bad_act) {
+    if (bad_act && !bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
+    a.contrib[t] = bad_off ? (double)NAN : 0.0;
+    a.state[t] = 0;
+    if (a.token_logp) a.token_logp[t] = 0.f;
+    rs.nc = -INFINITY;  // every d_v = 0
+    rs.sign = 1.f;
+    rs.d_a = 0.f;
+    rs.act = -1;
+    return rs;
+  }
+  const double l = z_a - lse;
+  const double b = (double)a.behave[t];
+  const double p = a.prox ? (double)a.prox[t] : b;
+  const double A = (double)a.adv[i];
+  const TokenOut o = token_surrogate(l, b, p, A, a.w[i], a.lo, a.hi, a.c, a.grad_scale);
+  if (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) atomicOr(&a.hdr->flags, GRPO_FLAG_NONFINITE);
+  a.contrib[t] = o.contrib;
+  a.state[t] = (int8_t)o.state;
+  if (a.token_logp) a.token_logp[t] = (float)l;
+  // d_v = g exp(z_v - lse) = sign(g) 2^(z_v L - lse L + log2|g|), with L = log2(e) as rounded on the device
+  rs.nc = (float)(-lse * (double)kLog2e + log2(fabs(o.g)));
+  rs.sign = (o.g < 0.0) ? -1.f : 1.f;
+  rs.d_a = (float)(o.g * expm1(l));  // g (p_a - 1), without cancellation
+  if (isnan(o.g)) rs.nc = NAN;
+  return rs;
 }
 
 }  // namespace grpo

@@ -6,6 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "device.h"
 #include "grpo.h"
 
 namespace grpo {
@@ -13,13 +14,6 @@ namespace grpo {
 constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
-
-// Header block at the start of every workspace.
-struct WsHeader {
-  int32_t flags;      // GRPO_FLAG_* of this call (set by the segment pass, OR-ed by the row pass)
-  uint32_t done;      // reduction blocks finished (last-block pattern)
-  int64_t counts[2];  // eps-clip / dual-clip cut counts
-};
 
 // Workspace of the loss: per-trajectory and per-token scratch.
 struct LossWs {

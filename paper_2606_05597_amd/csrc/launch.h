@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include "grpo.h"
+#include "device.h"
 #include "host.h"
 
 namespace grpo {
@@ -13,6 +14,11 @@ namespace grpo {
 // workspace header (flags, counters).  One workgroup.
 hipError_t launch_segments(const grpo_segments* seg, int64_t T, const grpo_loss_params* p, char* ws,
                            const LossWs& L, int32_t* aux_traj_tok_off, hipStream_t s);
+
+// The token-epilogue arguments of a loss call (device.h TokenArgs).
+TokenArgs make_token_args(int64_t V, int64_t ld, const int32_t* actions, const float* behave, const float* prox,
+                          const float* adv, const grpo_segments* seg, const grpo_loss_params* p, char* ws,
+                          const LossWs& L, const grpo_aux* aux);
 
 // Reduces the per-token loss contributions: per trajectory, then over
 // trajectories, both in a fixed order; writes loss_out and the aux outputs.

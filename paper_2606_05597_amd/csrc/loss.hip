@@ -16,24 +16,11 @@ namespace grpo {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Row-pass arguments: the logits, the dlogits destination and the token epilogue.
 struct RowArgs {
   const void* logits;
   void* dlogits;  // nullable: forward only
-  int64_t V, ld;
-  int32_t n_traj;
-  const int32_t* actions;
-  const float* behave;
-  const float* prox;  // nullable: coupled
-  const float* adv;
-  const int32_t* traj_tok_off;  // ws
-  const double* w;              // ws
-  WsHeader* hdr;                // ws
-  double* contrib;              // ws [T]
-  int8_t* state;                // ws [T]
-  float* token_logp;            // aux, nullable
-  int32_t* tok_traj;            // aux, nullable
-  int64_t* gather_idx;          // aux, nullable
-  double lo, hi, c, grad_scale;
+  TokenArgs tok;
 };
 
 template <typename Tin>
@@ -43,54 +30,13 @@ __device__ __forceinline__ float load_elem<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
 
-// What the epilogue hands to the dlogits pass: d_v = sign * 2^(z_v*log2e + nc)
-// for v != a_t (nc folds -lse*log2e + log2|g|), and d_a for the action column.
-struct RowScale {
-  float nc, sign, d_a;
-  int act;
-};
-
-// The per-token epilogue, run by one thread once the row's max M and
-// S = sum exp(z - M) are known.  Writes the token outputs and returns the
-// scale of the dlogits row.
+// The epilogue of one row once its max M and S = sum exp(z - M) are known.
 template <typename Tin>
 __device__ RowScale row_epilogue(const RowArgs& a, int t, const Tin* row, double M, double S) {
-  RowScale rs;
-  const int act = a.actions[t];
-  const int flags = __hip_atomic_load(&a.hdr->flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const bool bad_off = flags & GRPO_FLAG_OFFSETS;
-  const bool bad_act = act < 0 || (int64_t)act >= a.V;
-  const int i = find_traj(a.traj_tok_off, a.n_traj, t);
-  if (a.tok_traj) a.tok_traj[t] = bad_off ? -1 : i;
-  if (a.gather_idx) a.gather_idx[t] = (int64_t)t * a.ld + act;
-  rs.act = act;
-  if (bad_off || bad_act) {
-    if (bad_act && !bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
-    a.contrib[t] = bad_off ? (double)NAN : 0.0;
-    a.state[t] = 0;
-    if (a.token_logp) a.token_logp[t] = 0.f;
-    rs.nc = -INFINITY;  // every d_v = 0
-    rs.sign = 1.f;
-    rs.d_a = 0.f;
-    rs.act = -1;
-    return rs;
-  }
-  const double lse = M + log(S);
-  const double l = (double)load_elem<Tin>(row + act) - lse;
-  const double b = (double)a.behave[t];
-  const double p = a.prox ? (double)a.prox[t] : b;
-  const double A = (double)a.adv[i];
-  const TokenOut o = token_surrogate(l, b, p, A, a.w[i], a.lo, a.hi, a.c, a.grad_scale);
-  if (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) atomicOr(&a.hdr->flags, GRPO_FLAG_NONFINITE);
-  a.contrib[t] = o.contrib;
-  a.state[t] = (int8_t)o.state;
-  if (a.token_logp) a.token_logp[t] = (float)l;
-  // d_v = g * exp(z_v - lse) = sign(g) * 2^(z_v*L - lse*L + log2|g|), L = log2(e) as used on the device
-  rs.nc = (float)(-lse * (double)kLog2e + log2(fabs(o.g)));
-  rs.sign = (o.g < 0.0) ? -1.f : 1.f;
-  rs.d_a = (float)(o.g * expm1(l));  // g * (p_a - 1), without cancellation
-  if (isnan(o.g)) rs.nc = NAN;
-  return rs;
+  const int act = a.tok.actions[t];
+  const bool ok = act >= 0 && (int64_t)act < a.tok.V;
+  const double z_a = ok ? (double)load_elem<Tin>(row + act) : 0.0;
+  return token_finish(a.tok, t, act, M + log(S), z_a);
 }
 
 // ---- register-resident row kernel -------------------------------------------
@@ -107,8 +53,8 @@ __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
 
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
-  const int nvec = (int)(a.V / EPV);
-  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld;
+  const int nvec = (int)(a.tok.V / EPV);
+  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.tok.ld;
   const u32x4* src = reinterpret_cast<const u32x4*>(row);
 
   u32x4 buf[NV];
@@ -175,7 +121,7 @@ __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
   const RowScale rs = sh_rs;
   const int act_vec = rs.act >= 0 ? rs.act / EPV : -1;
   const int act_lane = rs.act >= 0 ? rs.act % EPV : 0;
-  u32x4* dst = reinterpret_cast<u32x4*>(static_cast<Tin*>(a.dlogits) + (int64_t)t * a.ld);
+  u32x4* dst = reinterpret_cast<u32x4*>(static_cast<Tin*>(a.dlogits) + (int64_t)t * a.tok.ld);
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int vi = j * NT + tid;
@@ -223,9 +169,9 @@ __global__ __launch_bounds__(256) void k_rows_generic(const RowArgs a) {
   __shared__ double sh_s[NW];
   __shared__ RowScale sh_rs;
   const int t = blockIdx.x, tid = threadIdx.x;
-  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld;
+  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.tok.ld;
   float m = -INFINITY;
-  for (int64_t v = tid; v < a.V; v += NT) m = fmaxf(m, load_elem<Tin>(row + v));
+  for (int64_t v = tid; v < a.tok.V; v += NT) m = fmaxf(m, load_elem<Tin>(row + v));
   const float mw = wave_max(m);
   const int lane = tid & 63, wv = tid >> 6;
   if (lane == 0) sh_m[wv] = mw;
@@ -234,7 +180,7 @@ __global__ __launch_bounds__(256) void k_rows_generic(const RowArgs a) {
   for (int q = 0; q < NW; ++q) M = fmaxf(M, sh_m[q]);
   const float nmb = (M == -INFINITY) ? 0.f : -M * kLog2e;
   double s = 0.0;
-  for (int64_t v = tid; v < a.V; v += NT) s += (double)__builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, nmb));
+  for (int64_t v = tid; v < a.tok.V; v += NT) s += (double)__builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, nmb));
   s = wave_sum(s);
   if (lane == 0) sh_s[wv] = s;
   __syncthreads();
@@ -246,8 +192,8 @@ __global__ __launch_bounds__(256) void k_rows_generic(const RowArgs a) {
   __syncthreads();
   if (!a.dlogits) return;
   const RowScale rs = sh_rs;
-  Tin* drow = static_cast<Tin*>(a.dlogits) + (int64_t)t * a.ld;
-  for (int64_t v = tid; v < a.V; v += NT) {
+  Tin* drow = static_cast<Tin*>(a.dlogits) + (int64_t)t * a.tok.ld;
+  for (int64_t v = tid; v < a.tok.V; v += NT) {
     float d = (v == rs.act) ? rs.d_a : rs.sign * __builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, rs.nc));
     if constexpr (sizeof(Tin) == 2) {
       drow[v] = (uint16_t)(pack_bf16(d, 0.f) & 0xffffu);
@@ -324,25 +270,7 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
     RowArgs a;
     a.logits = logits;
     a.dlogits = dlogits;
-    a.V = V;
-    a.ld = ld;
-    a.n_traj = seg->n_traj;
-    a.actions = actions;
-    a.behave = behave_logp;
-    a.prox = prox_logp;
-    a.adv = adv;
-    a.traj_tok_off = reinterpret_cast<const int32_t*>(w + L.traj_tok_off);
-    a.w = reinterpret_cast<const double*>(w + L.w);
-    a.hdr = reinterpret_cast<WsHeader*>(w + L.hdr);
-    a.contrib = reinterpret_cast<double*>(w + L.contrib);
-    a.state = reinterpret_cast<int8_t*>(w + L.state);
-    a.token_logp = aux ? aux->token_logp : nullptr;
-    a.tok_traj = aux ? aux->tok_traj : nullptr;
-    a.gather_idx = aux ? aux->gather_idx : nullptr;
-    a.lo = 1.0 - (double)p->eps_low;
-    a.hi = 1.0 + (double)p->eps_high;
-    a.c = (double)p->dual_clip_c;
-    a.grad_scale = (double)p->grad_scale;
+    a.tok = make_token_args(V, ld, actions, behave_logp, prox_logp, adv, seg, p, w, L, aux);
     int nt = 256;
     RowKernel k = pick_row_kernel(dt, V, ld, logits, dlogits, &nt);
     const bool timed = aux && aux->hot_begin && aux->hot_end;

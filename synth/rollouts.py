@@ -98,6 +98,8 @@ class Structure:
 
 def _largest_remainder(counts: np.ndarray, total: int) -> np.ndarray:
     """Integer counts (each >= 1) proportional to ``counts`` summing to ``total``."""
+    if total < len(counts):
+        raise ValueError(f"cannot spread {total} tokens over {len(counts)} steps with at least one each")
     x = counts.astype(np.float64) * (total / counts.sum())
     base = np.maximum(1, np.floor(x)).astype(np.int64)
     deficit = total - int(base.sum())
