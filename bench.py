@@ -7,6 +7,11 @@ row pass with dlogits, loss reduction).  Workload: 16 task groups x G = 8
 trajectories, T = 120,000 action tokens, V = 151,936, bf16 logits (the
 realistic-vocabulary rollout batch), synthetic and seeded.
 
+The fused LM-head path is measured in the same run on its own workload
+(hidden bf16 [65,536, 3,584], W bf16 [3,584, 151,936], vocabulary chunks of
+8192) and reported under "fused_lmhead" against the bf16 dense MFMA peak, with
+the algorithmic work of three products (6 T H V flop) and the four executed.
+
 Prints one JSON line.  ``value`` is tokens/s of the whole step.  ``roofline``
 reports the dominant kernel (the row pass): algorithmic bytes per launch,
 T * (4V + 16), over its average duration from HIP events recorded around it
@@ -30,6 +35,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "GRPO loss fwd+bwd tokens/s at V=151,936 bf16; % of HBM (or MFMA) roofline"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rows_resident_v152k_traffic.md")
 KERNEL_SOURCES = ["paper_2606_05597_amd/csrc/loss.hip", "paper_2606_05597_amd/csrc/device.h"]
 
@@ -58,6 +64,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (0 = skip)")
+    ap.add_argument("--fused-steps", type=int, default=3, help="timed steps of the fused path (0 = skip)")
+    ap.add_argument("--skip-logits", action="store_true", help="measure only the fused path")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter calibration)")
     return ap.parse_args()
@@ -105,6 +113,60 @@ def cpu_baseline(b: dict, adv64, budget_s: float) -> dict:
                       f"{chunk}; {rows} rows in {el:.1f} s"}
 
 
+def bench_fused(steps: int, warmup: int = 1) -> dict:
+    """Times fused_lmhead_grpo on the fused workload; the hot region is pass 1 through pass 2."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    from synth import make_fused_batch
+
+    dev = torch.device("cuda:0")
+    b = make_fused_batch("fused", dev)
+    cfg, st = b["cfg"], b["structure"]
+    T, H, V = st.T, b["H"], b["V"]
+    N = len(st.rewards)
+    sto = torch.from_numpy(st.step_tok_off).to(dev)
+    tso = torch.from_numpy(st.traj_step_off).to(dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    dh = torch.empty_like(b["hidden"])
+    dw = torch.empty((H, V), dtype=torch.float32, device=dev)
+    ws = torch.empty(grpo.fused_lmhead_workspace_bytes(T, H, V, cfg.vocab_chunk, N), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for e in ev0 + ev1:
+        e.record(stream)
+    torch.cuda.synchronize()
+
+    def step(i=None):
+        grpo.grpo_advantages(b["rewards"], cfg.G, out=adv)
+        aux = None if i is None else grpo.LossAux(hot_events=(ev0[i].cuda_event, ev1[i].cuda_event))
+        grpo.fused_lmhead_grpo(b["hidden"], b["W"], b["actions"], b["behave"], adv, sto, tso, cfg.G,
+                               vocab_chunk=cfg.vocab_chunk, norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, dual_clip_c=3.0,
+                               dhidden=dh, dw_lm=dw, aux=aux, workspace=ws, loss_out=loss)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(steps)) / steps
+    alg = 6.0 * T * H * V
+    achieved = alg / (hot_ms * 1e-3) / 1e12
+    return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
+            "workload": f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], chunks of {cfg.vocab_chunk}, "
+                        f"{cfg.n_groups} groups x G={cfg.G}",
+            "loss": float(loss.item()),
+            "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "hot_ms": hot_ms,
+                         "algorithmic_flop_per_launch": alg,
+                         "executed_frac": (8.0 * T * H * V) / (hot_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -113,6 +175,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.skip_logits:
+        print(json.dumps({"fused_lmhead": bench_fused(max(1, args.fused_steps))}), flush=True)
         return
     import numpy as np
     import torch
@@ -180,14 +245,18 @@ def main():
                    "normalizer": "1/k (k=10)", "eps": 0.2, "dual_clip_c": 3.0, "loss": float(loss.item())},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_rows_resident<bf16, 1024, 19>", "kernel_ms": hot_ms,
+                     "kernel": "k_rows_pipe<19, 9> (bf16, 1024 threads, one workgroup per CU)", "kernel_ms": hot_ms,
                      "algorithmic_bytes_per_launch": alg_bytes},
     }
+    del dlogits
     if args.cpu_seconds > 0:
         import oracle
         A = oracle.advantages(st.rewards, cfg.G).astype(np.float32).astype(np.float64)
-        del dlogits
         out["cpu_baseline"] = cpu_baseline(b, A, args.cpu_seconds)
+    if args.fused_steps > 0:
+        del b
+        torch.cuda.empty_cache()
+        out["fused_lmhead"] = bench_fused(args.fused_steps)
     print(json.dumps(out), flush=True)
 
 

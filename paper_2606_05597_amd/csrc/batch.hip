@@ -58,8 +58,27 @@ __global__ __launch_bounds__(256) void k_segments(const SegArgs a) {
   }
 }
 
-hipError_t launch_segments(const grpo_segments* seg, int64_t T, const grpo_loss_params* p, char* ws,
-                           const LossWs& L, int32_t* aux_traj_tok_off, hipStream_t s) {
+// The trajectory of every token, found by binary search over the trajectory
+// starts, and what the token epilogue needs from it (advantage, normaliser
+// weight), so that the row passes read per-token values only.  Also the
+// optional token outputs that need no logits.  One thread per token.
+__global__ __launch_bounds__(256) void k_tok_traj(int64_t T, int32_t n_traj, const int32_t* traj_tok_off,
+                                                  const WsHeader* hdr, const int32_t* actions, int64_t ld,
+                                                  const float* adv, const double* w, float* tok_adv, double* tok_w,
+                                                  int32_t* aux_tok_traj, int64_t* aux_gather) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  const int i = find_traj(traj_tok_off, n_traj, (int)t);
+  tok_adv[t] = adv[i];
+  tok_w[t] = w[i];
+  if (aux_tok_traj) aux_tok_traj[t] = (hdr->flags & GRPO_FLAG_OFFSETS) ? -1 : i;
+  if (aux_gather) aux_gather[t] = t * ld + actions[t];
+}
+
+hipError_t launch_segments(const grpo_segments* seg, int64_t T, int64_t ld, const int32_t* actions,
+                           const float* adv, const grpo_loss_params* p, char* ws, const LossWs& L,
+                           const grpo_aux* aux, hipStream_t s) {
+  int32_t* aux_traj_tok_off = aux ? aux->traj_tok_off : nullptr;
   SegArgs a;
   a.sto = seg->step_tok_off;
   a.tso = seg->traj_step_off;
@@ -75,28 +94,28 @@ hipError_t launch_segments(const grpo_segments* seg, int64_t T, const grpo_loss_
   a.w = reinterpret_cast<double*>(ws + L.w);
   a.aux_traj_tok_off = aux_traj_tok_off;
   hipLaunchKernelGGL(k_segments, dim3(1), dim3(256), 0, s, a);
+  if (T > 0)
+    hipLaunchKernelGGL(k_tok_traj, dim3((unsigned)((T + 255) / 256)), dim3(256), 0, s, T, seg->n_traj,
+                       a.traj_tok_off, a.hdr, actions, ld, adv, a.w, reinterpret_cast<float*>(ws + L.tok_adv),
+                       reinterpret_cast<double*>(ws + L.tok_w), aux ? aux->tok_traj : nullptr,
+                       aux ? aux->gather_idx : nullptr);
   return hipGetLastError();
 }
 
-TokenArgs make_token_args(int64_t V, int64_t ld, const int32_t* actions, const float* behave, const float* prox,
-                          const float* adv, const grpo_segments* seg, const grpo_loss_params* p, char* ws,
-                          const LossWs& L, const grpo_aux* aux) {
+TokenArgs make_token_args(int64_t V, const int32_t* actions, const float* behave, const float* prox,
+                          const float* adv, const grpo_loss_params* p, char* ws, const LossWs& L,
+                          const grpo_aux* aux) {
   TokenArgs a;
   a.V = V;
-  a.ld = ld;
-  a.n_traj = seg->n_traj;
   a.actions = actions;
   a.behave = behave;
   a.prox = prox;
-  a.adv = adv;
-  a.traj_tok_off = reinterpret_cast<const int32_t*>(ws + L.traj_tok_off);
-  a.w = reinterpret_cast<const double*>(ws + L.w);
+  a.tok_adv = reinterpret_cast<const float*>(ws + L.tok_adv);
+  a.tok_w = reinterpret_cast<const double*>(ws + L.tok_w);
   a.hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   a.contrib = reinterpret_cast<double*>(ws + L.contrib);
   a.state = reinterpret_cast<int8_t*>(ws + L.state);
   a.token_logp = aux ? aux->token_logp : nullptr;
-  a.tok_traj = aux ? aux->tok_traj : nullptr;
-  a.gather_idx = aux ? aux->gather_idx : nullptr;
   a.lo = 1.0 - (double)p->eps_low;
   a.hi = 1.0 + (double)p->eps_high;
   a.c = (double)p->dual_clip_c;

@@ -67,9 +67,11 @@ struct TokenOut {
 // rho*A except when the clip (or the dual-clip floor) holds the term fixed.
 __device__ __forceinline__ TokenOut token_surrogate(double l, double b, double p, double A, double w,
                                                     double lo, double hi, double c, double grad_scale) {
-  const double rho = exp(l - b);    // pi / pi_behave
-  const double r = exp(l - p);      // pi / pi_prox
-  const double omega = exp(p - b);  // pi_prox / pi_behave
+  // rho = pi / pi_behave, r = pi / pi_prox, omega = pi_prox / pi_behave; with
+  // pi_prox = pi_behave (the coupled ratio) omega = 1 and r = rho exactly.
+  const double rho = exp(l - b);
+  const double r = (p == b) ? rho : exp(l - p);
+  const double omega = (p == b) ? 1.0 : exp(p - b);
   const bool inside = (r >= lo) && (r <= hi);
   const double r_cl = fmin(fmax(r, lo), hi);
   const double u1 = rho * A;
@@ -110,22 +112,37 @@ __device__ __forceinline__ int find_traj(const int32_t* __restrict__ traj_tok_of
 
 // ---- the per-token epilogue shared by the logits and fused paths -------------
 struct TokenArgs {
-  int64_t V, ld;
-  int32_t n_traj;
+  int64_t V;
   const int32_t* actions;
   const float* behave;
-  const float* prox;            // nullable: coupled ratio
-  const float* adv;
-  const int32_t* traj_tok_off;  // ws
-  const double* w;              // ws: per-trajectory normaliser weight
-  WsHeader* hdr;                // ws
-  double* contrib;              // ws [T]
-  int8_t* state;                // ws [T]
-  float* token_logp;            // aux, nullable
-  int32_t* tok_traj;            // aux, nullable
-  int64_t* gather_idx;          // aux, nullable
+  const float* prox;        // nullable: coupled ratio
+  const float* tok_adv;     // ws [T]: advantage of each token's trajectory (segment pass)
+  const double* tok_w;      // ws [T]: normaliser weight of each token's trajectory
+  WsHeader* hdr;            // ws
+  double* contrib;          // ws [T]
+  int8_t* state;            // ws [T]
+  float* token_logp;        // aux, nullable
   double lo, hi, c, grad_scale;
 };
+
+// The per-token inputs of the epilogue.  Every address depends only on t, so
+// a workgroup can issue these loads long before it needs them.
+struct TokenIn {
+  int act, bad_off;
+  float b, p, A;
+  double w;
+};
+
+__device__ __forceinline__ TokenIn token_load(const TokenArgs& a, int t) {
+  TokenIn in;
+  in.act = a.actions[t];
+  in.bad_off = a.hdr->flags & GRPO_FLAG_OFFSETS;  // final before any row pass starts
+  in.b = a.behave[t];
+  in.p = a.prox ? a.prox[t] : in.b;
+  in.A = a.tok_adv[t];
+  in.w = a.tok_w[t];
+  return in;
+}
 
 // How the dlogits row is formed: d_v = sign * 2^(z_v*log2e + nc) for v != a_t
 // (nc folds -lse*log2e + log2|g|), and d_a for the action column.  act < 0
@@ -137,19 +154,14 @@ struct RowScale {
 
 // Runs once per token after the row's log-sum-exp is known.  z_a is the
 // action's logit (ignored when the action is out of range).  Writes the
-// token's loss contribution, clip state and optional outputs.
-__device__ inline RowScale token_finish(const TokenArgs& a, int t, int act, double lse, double z_a) {
+// token's loss contribution, clip state and log-prob.
+__device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn& in, double lse, double z_a) {
   RowScale rs;
-  const int flags = __hip_atomic_load(&a.hdr->flags, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const bool bad_off = flags & GRPO_FLAG_OFFSETS;
-  const bool bad_act = act < 0 || (int64_t)act >= a.V;
-  const int i = find_traj(a.traj_tok_off, a.n_traj, t);
-  if (a.tok_traj) a.tok_traj[t] = bad_off ? -1 : i;
-  if (a.gather_idx) a.gather_idx[t] = (int64_t)t * a.ld + act;
-  rs.act = act;
-  if (bad_off || bad_act) {
-    if (bad_act && !bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
-    a.contrib[t] = bad_off ? (double)NAN : 0.0;
+  const bool bad_act = in.act < 0 || (int64_t)in.act >= a.V;
+  rs.act = in.act;
+  if (in.bad_off || bad_act) {
+    if (bad_act && !in.bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
+    a.contrib[t] = in.bad_off ? (double)NAN : 0.0;
     a.state[t] = 0;
     if (a.token_logp) a.token_logp[t] = 0.f;
     rs.nc = -INFINITY;  // every d_v = 0
@@ -159,10 +171,8 @@ __device__ inline RowScale token_finish(const TokenArgs& a, int t, int act, doub
     return rs;
   }
   const double l = z_a - lse;
-  const double b = (double)a.behave[t];
-  const double p = a.prox ? (double)a.prox[t] : b;
-  const double A = (double)a.adv[i];
-  const TokenOut o = token_surrogate(l, b, p, A, a.w[i], a.lo, a.hi, a.c, a.grad_scale);
+  const double b = (double)in.b, p = (double)in.p, A = (double)in.A;
+  const TokenOut o = token_surrogate(l, b, p, A, in.w, a.lo, a.hi, a.c, a.grad_scale);
   if (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) atomicOr(&a.hdr->flags, GRPO_FLAG_NONFINITE);
   a.contrib[t] = o.contrib;
   a.state[t] = (int8_t)o.state;

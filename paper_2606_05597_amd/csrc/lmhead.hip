@@ -192,9 +192,9 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   __syncthreads();
   if (tid == 0) {
     const double S = sh_s[0] + sh_s[1] + sh_s[2] + sh_s[3];
-    const int act = a.tok.actions[t];
-    const bool ok = act >= 0 && (int64_t)act < a.tok.V;
-    a.rs[t] = token_finish(a.tok, t, act, (double)M + log(S), ok ? (double)a.za[t] : 0.0);
+    const TokenIn in = token_load(a.tok, t);
+    const bool ok = in.act >= 0 && (int64_t)in.act < a.tok.V;
+    a.rs[t] = token_finish(a.tok, t, in, (double)M + log(S), ok ? (double)a.za[t] : 0.0);
   }
 }
 
@@ -407,7 +407,7 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   const int C = vocab_chunk;
   const int Tp = (int)L.Tp;
 
-  if (launch_segments(seg, T, p, w, L.loss, aux ? aux->traj_tok_off : nullptr, s) != hipSuccess) return GRPO_ERR_HIP;
+  if (launch_segments(seg, T, V, actions, adv, p, w, L.loss, aux, s) != hipSuccess) return GRPO_ERR_HIP;
   if (T == 0) {
     if (!accumulate_dw) hipLaunchKernelGGL(k_fill_f32, dim3(1024), dim3(256), 0, s, dw_lm, H * V, 0.f);
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
@@ -432,7 +432,7 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   hipLaunchKernelGGL(k_lm_partial, grid2(V, T), dim3(GEMM_NT), 0, s, pa);
   // combine
   CombineArgs ca;
-  ca.tok = make_token_args(V, V, actions, behave_logp, prox_logp, adv, seg, p, w, L.loss, aux);
+  ca.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
   ca.part = part;
   ca.za = za;
   ca.rs = rs;

@@ -1,11 +1,17 @@
 // The logits path: streaming log-softmax + gather, the per-token surrogate of
 // Eq. 1 (dual clip of Eq. 2), and dlogits, one workgroup per token row.
 //
-// Hot kernel (k_rows_resident): the row is read from HBM exactly once into
-// registers with 16-byte loads (the wavefront covers 1 KiB contiguous per
-// instruction), reduced to (max, sum exp) per thread, combined across the
-// workgroup, and dlogits are formed from the same registers and written once.
-// Bytes per token: V*s read + V*s written + a few scalars.
+// Every row is read from HBM once with 16-byte loads (a wavefront covers 1 KiB
+// contiguous per instruction), reduced to (max, sum exp) per thread, combined
+// across the workgroup, and dlogits are formed from the same registers and
+// written once: V*s bytes read and V*s written per token.
+//
+//  k_rows_pipe      long bf16 rows (V up to 155,648): persistent, one
+//                   workgroup of 1024 threads per CU.  Row t+G streams in
+//                   while row t's dlogits are written: part of each row lives
+//                   in LDS (global_load_lds), the rest in registers.
+//  k_rows_resident  shorter rows: one workgroup per row, several per CU.
+//  k_rows_generic   any V, stride or alignment: element loads, three sweeps.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -20,6 +26,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 struct RowArgs {
   const void* logits;
   void* dlogits;  // nullable: forward only
+  int64_t ld;     // row stride in elements
+  int T;
   TokenArgs tok;
 };
 
@@ -30,13 +38,246 @@ __device__ __forceinline__ float load_elem<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
 
-// The epilogue of one row once its max M and S = sum exp(z - M) are known.
+// Element e of a 16-byte vector (8 bf16 or 4 fp32), widened to fp32.
 template <typename Tin>
-__device__ RowScale row_epilogue(const RowArgs& a, int t, const Tin* row, double M, double S) {
-  const int act = a.tok.actions[t];
-  const bool ok = act >= 0 && (int64_t)act < a.tok.V;
-  const double z_a = ok ? (double)load_elem<Tin>(row + act) : 0.0;
-  return token_finish(a.tok, t, act, M + log(S), z_a);
+__device__ __forceinline__ float vec_elem(const u32x4& x, int e) {
+  if constexpr (sizeof(Tin) == 2) {
+    uint32_t w = x[0];
+#pragma unroll
+    for (int q = 1; q < 4; ++q)
+      if ((e >> 1) == q) w = x[q];
+    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+  } else {
+    uint32_t w = x[0];
+#pragma unroll
+    for (int q = 1; q < 4; ++q)
+      if (e == q) w = x[q];
+    return __uint_as_float(w);
+  }
+}
+
+// Upper bound of the vector's elements, good enough as the exp shift: the
+// high bf16 of each dword is read with the low one's bits as extra mantissa
+// (within one bf16 ulp), saving the unpack.
+template <typename Tin>
+__device__ __forceinline__ float vec_max(const u32x4& x, float m) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if constexpr (sizeof(Tin) == 2) m = fmaxf(m, fmaxf(__uint_as_float(x[q]), bf16_lo(x[q])));
+    else m = fmaxf(m, __uint_as_float(x[q]));
+  }
+  return m;
+}
+
+// sum of exp(z - m) over the vector, with nmb = -m*log2(e)
+template <typename Tin>
+__device__ __forceinline__ float vec_sumexp(const u32x4& x, float nmb) {
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if constexpr (sizeof(Tin) == 2) {
+      s += __builtin_amdgcn_exp2f(fmaf(bf16_lo(x[q]), kLog2e, nmb)) +
+           __builtin_amdgcn_exp2f(fmaf(bf16_hi(x[q]), kLog2e, nmb));
+    } else {
+      s += __builtin_amdgcn_exp2f(fmaf(__uint_as_float(x[q]), kLog2e, nmb));
+    }
+  }
+  return s;
+}
+
+// dlogits of one vector: |d_v| = 2^(z_v*log2e + nc), the row's sign applied to
+// the packed result, and the action column (when it falls in this vector)
+// replaced by d_a.
+template <typename Tin>
+__device__ __forceinline__ u32x4 vec_dlogits(const u32x4& x, const RowScale& rs, uint32_t signmask, bool has_act,
+                                             int act_lane) {
+  u32x4 o;
+  if constexpr (sizeof(Tin) == 2) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float lo = __builtin_amdgcn_exp2f(fmaf(bf16_lo(x[q]), kLog2e, rs.nc));
+      const float hi = __builtin_amdgcn_exp2f(fmaf(bf16_hi(x[q]), kLog2e, rs.nc));
+      o[q] = pack_bf16(lo, hi) ^ signmask;
+    }
+    if (has_act) {
+      const uint32_t da = pack_bf16(rs.d_a, 0.f) & 0xffffu;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((act_lane >> 1) == q) o[q] = (act_lane & 1) ? ((o[q] & 0xffffu) | (da << 16)) : ((o[q] & 0xffff0000u) | da);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      o[q] = __float_as_uint(__builtin_amdgcn_exp2f(fmaf(__uint_as_float(x[q]), kLog2e, rs.nc))) ^ signmask;
+    if (has_act) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (act_lane == q) o[q] = __float_as_uint(rs.d_a);
+    }
+  }
+  return o;
+}
+
+template <typename Tin>
+__device__ __forceinline__ uint32_t sign_mask(const RowScale& rs) {
+  if (rs.sign >= 0.f) return 0u;
+  return sizeof(Tin) == 2 ? 0x80008000u : 0x80000000u;
+}
+
+// Combines every thread's (max m, sum s of exp(z - m)) into the row's (M, S),
+// valid in thread 0: within each wave, then across the NW waves by the lanes of
+// wave 0, one wave partial per lane.  The rescale factors exp(m - M) <= 1 are
+// fp32 and the sums fp64.  Ends with every wave past a barrier.
+template <int NW>
+__device__ __forceinline__ void block_combine(float m, float s, float* sh_m, double* sh_s, double& M_out,
+                                              double& S_out) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const float mw = wave_max(m);
+  const double sw =
+      wave_sum((m == -INFINITY) ? 0.0 : (double)s * (double)__builtin_amdgcn_exp2f((m - mw) * kLog2e));
+  if (lane == 0) {
+    sh_m[wv] = mw;
+    sh_s[wv] = sw;
+  }
+  __syncthreads();
+  if (wv == 0) {
+    const float mq = lane < NW ? sh_m[lane] : -INFINITY;
+    const float M = wave_max(mq);
+    const double S =
+        wave_sum(mq == -INFINITY ? 0.0 : sh_s[lane < NW ? lane : 0] * (double)__builtin_amdgcn_exp2f((mq - M) * kLog2e));
+    M_out = (double)M;
+    S_out = S;
+  }
+}
+
+// ---- persistent pipelined kernel for long bf16 rows ----------------------------
+// Buffer resources cover exactly one row (V*2 bytes): every access is a 32-bit
+// lane offset (tid*16) plus a constant per-vector offset, and the hardware
+// range check returns 0 for loads past the row and drops such stores.
+constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format
+constexpr int kStream = 2;                    // non-temporal cache policy for streamed rows
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRsrcWord3);
+}
+
+// Hides the register vectors' values from the optimiser, so that the widened
+// bf16 of one pass is recomputed in the next instead of kept live across it.
+template <int N>
+__device__ __forceinline__ void fresh(u32x4 (&v)[N]) {
+#pragma unroll
+  for (int q = 0; q < N; ++q) asm volatile("" : "+v"(v[q]));
+}
+
+// Each thread owns NV vectors of 8 bf16, with (NV-1)*1024 < V/8 <= NV*1024 so
+// that only the last vector can be partial.  The first NP live in LDS (staged
+// with buffer loads straight to LDS and read back in every pass), the other
+// NR = NV - NP in registers.  Once the row's lse is known, dlogits are written
+// first for the LDS part, which is then re-staged with the next row, and then
+// for the register part, each register being reloaded with the next row's
+// vector as soon as its dlogits are stored.
+template <int NV, int NP>
+__global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
+  constexpr int NT = 1024, NW = NT / 64, NR = NV - NP, VB = NT * 16;  // VB: bytes per vector slot
+  __shared__ __attribute__((aligned(16))) u32x4 stage[NP * NT];
+  __shared__ float sh_m[NW];
+  __shared__ double sh_s[NW];
+  __shared__ float sh_za;
+  __shared__ RowScale sh_rs;
+  const int wv = threadIdx.x >> 6;
+  const int nvec = (int)(a.tok.V / 8);
+  const int row_bytes = nvec * 16;
+  const uint16_t* logits = static_cast<const uint16_t*>(a.logits);
+  uint16_t* dlogits = static_cast<uint16_t*>(a.dlogits);
+
+  auto stage_row = [&](int r, int voff) {  // vectors 0..NP-1 of row r -> LDS, asynchronously
+    const __amdgpu_buffer_rsrc_t src = row_rsrc(logits + (int64_t)r * a.ld, row_bytes);
+#pragma unroll
+    for (int j = 0; j < NP; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (__attribute__((address_space(3))) void*)(stage + j * NT + wv * 64),
+                                               16, voff, j * VB, 0, kStream);
+  };
+  auto load_regs = [&](u32x4 (&dst)[NR], int r, int voff) {
+    const __amdgpu_buffer_rsrc_t src = row_rsrc(logits + (int64_t)r * a.ld, row_bytes);
+#pragma unroll
+    for (int q = 0; q < NR; ++q) dst[q] = __builtin_amdgcn_raw_buffer_load_b128(src, voff, (NP + q) * VB, kStream);
+  };
+
+  int t = blockIdx.x;
+  if (t >= a.T) return;
+  u32x4 reg[NR];
+  stage_row(t, threadIdx.x * 16);
+  load_regs(reg, t, threadIdx.x * 16);
+  TokenIn in = token_load(a.tok, t);
+
+  for (; t < a.T; t += gridDim.x) {
+    // The thread index is laundered per row so that nothing derived from it
+    // is hoisted out of the row loop and kept live across it.
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int voff = tid * 16;
+    const bool last_full = tid < nvec - (NV - 1) * NT;
+    const int tn = t + gridDim.x;
+    const int act_vec = (in.act >= 0 && in.act < a.tok.V) ? in.act / 8 : -1;
+    const int act_lane = in.act & 7;
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's loads of row t have landed
+    __syncthreads();                     // ... and every wave's LDS staging
+
+    float m = -INFINITY;
+#pragma unroll 1
+    for (int j = 0; j < NP; ++j) {
+      const u32x4 x = stage[j * NT + tid];
+      m = vec_max<uint16_t>(x, m);
+      if (j * NT + tid == act_vec) sh_za = vec_elem<uint16_t>(x, act_lane);
+    }
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+      const int j = NP + q;
+      if (j < NV - 1 || last_full) {
+        m = vec_max<uint16_t>(reg[q], m);
+        if (j * NT + tid == act_vec) sh_za = vec_elem<uint16_t>(reg[q], act_lane);
+      }
+    }
+    const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
+    float s = 0.f;
+    fresh(reg);
+#pragma unroll 1
+    for (int j = 0; j < NP; ++j) s += vec_sumexp<uint16_t>(stage[j * NT + tid], nmb);
+#pragma unroll
+    for (int q = 0; q < NR; ++q)
+      if (NP + q < NV - 1 || last_full) s += vec_sumexp<uint16_t>(reg[q], nmb);
+
+    double M, S;
+    block_combine<NW>(m, s, sh_m, sh_s, M, S);  // barrier: sh_za is visible
+    if (tid == 0) sh_rs = token_finish(a.tok, t, in, M + log(S), (double)sh_za);
+    __syncthreads();
+
+    const RowScale rs = sh_rs;
+    const uint32_t smask = sign_mask<uint16_t>(rs);
+    const int act_v = rs.act >= 0 ? rs.act / 8 : -1;
+    fresh(reg);
+    // forward only: a zero-sized destination, so the range check drops every store
+    const bool write = dlogits != nullptr;
+    const __amdgpu_buffer_rsrc_t dst = row_rsrc(write ? dlogits + (int64_t)t * a.ld : logits, write ? row_bytes : 0);
+#pragma unroll 1
+    for (int j = 0; j < NP; ++j)
+      __builtin_amdgcn_raw_buffer_store_b128(
+          vec_dlogits<uint16_t>(stage[j * NT + tid], rs, smask, j * NT + tid == act_v, rs.act & 7), dst, voff, j * VB,
+          kStream);
+    __syncthreads();  // every wave is done with stage[]
+    if (tn < a.T) stage_row(tn, voff);
+    const TokenIn in_next = token_load(a.tok, tn < a.T ? tn : t);  // lands during the register part
+    // past the last row: a zero-sized source, every load returns 0
+    const __amdgpu_buffer_rsrc_t nxt = row_rsrc(logits + (int64_t)(tn < a.T ? tn : t) * a.ld, tn < a.T ? row_bytes : 0);
+#pragma unroll
+    for (int q = 0; q < NR; ++q) {
+      const int j = NP + q;
+      __builtin_amdgcn_raw_buffer_store_b128(
+          vec_dlogits<uint16_t>(reg[q], rs, smask, j * NT + tid == act_v, rs.act & 7), dst, voff, j * VB, kStream);
+      reg[q] = __builtin_amdgcn_raw_buffer_load_b128(nxt, voff, j * VB, kStream);
+    }
+    in = in_next;
+  }
 }
 
 // ---- register-resident row kernel -------------------------------------------
@@ -46,16 +287,18 @@ template <typename Tin, int NT, int NV>
 __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
   constexpr int EPV = 16 / sizeof(Tin);  // elements per vector: 8 bf16 or 4 fp32
   constexpr int NW = NT / 64;
-  constexpr bool kBF16 = sizeof(Tin) == 2;
   __shared__ float sh_m[NW];
   __shared__ double sh_s[NW];
+  __shared__ float sh_za;
   __shared__ RowScale sh_rs;
 
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
   const int nvec = (int)(a.tok.V / EPV);
-  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.tok.ld;
-  const u32x4* src = reinterpret_cast<const u32x4*>(row);
+  const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld);
+  const TokenIn in = token_load(a.tok, t);
+  const int act_vec = (in.act >= 0 && in.act < a.tok.V) ? in.act / EPV : -1;
+  const int act_lane = in.act % EPV;
 
   u32x4 buf[NV];
 #pragma unroll
@@ -63,105 +306,43 @@ __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
     const int vi = j * NT + tid;
     if (vi < nvec) buf[j] = __builtin_nontemporal_load(src + vi);
   }
-
-  // pass A: this thread's max
   float m = -INFINITY;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    if (j * NT + tid < nvec) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if constexpr (kBF16) m = fmaxf(m, fmaxf(bf16_hi(buf[j][q]), bf16_lo(buf[j][q])));
-        else m = fmaxf(m, __uint_as_float(buf[j][q]));
-      }
-    }
-  }
-  // pass B: this thread's sum of exp(z - m)
-  const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
-  float s = 0.f;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    if (j * NT + tid < nvec) {
-      float part = 0.f;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if constexpr (kBF16) {
-          part += __builtin_amdgcn_exp2f(fmaf(bf16_lo(buf[j][q]), kLog2e, nmb)) +
-                  __builtin_amdgcn_exp2f(fmaf(bf16_hi(buf[j][q]), kLog2e, nmb));
-        } else {
-          part += __builtin_amdgcn_exp2f(fmaf(__uint_as_float(buf[j][q]), kLog2e, nmb));
-        }
-      }
-      s += part;
-    }
-  }
-  // combine (m, s) over the wave, then over the workgroup
-  const float mw = wave_max(m);
-  const double sw = wave_sum((m == -INFINITY) ? 0.0 : (double)s * exp2((double)((m - mw) * kLog2e)));
-  const int lane = tid & 63, wv = tid >> 6;
-  if (lane == 0) {
-    sh_m[wv] = mw;
-    sh_s[wv] = sw;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    float M = -INFINITY;
-#pragma unroll
-    for (int q = 0; q < NW; ++q) M = fmaxf(M, sh_m[q]);
-    double S = 0.0;
-#pragma unroll
-    for (int q = 0; q < NW; ++q)
-      if (sh_m[q] != -INFINITY) S += sh_s[q] * exp((double)sh_m[q] - (double)M);
-    sh_rs = row_epilogue<Tin>(a, t, row, (double)M, S);
-  }
-  __syncthreads();
-  if (!a.dlogits) return;
-
-  // pass C: dlogits from the registers, written once
-  const RowScale rs = sh_rs;
-  const int act_vec = rs.act >= 0 ? rs.act / EPV : -1;
-  const int act_lane = rs.act >= 0 ? rs.act % EPV : 0;
-  u32x4* dst = reinterpret_cast<u32x4*>(static_cast<Tin*>(a.dlogits) + (int64_t)t * a.tok.ld);
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int vi = j * NT + tid;
     if (vi < nvec) {
-      u32x4 o;
-      if constexpr (kBF16) {
-        float d[8];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          d[2 * q] = rs.sign * __builtin_amdgcn_exp2f(fmaf(bf16_lo(buf[j][q]), kLog2e, rs.nc));
-          d[2 * q + 1] = rs.sign * __builtin_amdgcn_exp2f(fmaf(bf16_hi(buf[j][q]), kLog2e, rs.nc));
-        }
-        if (vi == act_vec) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e == act_lane) d[e] = rs.d_a;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = pack_bf16(d[2 * q], d[2 * q + 1]);
-      } else {
-        float d[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          d[q] = rs.sign * __builtin_amdgcn_exp2f(fmaf(__uint_as_float(buf[j][q]), kLog2e, rs.nc));
-        if (vi == act_vec) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (e == act_lane) d[e] = rs.d_a;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = __float_as_uint(d[q]);
-      }
-      __builtin_nontemporal_store(o, dst + vi);
+      m = vec_max<Tin>(buf[j], m);
+      if (vi == act_vec) sh_za = vec_elem<Tin>(buf[j], act_lane);
     }
+  }
+  const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+    if (j * NT + tid < nvec) s += vec_sumexp<Tin>(buf[j], nmb);
+
+  double M, S;
+  block_combine<NW>(m, s, sh_m, sh_s, M, S);
+  if (tid == 0) sh_rs = token_finish(a.tok, t, in, M + log(S), (double)sh_za);
+  __syncthreads();
+  if (!a.dlogits) return;
+
+  const RowScale rs = sh_rs;
+  const uint32_t smask = sign_mask<Tin>(rs);
+  u32x4* dst = reinterpret_cast<u32x4*>(static_cast<Tin*>(a.dlogits) + (int64_t)t * a.ld);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int vi = j * NT + tid;
+    if (vi < nvec)
+      __builtin_nontemporal_store(vec_dlogits<Tin>(buf[j], rs, smask, vi == rs.act / EPV && rs.act >= 0,
+                                                   rs.act % EPV),
+                                  dst + vi);
   }
 }
 
 // ---- generic row kernel ------------------------------------------------------
 // Any V, ld and element alignment: element-wise loads, the row read three
-// times (max, sum, dlogits).  Used when the resident kernel does not apply.
+// times (max, sum, dlogits).  Used when the vector kernels do not apply.
 template <typename Tin>
 __global__ __launch_bounds__(256) void k_rows_generic(const RowArgs a) {
   constexpr int NT = 256, NW = NT / 64;
@@ -169,32 +350,26 @@ __global__ __launch_bounds__(256) void k_rows_generic(const RowArgs a) {
   __shared__ double sh_s[NW];
   __shared__ RowScale sh_rs;
   const int t = blockIdx.x, tid = threadIdx.x;
-  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.tok.ld;
+  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld;
+  const TokenIn in = token_load(a.tok, t);
   float m = -INFINITY;
   for (int64_t v = tid; v < a.tok.V; v += NT) m = fmaxf(m, load_elem<Tin>(row + v));
-  const float mw = wave_max(m);
-  const int lane = tid & 63, wv = tid >> 6;
-  if (lane == 0) sh_m[wv] = mw;
-  __syncthreads();
-  float M = -INFINITY;
-  for (int q = 0; q < NW; ++q) M = fmaxf(M, sh_m[q]);
-  const float nmb = (M == -INFINITY) ? 0.f : -M * kLog2e;
-  double s = 0.0;
-  for (int64_t v = tid; v < a.tok.V; v += NT) s += (double)__builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, nmb));
-  s = wave_sum(s);
-  if (lane == 0) sh_s[wv] = s;
-  __syncthreads();
+  const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
+  float s = 0.f;
+  for (int64_t v = tid; v < a.tok.V; v += NT) s += __builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, nmb));
+  double M, S;
+  block_combine<NW>(m, s, sh_m, sh_s, M, S);
   if (tid == 0) {
-    double S = 0.0;
-    for (int q = 0; q < NW; ++q) S += sh_s[q];
-    sh_rs = row_epilogue<Tin>(a, t, row, (double)M, S);
+    const bool ok = in.act >= 0 && (int64_t)in.act < a.tok.V;
+    sh_rs = token_finish(a.tok, t, in, M + log(S), ok ? (double)load_elem<Tin>(row + in.act) : 0.0);
   }
   __syncthreads();
   if (!a.dlogits) return;
   const RowScale rs = sh_rs;
-  Tin* drow = static_cast<Tin*>(a.dlogits) + (int64_t)t * a.tok.ld;
+  Tin* drow = static_cast<Tin*>(a.dlogits) + (int64_t)t * a.ld;
   for (int64_t v = tid; v < a.tok.V; v += NT) {
-    float d = (v == rs.act) ? rs.d_a : rs.sign * __builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, rs.nc));
+    const float d =
+        (v == rs.act) ? rs.d_a : rs.sign * __builtin_amdgcn_exp2f(fmaf(load_elem<Tin>(row + v), kLog2e, rs.nc));
     if constexpr (sizeof(Tin) == 2) {
       drow[v] = (uint16_t)(pack_bf16(d, 0.f) & 0xffffu);
     } else {
@@ -220,23 +395,43 @@ static const Variant kVariants[] = {
     GRPO_VARIANT(256, 4),   GRPO_VARIANT(256, 8),   GRPO_VARIANT(256, 12),  GRPO_VARIANT(256, 16),
     GRPO_VARIANT(256, 20),  GRPO_VARIANT(256, 24),  GRPO_VARIANT(1024, 8),  GRPO_VARIANT(1024, 12),
     GRPO_VARIANT(1024, 16), GRPO_VARIANT(1024, 19),
-};  // 1024 threads x 19 vectors (127 VGPRs) is the largest that does not spill
+};  // 1024 threads x 19 vectors is the largest that does not spill
 
-static RowKernel pick_row_kernel(grpo_dtype dt, int64_t V, int64_t ld, const void* logits, const void* dlogits,
-                                 int* nt_out) {
+// The persistent kernels for long bf16 rows, one per NV = ceil(V/8/1024) so
+// that only each thread's last vector can be partial; NP vectors in LDS.
+static const RowKernel kPipe[] = {
+    k_rows_pipe<7, 4>,   k_rows_pipe<8, 4>,   k_rows_pipe<9, 5>,   k_rows_pipe<10, 5>, k_rows_pipe<11, 6>,
+    k_rows_pipe<12, 6>,  k_rows_pipe<13, 7>,  k_rows_pipe<14, 7>,  k_rows_pipe<15, 8>, k_rows_pipe<16, 8>,
+    k_rows_pipe<17, 9>,  k_rows_pipe<18, 9>,  k_rows_pipe<19, 9>,
+};
+constexpr int kPipeMinNV = 7, kPipeMaxNV = 19;
+
+struct Launch {
+  RowKernel k;
+  int nt;
+  unsigned grid;
+};
+
+static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const void* logits,
+                              const void* dlogits) {
   const int epv = (dt == GRPO_BF16) ? 8 : 4;
   const bool vec_ok = (V % epv == 0) && (ld % epv == 0) && aligned(logits, 16) && aligned(dlogits, 16);
   if (vec_ok) {
     const int64_t nvec = V / epv;
+    const int64_t nv = (nvec + 1023) / 1024;
+    if (dt == GRPO_BF16 && nv >= kPipeMinNV && nv <= kPipeMaxNV) {
+      int dev = 0, n_cu = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+        n_cu = 256;
+      const int64_t g = T < n_cu ? T : n_cu;  // one workgroup per CU (LDS bound)
+      return Launch{kPipe[nv - kPipeMinNV], 1024, (unsigned)g};
+    }
     for (const Variant& v : kVariants) {
-      if ((int64_t)v.nt * v.nv >= nvec) {
-        *nt_out = v.nt;
-        return dt == GRPO_BF16 ? v.bf16 : v.f32;
-      }
+      if ((int64_t)v.nt * v.nv >= nvec) return Launch{dt == GRPO_BF16 ? v.bf16 : v.f32, v.nt, (unsigned)T};
     }
   }
-  *nt_out = 256;
-  return dt == GRPO_BF16 ? k_rows_generic<uint16_t> : k_rows_generic<float>;
+  return Launch{dt == GRPO_BF16 ? k_rows_generic<uint16_t> : k_rows_generic<float>, 256, (unsigned)T};
 }
 
 }  // namespace grpo
@@ -257,7 +452,7 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
   if (st != GRPO_OK) return st;
   if (dt != GRPO_BF16 && dt != GRPO_F32) return GRPO_ERR_DTYPE;
   if (T > 0 && !logits) return GRPO_ERR_ARG;
-  if (V < 1 || ld < V) return GRPO_ERR_SHAPE;
+  if (V < 1 || ld < V || V >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
   const size_t esz = (dt == GRPO_BF16) ? 2 : 4;
   if (!aligned(logits, esz) || !aligned(dlogits, esz)) return GRPO_ERR_ALIGN;
   const LossWs L = loss_ws_layout(T, seg->n_traj);
@@ -265,17 +460,18 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
   if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
   char* w = static_cast<char*>(ws);
 
-  if (launch_segments(seg, T, p, w, L, aux ? aux->traj_tok_off : nullptr, s) != hipSuccess) return GRPO_ERR_HIP;
+  if (launch_segments(seg, T, ld, actions, adv, p, w, L, aux, s) != hipSuccess) return GRPO_ERR_HIP;
   if (T > 0) {
     RowArgs a;
     a.logits = logits;
     a.dlogits = dlogits;
-    a.tok = make_token_args(V, ld, actions, behave_logp, prox_logp, adv, seg, p, w, L, aux);
-    int nt = 256;
-    RowKernel k = pick_row_kernel(dt, V, ld, logits, dlogits, &nt);
+    a.ld = ld;
+    a.T = (int)T;
+    a.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L, aux);
+    const Launch k = pick_row_kernel(dt, T, V, ld, logits, dlogits);
     const bool timed = aux && aux->hot_begin && aux->hot_end;
     if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
-    hipLaunchKernelGGL(k, dim3((unsigned)T), dim3(nt), 0, s, a);
+    hipLaunchKernelGGL(k.k, dim3(k.grid), dim3(k.nt), 0, s, a);
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
     if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   }
