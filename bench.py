@@ -36,7 +36,7 @@ sys.path.insert(0, ROOT)
 METRIC = "GRPO loss fwd+bwd tokens/s at V=151,936 bf16; % of HBM (or MFMA) roofline"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rows_resident_v152k_traffic.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_rows_pipe_v152k_traffic.md")
 KERNEL_SOURCES = ["paper_2606_05597_amd/csrc/loss.hip", "paper_2606_05597_amd/csrc/device.h"]
 
 
