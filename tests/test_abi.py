@@ -1,0 +1,150 @@
+"""The C ABI as seen from the host (CPU only): exported symbols and argument checks.
+
+Every call here fails host-side validation, which the header specifies happens
+before anything is enqueued, so no GPU is touched; pointers are dummy
+addresses that the library never dereferences on the host.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_05597_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "grpo.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.SO):
+        from paper_2606_05597_amd.build import build
+        build()
+    return _lib.load()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|size_t|const char\s*\*)\s+(\w+)\s*\(", src, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(["grpo_advantages", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd",
+                                           "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_status_str"])
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.check_output(["nm", "-D", "--defined-only", _lib.SO], text=True)
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_status_strings(lib):
+    for code in range(-6, 1):
+        s = lib.grpo_status_str(code).decode()
+        assert s.startswith("GRPO_"), s
+    assert "unknown" in lib.grpo_status_str(-99).decode()
+
+
+def test_workspace_queries(lib):
+    small = lib.grpo_loss_workspace_bytes(100, 4)
+    big = lib.grpo_loss_workspace_bytes(120000, 128)
+    assert 0 < small < big and big % 256 == 0
+    assert lib.grpo_loss_workspace_bytes(-1, 4) == 0 and lib.grpo_loss_workspace_bytes(10, 0) == 0
+    assert lib.grpo_loss_workspace_bytes(0, 4) > 0  # an empty batch still needs the header and per-trajectory tables
+    f = lib.fused_lmhead_workspace_bytes(65536, 3584, 151936, 8192, 64)
+    assert f > 5e9  # transposed W and h, partials, one dlogits chunk and its transpose, dhidden accumulator
+
+
+D = ctypes.c_void_p(0x100000)  # a dummy, 256-byte aligned device address
+
+
+def call_loss(lib, *, T=8, V=64, ld=64, dt=_lib.GRPO_BF16, n_traj=4, G=4, n_steps=4, norm=1, k=10.0, eps_low=0.2,
+              eps_high=0.2, c=3.0, gs=1.0, ng=0.0, logits=D, actions=D, behave=D, adv=D, loss=D, ws=D,
+              ws_bytes=1 << 30, seg_ptrs=(D, D), dlogits=D):
+    seg = _lib.Segments()
+    seg.n_traj, seg.group_size, seg.n_steps = n_traj, G, n_steps
+    seg.step_tok_off, seg.traj_step_off = seg_ptrs
+    p = _lib.LossParams()
+    p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale, p.n_groups_total = norm, k, eps_low, eps_high, c, gs, ng
+    return lib.grpo_loss_fwd_bwd(logits, dt, T, V, ld, actions, behave, None, adv, ctypes.byref(seg),
+                                 ctypes.byref(p), loss, dlogits, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(actions=None), _lib.GRPO_ERR_ARG),
+    (dict(behave=None), _lib.GRPO_ERR_ARG),
+    (dict(adv=None), _lib.GRPO_ERR_ARG),
+    (dict(loss=None), _lib.GRPO_ERR_ARG),
+    (dict(logits=None), _lib.GRPO_ERR_ARG),
+    (dict(seg_ptrs=(None, D)), _lib.GRPO_ERR_ARG),
+    (dict(ld=63), _lib.GRPO_ERR_SHAPE),
+    (dict(V=0), _lib.GRPO_ERR_SHAPE),
+    (dict(T=-1), _lib.GRPO_ERR_SHAPE),
+    (dict(T=1 << 31), _lib.GRPO_ERR_SHAPE),
+    (dict(n_traj=6), _lib.GRPO_ERR_SHAPE),          # not a multiple of G
+    (dict(n_steps=3), _lib.GRPO_ERR_SHAPE),         # fewer steps than trajectories
+    (dict(G=0), _lib.GRPO_ERR_SHAPE),
+    (dict(norm=7), _lib.GRPO_ERR_ARG),
+    (dict(k=0.0), _lib.GRPO_ERR_ARG),               # CONST_K needs k > 0
+    (dict(eps_low=1.0), _lib.GRPO_ERR_ARG),
+    (dict(eps_low=-0.1), _lib.GRPO_ERR_ARG),
+    (dict(eps_high=-0.1), _lib.GRPO_ERR_ARG),
+    (dict(c=0.5), _lib.GRPO_ERR_ARG),               # the dual clip needs c > 1 (or 0 = off)
+    (dict(c=1.0), _lib.GRPO_ERR_ARG),
+    (dict(gs=float("inf")), _lib.GRPO_ERR_ARG),
+    (dict(ng=-1.0), _lib.GRPO_ERR_ARG),
+    (dict(dt=5), _lib.GRPO_ERR_DTYPE),
+    (dict(logits=ctypes.c_void_p(0x100001)), _lib.GRPO_ERR_ALIGN),
+    (dict(dlogits=ctypes.c_void_p(0x100003), dt=_lib.GRPO_F32), _lib.GRPO_ERR_ALIGN),
+    (dict(ws=None), _lib.GRPO_ERR_WORKSPACE),
+    (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
+    (dict(ws=ctypes.c_void_p(0x100010)), _lib.GRPO_ERR_ALIGN),
+])
+def test_loss_rejects_bad_arguments(lib, kw, status):
+    assert call_loss(lib, **kw) == status
+
+
+def test_trajectory_normaliser_ignores_k(lib):
+    # k is only checked for the constant normaliser; with 1/|tau_i| a zero k passes validation
+    # (a workspace that is too small then stops the call before any launch)
+    assert call_loss(lib, norm=0, k=0.0, ws_bytes=16) == _lib.GRPO_ERR_WORKSPACE
+
+
+def test_advantages_rejects_bad_arguments(lib):
+    f = lib.grpo_advantages
+    assert f(None, 8, 8, 1, 0.0, D, None) == _lib.GRPO_ERR_ARG
+    assert f(D, 8, 8, 2, 0.0, D, None) == _lib.GRPO_ERR_ARG          # ddof in {0, 1}
+    assert f(D, 8, 8, 1, -1.0, D, None) == _lib.GRPO_ERR_ARG         # std_eps >= 0
+    assert f(D, 12, 8, 1, 0.0, D, None) == _lib.GRPO_ERR_SHAPE       # n_traj % G
+    assert f(D, 0, 8, 1, 0.0, D, None) == _lib.GRPO_ERR_SHAPE
+
+
+def call_fused(lib, *, T=8, H=64, V=512, chunk=256, hidden=D, w=D, dh=D, dw=D, ws=D, ws_bytes=1 << 40):
+    seg = _lib.Segments()
+    seg.n_traj, seg.group_size, seg.n_steps = 4, 4, 4
+    seg.step_tok_off, seg.traj_step_off = D, D
+    p = _lib.LossParams()
+    p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale = 1, 10.0, 0.2, 0.2, 0.0, 1.0
+    return lib.fused_lmhead_grpo(hidden, w, T, H, V, chunk, D, D, None, D, ctypes.byref(seg), ctypes.byref(p), D, dh,
+                                 dw, 0, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=96), _lib.GRPO_ERR_SHAPE),        # H a multiple of 64
+    (dict(V=500), _lib.GRPO_ERR_SHAPE),       # V a multiple of 8
+    (dict(chunk=300), _lib.GRPO_ERR_SHAPE),   # chunk a multiple of 256
+    (dict(chunk=0), _lib.GRPO_ERR_SHAPE),
+    (dict(w=None), _lib.GRPO_ERR_ARG),
+    (dict(dw=None), _lib.GRPO_ERR_ARG),
+    (dict(hidden=None), _lib.GRPO_ERR_ARG),
+    (dict(dh=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),
+    (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
+])
+def test_fused_rejects_bad_arguments(lib, kw, status):
+    assert call_fused(lib, **kw) == status
