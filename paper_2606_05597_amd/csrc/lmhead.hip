@@ -2,7 +2,7 @@
 // final hidden states h [T, H] and the LM-head weight W [H, V], with the logits
 // z = h W formed on the matrix cores and never stored whole.
 //
-//   pass 1  z tiles = h W           -> per (row, 128-column tile) max and sum exp,
+//   pass 1  z tiles = h W           -> per (row, 256-column tile) max and sum exp,
 //                                      and the action logit
 //   rows    combine the partials    -> lse, log-prob, token epilogue, dlogits scale
 //   pass 2  for each vocabulary chunk c of `vocab_chunk` columns:
@@ -10,99 +10,32 @@
 //             stored as D_c [Tp, C] and its transpose D_c^T [C, Tp]
 //             dhidden += D_c W_c^T       (fp32 accumulator, bf16 at the end)
 //             dW[:, c] = h^T D_c
-// Every product is one GEMM kernel with both operands K-contiguous
+// Every product is one GEMM core (gemm.h) with both operands K-contiguous
 // (C[m, n] = sum_k A[m, k] B[n, k]); W and h are transposed once so that this
-// holds for all four.  MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation.
+// holds for all four.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
 #include "device.h"
+#include "gemm.h"
 #include "launch.h"
 
 namespace grpo {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int LDK = BK + 8;  // LDS row stride (bf16): 144 B keeps the 16-B fragment reads spread over banks
-constexpr int GEMM_NT = 256;  // 4 waves in a 2 x 2 arrangement, 64 x 64 outputs each
+typedef GemmCfg<256, 256, 64, 2, 4> LmCfg;  // BM, BN, BK, waves in M, waves in N
+constexpr int TILE = 256;                   // BM = BN
 
-struct GemmArgs {
-  const uint16_t* A;  // [M, K], row stride lda
-  const uint16_t* B;  // [N, K], row stride ldb
-  int64_t lda, ldb;
-  int M, N, K;        // K a multiple of 8
+// Shared memory of every GEMM kernel: the mainloop's double-buffered slabs; the
+// epilogues reuse it once the mainloop's final barrier has passed.
+struct GemmSmem {
+  uint16_t a[2 * LmCfg::BM * LmCfg::LDK];
+  uint16_t b[2 * LmCfg::BN * LmCfg::LDK];
 };
 
-// Output coordinates of accumulator register r of MFMA block (i, j) in lane
-// `lane` (32x32x16 layout: column lane%32, rows 8(r/4) + 4(lane/32) + r%4).
-__device__ __forceinline__ int out_row(int wm, int i, int r, int lane) {
-  return wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-}
-__device__ __forceinline__ int out_col(int wn, int j, int lane) { return wn * 64 + j * 32 + (lane & 31); }
-
-// The main loop of one BM x BN tile: double-buffered LDS, global loads of the
-// next K block in flight while the current one feeds the matrix cores.
-// Loads outside [0, M) x [0, K) or [0, N) x [0, K) read as zero.
-__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int m0, int n0, f32x16 (&acc)[2][2],
-                                          uint16_t* sA, uint16_t* sB) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int lr = tid >> 3, lv = tid & 7;  // loader: rows lr + 32q, 8-element vector lv
-  u32x4 ra[4], rb[4];
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  auto gload = [&](int k0) {
-    const int k = k0 + lv * 8;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int m = m0 + lr + 32 * q, n = n0 + lr + 32 * q;
-      ra[q] = (m < g.M && k < g.K) ? *reinterpret_cast<const u32x4*>(g.A + (int64_t)m * g.lda + k) : zero;
-      rb[q] = (n < g.N && k < g.K) ? *reinterpret_cast<const u32x4*>(g.B + (int64_t)n * g.ldb + k) : zero;
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *reinterpret_cast<u32x4*>(sA + (buf * BM + lr + 32 * q) * LDK + lv * 8) = ra[q];
-      *reinterpret_cast<u32x4*>(sB + (buf * BN + lr + 32 * q) * LDK + lv * 8) = rb[q];
-    }
-  };
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int nk = (g.K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 a[2], b[2];
-      const int kk = ks * 16 + (lane >> 5) * 8;
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(sA + (buf * BM + wm * 64 + i * 32 + (lane & 31)) * LDK + kk);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(sB + (buf * BN + wn * 64 + j * 32 + (lane & 31)) * LDK + kk);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
-  }
-}
+__device__ __forceinline__ int tiles_of(int n) { return (n + TILE - 1) / TILE; }
 
 // ---- pass 1: per-tile (max, sum exp) of every row, and the action logit ---------
 struct PartialArgs {
@@ -113,47 +46,59 @@ struct PartialArgs {
   int n_tiles;
 };
 
-__global__ __launch_bounds__(GEMM_NT) void k_lm_partial(const PartialArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2 * BM * LDK], sB[2 * BN * LDK];
-  __shared__ int sh_act[BM];
-  __shared__ float sh_m[2][BM], sh_s[2][BM];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
-  if (tid < BM) sh_act[tid] = (m0 + tid < p.g.M) ? p.actions[m0 + tid] : -1;
-  f32x16 acc[2][2];
-  gemm_tile(p.g, m0, n0, acc, sA, sB);  // ends with a barrier, so sh_act is visible
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  __shared__ int sh_act[TILE];
+  int tm, tn;
+  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  const int m0 = tm * TILE, n0 = tn * TILE;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
+  if (tid < TILE) sh_act[tid] = (m0 + tid < p.g.M) ? p.actions[m0 + tid] : -1;
+  g_f32x16 acc[LmCfg::IB][LmCfg::JB];
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);  // ends with a barrier: sh_act visible, slabs free
+  float* sh_m = reinterpret_cast<float*>(sm.a);       // [WGN][TILE]
+  float* sh_s = sh_m + LmCfg::WGN * TILE;              // [WGN][TILE]
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < LmCfg::IB; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = out_row(wm, i, r, lane);
-      const int c0 = n0 + out_col(wn, 0, lane), c1 = n0 + out_col(wn, 1, lane);
-      const float v0 = (c0 < p.g.N) ? acc[i][0][r] : -INFINITY;
-      const float v1 = (c1 < p.g.N) ? acc[i][1][r] : -INFINITY;
+      const int row = gemm_row<LmCfg>(wm, i, r, lane);
       const int act = sh_act[row];
-      if (act == c0) p.za[m0 + row] = v0;
-      if (act == c1) p.za[m0 + row] = v1;
-      float m = fmaxf(v0, v1);
+      float v[LmCfg::JB];
+      float m = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < LmCfg::JB; ++j) {
+        const int c = n0 + gemm_col<LmCfg>(wn, j, lane);
+        v[j] = (c < p.g.N) ? acc[i][j][r] : -INFINITY;
+        if (act == c) p.za[m0 + row] = v[j];
+        m = fmaxf(m, v[j]);
+      }
 #pragma unroll
       for (int o = 16; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));  // within the 32-lane half
       const float nm = (m == -INFINITY) ? 0.f : -m * kLog2e;
-      float s = __builtin_amdgcn_exp2f(fmaf(v0, kLog2e, nm)) + __builtin_amdgcn_exp2f(fmaf(v1, kLog2e, nm));
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < LmCfg::JB; ++j) s += __builtin_amdgcn_exp2f(fmaf(v[j], kLog2e, nm));
 #pragma unroll
       for (int o = 16; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
       if ((lane & 31) == 0) {
-        sh_m[wn][row] = m;
-        sh_s[wn][row] = s;
+        sh_m[wn * TILE + row] = m;
+        sh_s[wn * TILE + row] = s;
       }
     }
   }
   __syncthreads();
-  if (tid < BM && m0 + tid < p.g.M) {
-    const float ma = sh_m[0][tid], mb = sh_m[1][tid];
-    const float M = fmaxf(ma, mb);
+  if (tid < TILE && m0 + tid < p.g.M) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < LmCfg::WGN; ++q) M = fmaxf(M, sh_m[q * TILE + tid]);
     float S = 0.f;
     if (M != -INFINITY)
-      S = sh_s[0][tid] * __builtin_amdgcn_exp2f((ma - M) * kLog2e) + sh_s[1][tid] * __builtin_amdgcn_exp2f((mb - M) * kLog2e);
-    p.part[(int64_t)(m0 + tid) * p.n_tiles + blockIdx.x] = make_float2(M, S);
+#pragma unroll
+      for (int q = 0; q < LmCfg::WGN; ++q)
+        S += sh_s[q * TILE + tid] * __builtin_amdgcn_exp2f((sh_m[q * TILE + tid] - M) * kLog2e);
+    p.part[(int64_t)(m0 + tid) * p.n_tiles + tn] = make_float2(M, S);
   }
 }
 
@@ -185,7 +130,7 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   if (M != -INFINITY)
     for (int j = tid; j < a.n_tiles; j += 256) {
       const float2 q = pr[j];
-      if (q.x != -INFINITY) s += (double)q.y * exp((double)q.x - (double)M);
+      if (q.x != -INFINITY) s += (double)q.y * (double)__builtin_amdgcn_exp2f((q.x - M) * kLog2e);
     }
   s = wave_sum(s);
   if (lane == 0) sh_s[wv] = s;
@@ -207,19 +152,22 @@ struct DlogitsArgs {
   int c0, C, Tp;
 };
 
-__global__ __launch_bounds__(GEMM_NT) void k_lm_dlogits(const DlogitsArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2 * BM * LDK], sB[2 * BN * LDK];
-  __shared__ RowScale sh_rs[BM];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
-  if (tid < BM) sh_rs[tid] = p.rs[m0 + tid];  // m0 + tid < Tp: the grid covers Tp rows exactly
-  f32x16 acc[2][2];
-  gemm_tile(p.g, m0, n0, acc, sA, sB);
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  __shared__ RowScale sh_rs[TILE];
+  int tm, tn;
+  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.Tp), tiles_of(p.g.N), tm, tn)) return;
+  const int m0 = tm * TILE, n0 = tn * TILE;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
+  if (tid < TILE) sh_rs[tid] = p.rs[m0 + tid];  // m0 + tid < Tp: Tp is a multiple of the tile
+  g_f32x16 acc[LmCfg::IB][LmCfg::JB];
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < LmCfg::IB; ++i) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = n0 + out_col(wn, j, lane);
+    for (int j = 0; j < LmCfg::JB; ++j) {
+      const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
       if (n >= p.g.N) continue;
       const int vcol = p.c0 + n;
 #pragma unroll
@@ -228,10 +176,10 @@ __global__ __launch_bounds__(GEMM_NT) void k_lm_dlogits(const DlogitsArgs p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = rq * 4 + e;
-          const RowScale rs = sh_rs[out_row(wm, i, r, lane)];
+          const RowScale rs = sh_rs[gemm_row<LmCfg>(wm, i, r, lane)];
           d[e] = (vcol == rs.act) ? rs.d_a : rs.sign * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, rs.nc));
         }
-        const int row0 = m0 + out_row(wm, i, rq * 4, lane);
+        const int row0 = m0 + gemm_row<LmCfg>(wm, i, rq * 4, lane);
         u32x2 pk = {pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3])};
         *reinterpret_cast<u32x2*>(p.DT + (int64_t)n * p.Tp + row0) = pk;
 #pragma unroll
@@ -244,26 +192,29 @@ __global__ __launch_bounds__(GEMM_NT) void k_lm_dlogits(const DlogitsArgs p) {
 // ---- pass 2b: dhidden += D_c W_c^T --------------------------------------------------
 struct DhArgs {
   GemmArgs g;        // A = D_c [Tp, C] (M = T, K = Cw), B = W[:, chunk] as [H, Cw] with ldb = V
-  float* acc;        // [Tp, H] fp32 accumulator (unused when single)
+  float* acc;        // [Tp, H] fp32 accumulator (unused with a single chunk)
   uint16_t* dh;      // [T, H] bf16 output
   int first, last;
 };
 
-__global__ __launch_bounds__(GEMM_NT) void k_lm_dh(const DhArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2 * BM * LDK], sB[2 * BN * LDK];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
-  f32x16 acc[2][2];
-  gemm_tile(p.g, m0, n0, acc, sA, sB);
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_dh(const DhArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  int tm, tn;
+  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  const int m0 = tm * TILE, n0 = tn * TILE;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
+  g_f32x16 acc[LmCfg::IB][LmCfg::JB];
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);
   const int H = p.g.N;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < LmCfg::IB; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = n0 + out_col(wn, j, lane);
+    for (int j = 0; j < LmCfg::JB; ++j) {
+      const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = m0 + out_row(wm, i, r, lane);
+        const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
         if (m >= p.g.M || n >= H) continue;
         const int64_t o = (int64_t)m * H + n;
         float v = acc[i][j][r];
@@ -282,20 +233,23 @@ struct DwArgs {
   int c0, accumulate;
 };
 
-__global__ __launch_bounds__(GEMM_NT) void k_lm_dw(const DwArgs p) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2 * BM * LDK], sB[2 * BN * LDK];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
-  f32x16 acc[2][2];
-  gemm_tile(p.g, m0, n0, acc, sA, sB);
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_dw(const DwArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  int tm, tn;
+  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  const int m0 = tm * TILE, n0 = tn * TILE;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
+  g_f32x16 acc[LmCfg::IB][LmCfg::JB];
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < LmCfg::IB; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = n0 + out_col(wn, j, lane);
+    for (int j = 0; j < LmCfg::JB; ++j) {
+      const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = m0 + out_row(wm, i, r, lane);
+        const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
         if (m >= p.g.M || n >= p.g.N) continue;
         float* o = p.dw + (int64_t)m * p.V + p.c0 + n;
         *o = p.accumulate ? *o + acc[i][j][r] : acc[i][j][r];
@@ -349,8 +303,8 @@ struct LmWs {
 static LmWs lm_ws_layout(int64_t T, int64_t H, int64_t V, int32_t C, int32_t n_traj) {
   LmWs l;
   l.loss = loss_ws_layout(T, n_traj);
-  l.Tp = (T + BM - 1) / BM * BM;
-  l.n_tiles = (int)((V + BN - 1) / BN);
+  l.Tp = (T + TILE - 1) / TILE * TILE;
+  l.n_tiles = (int)((V + TILE - 1) / TILE);
   l.C = C;
   const int64_t n_chunks = (V + C - 1) / C;
   size_t o = l.loss.total;
@@ -366,7 +320,11 @@ static LmWs lm_ws_layout(int64_t T, int64_t H, int64_t V, int32_t C, int32_t n_t
   return l;
 }
 
-static dim3 grid2(int64_t N, int64_t M) { return dim3((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)); }
+// A multiple of 8 workgroups covering every tile of an M x N output (see gemm_tile_of).
+static dim3 gemm_grid(int64_t M, int64_t N) {
+  const int64_t tiles = ((M + TILE - 1) / TILE) * ((N + TILE - 1) / TILE);
+  return dim3((unsigned)((tiles + 7) / 8 * 8));
+}
 
 }  // namespace grpo
 
@@ -429,7 +387,7 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   pa.part = part;
   pa.za = za;
   pa.n_tiles = L.n_tiles;
-  hipLaunchKernelGGL(k_lm_partial, grid2(V, T), dim3(GEMM_NT), 0, s, pa);
+  hipLaunchKernelGGL(k_lm_partial, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
   // combine
   CombineArgs ca;
   ca.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
@@ -453,21 +411,21 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
     da.c0 = c0;
     da.C = C;
     da.Tp = Tp;
-    hipLaunchKernelGGL(k_lm_dlogits, grid2(Cw, Tp), dim3(GEMM_NT), 0, s, da);
+    hipLaunchKernelGGL(k_lm_dlogits, gemm_grid(Tp, Cw), dim3(LmCfg::NT), 0, s, da);
     DhArgs ha;
     ha.g = GemmArgs{D, W16 + c0, C, V, (int)T, (int)H, Cw};
     ha.acc = acc;
     ha.dh = static_cast<uint16_t*>(dhidden);
     ha.first = (c == 0);
     ha.last = (c == n_chunks - 1);
-    hipLaunchKernelGGL(k_lm_dh, grid2(H, T), dim3(GEMM_NT), 0, s, ha);
+    hipLaunchKernelGGL(k_lm_dh, gemm_grid(T, H), dim3(LmCfg::NT), 0, s, ha);
     DwArgs wa;
     wa.g = GemmArgs{hT, DT, Tp, Tp, (int)H, Cw, Tp};
     wa.dw = dw_lm;
     wa.V = V;
     wa.c0 = c0;
     wa.accumulate = accumulate_dw;
-    hipLaunchKernelGGL(k_lm_dw, grid2(Cw, H), dim3(GEMM_NT), 0, s, wa);
+    hipLaunchKernelGGL(k_lm_dw, gemm_grid(H, Cw), dim3(LmCfg::NT), 0, s, wa);
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   }
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
