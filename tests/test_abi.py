@@ -57,8 +57,12 @@ def test_workspace_queries(lib):
     assert 0 < small < big and big % 256 == 0
     assert lib.grpo_loss_workspace_bytes(-1, 4) == 0 and lib.grpo_loss_workspace_bytes(10, 0) == 0
     assert lib.grpo_loss_workspace_bytes(0, 4) > 0  # an empty batch still needs the header and per-trajectory tables
-    f = lib.fused_lmhead_workspace_bytes(65536, 3584, 151936, 8192, 64)
-    assert f > 5e9  # transposed W and h, partials, one dlogits chunk and its transpose, dhidden accumulator
+    T, H, V, C = 65536, 3584, 151936, 8192
+    f = lib.fused_lmhead_workspace_bytes(T, H, V, C, 64)
+    # at least: transposed W and h (bf16), one dlogits chunk and its transpose (bf16), the fp32 dhidden accumulator
+    assert f >= 2 * V * H + 2 * H * T + 2 * 2 * T * C + 4 * T * H and f % 256 == 0
+    # a single chunk needs no dhidden accumulator
+    assert lib.fused_lmhead_workspace_bytes(T, H, 4096, 4096, 64) < 2 * 4096 * H + 2 * H * T + 4 * T * 4096 + 4 * T * H
 
 
 D = ctypes.c_void_p(0x100000)  # a dummy, 256-byte aligned device address
