@@ -2,9 +2,9 @@
 // final hidden states h [T, H] and the LM-head weight W [H, V], with the logits
 // z = h W formed on the matrix cores and never stored whole.
 //
-//   pass 1  z tiles = h W           -> per (row, 256-column tile) max and sum exp,
-//                                      and the action logit
-//   rows    combine the partials    -> lse, log-prob, token epilogue, dlogits scale
+//   pass 1  z tiles = h W           -> per (row, 256-column tile) max and sum exp
+//   rows    combine the partials    -> lse; the action logit h_t . W[:, a_t] in fp64;
+//                                      log-prob, token epilogue, dlogits scale
 //   pass 2  for each vocabulary chunk c of `vocab_chunk` columns:
 //             z_c = h W_c (recomputed), D_c = g (softmax - onehot) in bf16,
 //             stored as D_c [Tp, C] and its transpose D_c^T [C, Tp]
@@ -12,9 +12,12 @@
 //             dW[:, c] = h^T D_c
 // Every product is one GEMM core (gemm.h) with both operands K-contiguous
 // (C[m, n] = sum_k A[m, k] B[n, k]); W and h are transposed once so that this
-// holds for all four.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16.
+// holds for all four.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16, slabs
+// loaded straight into LDS.
 #include <hip/hip_runtime.h>
 #include <math.h>
+
+#include <type_traits>
 
 #include "device.h"
 #include "gemm.h"
@@ -25,66 +28,94 @@ namespace grpo {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-typedef GemmCfg<256, 256, 64, 2, 4> LmCfg;  // BM, BN, BK, waves in M, waves in N
-constexpr int TILE = 256;                   // BM = BN
+typedef GemmCfg<256, 256, 2, 4> LmCfg;  // BM, BN, waves in M, waves in N
+constexpr int TILE = 256;               // BM = BN
 
-// Shared memory of every GEMM kernel: the mainloop's double-buffered slabs; the
-// epilogues reuse it once the mainloop's final barrier has passed.
+// Shared memory of every GEMM kernel: the mainloop's two slab buffers.  The
+// epilogues reuse it once the mainloop's last barrier has passed (every wave has
+// finished its LDS reads by then, and no DMA is left in flight).
 struct GemmSmem {
-  uint16_t a[2 * LmCfg::BM * LmCfg::LDK];
-  uint16_t b[2 * LmCfg::BN * LmCfg::LDK];
+  uint16_t s[2 * LmCfg::STAGE];
 };
 
 __device__ __forceinline__ int tiles_of(int n) { return (n + TILE - 1) / TILE; }
 
-// ---- pass 1: per-tile (max, sum exp) of every row, and the action logit ---------
+// ---- 16-lane DPP reductions ---------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  // every source lane of these patterns is valid, so bound_ctrl changes nothing; it
+  // lets the move fold into the consuming max / add
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
+}
+// Four steps give every lane of a 16-lane row the row's max (sum): swaps within
+// quads, then across the halves of each 8-lane group (half mirror), then across the
+// two 8-lane groups (mirror).
+// DPP controls: quad_perm [1, 0, 3, 2] = 0xB1, quad_perm [2, 3, 0, 1] = 0x4E,
+// row_half_mirror = 0x141, row_mirror = 0x140.
+__device__ __forceinline__ float add_f32(float a, float b) { return a + b; }
+
+// ---- pass 1: per-tile (max, sum exp) of every row ------------------------------------
 struct PartialArgs {
-  GemmArgs g;               // A = h [T, H], B = W^T [V, H]
-  const int32_t* actions;   // [T]
-  float2* part;             // [T, n_tiles] (max, sum exp over the tile's columns)
-  float* za;                // [T] action logit
+  GemmArgs g;    // A = h [T, H], B = W^T [V, H]
+  float2* part;  // [T, n_tiles] (max, sum exp over the tile's columns)
   int n_tiles;
 };
 
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
-  __shared__ int sh_act[TILE];
   int tm, tn;
   if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
   const int m0 = tm * TILE, n0 = tn * TILE;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
-  if (tid < TILE) sh_act[tid] = (m0 + tid < p.g.M) ? p.actions[m0 + tid] : -1;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);  // ends with a barrier: sh_act visible, slabs free
-  float* sh_m = reinterpret_cast<float*>(sm.a);       // [WGN][TILE]
-  float* sh_s = sh_m + LmCfg::WGN * TILE;              // [WGN][TILE]
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  // A 16-lane row of a wave holds 16 x JB columns of one output row: reduce them with
+  // DPP, then the 2 x WGN such groups of each row through LDS.
+  constexpr int NG = 2 * LmCfg::WGN;
+  float* sh_m = reinterpret_cast<float*>(sm.s);  // [NG][TILE]
+  float* sh_s = sh_m + NG * TILE;                 // [NG][TILE]
+  const int grp = wn * 2 + ((lane >> 4) & 1);
+  const int c = n0 + gemm_col<LmCfg>(wn, 0, lane);
+  const bool full = n0 + TILE <= p.g.N;
 #pragma unroll
   for (int i = 0; i < LmCfg::IB; ++i) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = gemm_row<LmCfg>(wm, i, r, lane);
-      const int act = sh_act[row];
-      float v[LmCfg::JB];
-      float m = -INFINITY;
+    for (int r0 = 0; r0 < 16; r0 += 4) {  // four rows at a time: independent DPP chains interleave
+      float v[4][LmCfg::JB], m[4], e[4];
 #pragma unroll
-      for (int j = 0; j < LmCfg::JB; ++j) {
-        const int c = n0 + gemm_col<LmCfg>(wn, j, lane);
-        v[j] = (c < p.g.N) ? acc[i][j][r] : -INFINITY;
-        if (act == c) p.za[m0 + row] = v[j];
-        m = fmaxf(m, v[j]);
+      for (int u = 0; u < 4; ++u) {
+        m[u] = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          v[u][j] = (full || c + 32 * j < p.g.N) ? acc[i][j][r0 + u] : -INFINITY;
+          m[u] = fmaxf(m[u], v[u][j]);
+        }
       }
+#define GRPO_DPP_STEP(OP, X, CTRL) _Pragma("unroll") for (int u = 0; u < 4; ++u) X[u] = OP(X[u], dpp_f32<CTRL>(X[u]));
+      GRPO_DPP_STEP(fmaxf, m, 0xB1)
+      GRPO_DPP_STEP(fmaxf, m, 0x4E)
+      GRPO_DPP_STEP(fmaxf, m, 0x141)
+      GRPO_DPP_STEP(fmaxf, m, 0x140)
 #pragma unroll
-      for (int o = 16; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));  // within the 32-lane half
-      const float nm = (m == -INFINITY) ? 0.f : -m * kLog2e;
-      float s = 0.f;
+      for (int u = 0; u < 4; ++u) {
+        const float nm = (m[u] == -INFINITY) ? 0.f : -m[u] * kLog2e;
+        e[u] = 0.f;
 #pragma unroll
-      for (int j = 0; j < LmCfg::JB; ++j) s += __builtin_amdgcn_exp2f(fmaf(v[j], kLog2e, nm));
+        for (int j = 0; j < LmCfg::JB; ++j) e[u] += __builtin_amdgcn_exp2f(fmaf(v[u][j], kLog2e, nm));
+      }
+      GRPO_DPP_STEP(add_f32, e, 0xB1)
+      GRPO_DPP_STEP(add_f32, e, 0x4E)
+      GRPO_DPP_STEP(add_f32, e, 0x141)
+      GRPO_DPP_STEP(add_f32, e, 0x140)
+#undef GRPO_DPP_STEP
+      if ((lane & 15) == 0) {
 #pragma unroll
-      for (int o = 16; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
-      if ((lane & 31) == 0) {
-        sh_m[wn * TILE + row] = m;
-        sh_s[wn * TILE + row] = s;
+        for (int u = 0; u < 4; ++u) {
+          const int row = gemm_row<LmCfg>(wm, i, r0 + u, lane);
+          sh_m[grp * TILE + row] = m[u];
+          sh_s[grp * TILE + row] = e[u];
+        }
       }
     }
   }
@@ -92,28 +123,29 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   if (tid < TILE && m0 + tid < p.g.M) {
     float M = -INFINITY;
 #pragma unroll
-    for (int q = 0; q < LmCfg::WGN; ++q) M = fmaxf(M, sh_m[q * TILE + tid]);
+    for (int q = 0; q < NG; ++q) M = fmaxf(M, sh_m[q * TILE + tid]);
     float S = 0.f;
     if (M != -INFINITY)
 #pragma unroll
-      for (int q = 0; q < LmCfg::WGN; ++q)
+      for (int q = 0; q < NG; ++q)
         S += sh_s[q * TILE + tid] * __builtin_amdgcn_exp2f((sh_m[q * TILE + tid] - M) * kLog2e);
     p.part[(int64_t)(m0 + tid) * p.n_tiles + tn] = make_float2(M, S);
   }
 }
 
-// ---- combine: lse, log-prob and the token epilogue, one workgroup per row --------
+// ---- combine: lse, action logit, log-prob and the token epilogue, one workgroup per row
 struct CombineArgs {
   TokenArgs tok;
   const float2* part;
-  const float* za;
-  RowScale* rs;  // [Tp]; rows >= T get the zero scale
-  int T, n_tiles;
+  const uint16_t* h;   // [T, H]
+  const uint16_t* WT;  // [V, H]
+  RowScale* rs;        // [Tp]; rows >= T get the zero scale
+  int T, H, n_tiles;
 };
 
 __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   __shared__ float sh_m[4];
-  __shared__ double sh_s[4];
+  __shared__ double sh_s[4], sh_z[4];
   const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (t >= a.T) {
     if (tid == 0) a.rs[t] = RowScale{-INFINITY, 1.f, 0.f, -1};
@@ -123,7 +155,28 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   float m = -INFINITY;
   for (int j = tid; j < a.n_tiles; j += 256) m = fmaxf(m, pr[j].x);
   m = wave_max(m);
-  if (lane == 0) sh_m[wv] = m;
+  // the action logit z_a = h_t . W[:, a] (row a of the transposed weight), in fp64
+  const int act = a.tok.actions[t];
+  const bool ok = act >= 0 && (int64_t)act < a.tok.V;
+  double z = 0.0;
+  if (ok) {
+    const uint16_t* hr = a.h + (int64_t)t * a.H;
+    const uint16_t* wr = a.WT + (int64_t)act * a.H;
+    for (int k = tid * 8; k < a.H; k += 256 * 8) {
+      const u32x4 x = *reinterpret_cast<const u32x4*>(hr + k);
+      const u32x4 y = *reinterpret_cast<const u32x4*>(wr + k);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        z += (double)bf16_lo(x[q]) * (double)bf16_lo(y[q]);
+        z += (double)bf16_hi(x[q]) * (double)bf16_hi(y[q]);
+      }
+    }
+  }
+  z = wave_sum(z);
+  if (lane == 0) {
+    sh_m[wv] = m;
+    sh_z[wv] = z;
+  }
   __syncthreads();
   const float M = fmaxf(fmaxf(sh_m[0], sh_m[1]), fmaxf(sh_m[2], sh_m[3]));
   double s = 0.0;
@@ -137,9 +190,9 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   __syncthreads();
   if (tid == 0) {
     const double S = sh_s[0] + sh_s[1] + sh_s[2] + sh_s[3];
+    const double za = sh_z[0] + sh_z[1] + sh_z[2] + sh_z[3];
     const TokenIn in = token_load(a.tok, t);
-    const bool ok = in.act >= 0 && (int64_t)in.act < a.tok.V;
-    a.rs[t] = token_finish(a.tok, t, in, (double)M + log(S), ok ? (double)a.za[t] : 0.0);
+    a.rs[t] = token_finish(a.tok, t, in, (double)M + log(S), za);
   }
 }
 
@@ -162,29 +215,51 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   if (tid < TILE) sh_rs[tid] = p.rs[m0 + tid];  // m0 + tid < Tp: Tp is a multiple of the tile
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);  // its first barrier publishes sh_rs
+  // Columns past the chunk's width (last tile of the last chunk) are written too: they
+  // stay inside D's C columns and D^T's C rows, and no product reads them.
+  // D^T straight from the registers: a lane holds 4 consecutive rows of one column.
+  // D through LDS: each wave stages 64 of its rows (row stride 72 bf16: the two
+  // 32-lane halves of a store land on different banks), then stores 16-byte rows.
+  constexpr int LDR = 72;
+  uint16_t* stage = sm.s + wave * 64 * LDR;
 #pragma unroll
-  for (int i = 0; i < LmCfg::IB; ++i) {
+  for (int half = 0; half < 2; ++half) {
 #pragma unroll
-    for (int j = 0; j < LmCfg::JB; ++j) {
-      const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
-      if (n >= p.g.N) continue;
-      const int vcol = p.c0 + n;
+    for (int ii = 0; ii < 2; ++ii) {
+      const int i = half * 2 + ii;
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {  // four consecutive rows per register quad
-        float d[4];
+      for (int q = 0; q < 4; ++q) {
+        RowScale rs[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = rq * 4 + e;
-          const RowScale rs = sh_rs[gemm_row<LmCfg>(wm, i, r, lane)];
-          d[e] = (vcol == rs.act) ? rs.d_a : rs.sign * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, rs.nc));
+        for (int e = 0; e < 4; ++e) rs[e] = sh_rs[gemm_row<LmCfg>(wm, i, 4 * q + e, lane)];
+#pragma unroll
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
+          const int vcol = p.c0 + n;
+          float d[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            d[e] = (vcol == rs[e].act) ? rs[e].d_a
+                                       : rs[e].sign * __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * q + e], kLog2e, rs[e].nc));
+          const uint32_t lo = pack_bf16(d[0], d[1]), hi = pack_bf16(d[2], d[3]);
+          const int row0 = m0 + gemm_row<LmCfg>(wm, i, 4 * q, lane);
+          *reinterpret_cast<u32x2*>(p.DT + (int64_t)n * p.Tp + row0) = u32x2{lo, hi};
+          const int lr = ii * 32 + 8 * q + 4 * (lane >> 5), lc = j * 32 + (lane & 31);
+          stage[(lr + 0) * LDR + lc] = (uint16_t)(lo & 0xffffu);
+          stage[(lr + 1) * LDR + lc] = (uint16_t)(lo >> 16);
+          stage[(lr + 2) * LDR + lc] = (uint16_t)(hi & 0xffffu);
+          stage[(lr + 3) * LDR + lc] = (uint16_t)(hi >> 16);
         }
-        const int row0 = m0 + gemm_row<LmCfg>(wm, i, rq * 4, lane);
-        u32x2 pk = {pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3])};
-        *reinterpret_cast<u32x2*>(p.DT + (int64_t)n * p.Tp + row0) = pk;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) p.D[(int64_t)(row0 + e) * p.C + n] = (uint16_t)(pack_bf16(d[e], 0.f) & 0xffffu);
       }
+    }
+    // this wave's 64 staged rows x 64 columns, 8 lanes per row (LDS runs a wave's accesses in order)
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {
+      const int lr = it * 8 + (lane >> 3), cv = (lane & 7) * 8;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stage + lr * LDR + cv);
+      const int grow = m0 + wm * LmCfg::WTM + half * 64 + lr;
+      *reinterpret_cast<u32x4*>(p.D + (int64_t)grow * p.C + n0 + wn * LmCfg::WTN + cv) = v;
     }
   }
 }
@@ -205,24 +280,42 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh(const DhArgs p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
   const int H = p.g.N;
+  // the uniform choices (interior tile, first / last chunk) are template arguments, so
+  // that the element loop has no branches
+  auto store = [&](auto full, auto first, auto last) {
 #pragma unroll
-  for (int i = 0; i < LmCfg::IB; ++i)
-#pragma unroll
-    for (int j = 0; j < LmCfg::JB; ++j) {
-      const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
+    for (int i = 0; i < LmCfg::IB; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
-        if (m >= p.g.M || n >= H) continue;
-        const int64_t o = (int64_t)m * H + n;
-        float v = acc[i][j][r];
-        if (!p.first) v += p.acc[o];
-        if (p.last) p.dh[o] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
-        else p.acc[o] = v;
+        if (!full && m >= p.g.M) continue;
+        const int64_t o = (int64_t)m * H + n0 + gemm_col<LmCfg>(wn, 0, lane);
+#pragma unroll
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          if (!full && n0 + gemm_col<LmCfg>(wn, j, lane) >= H) continue;
+          float v = acc[i][j][r];
+          if (!first) v += p.acc[o + 32 * j];
+          if (last) p.dh[o + 32 * j] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
+          else p.acc[o + 32 * j] = v;
+        }
       }
-    }
+  };
+  typedef std::true_type Y;
+  typedef std::false_type N;
+  const bool full = m0 + TILE <= p.g.M && n0 + TILE <= H;
+  const int mode = (full ? 4 : 0) | (p.first ? 2 : 0) | (p.last ? 1 : 0);
+  switch (mode) {
+    case 7: store(Y(), Y(), Y()); break;
+    case 6: store(Y(), Y(), N()); break;
+    case 5: store(Y(), N(), Y()); break;
+    case 4: store(Y(), N(), N()); break;
+    case 3: store(N(), Y(), Y()); break;
+    case 2: store(N(), Y(), N()); break;
+    case 1: store(N(), N(), Y()); break;
+    default: store(N(), N(), N()); break;
+  }
 }
 
 // ---- pass 2c: dW[:, chunk] = h^T D_c ----------------------------------------------
@@ -241,20 +334,32 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dw(const DwArgs p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.a, sm.b);
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  auto store = [&](auto full, auto accumulate) {
 #pragma unroll
-  for (int i = 0; i < LmCfg::IB; ++i)
-#pragma unroll
-    for (int j = 0; j < LmCfg::JB; ++j) {
-      const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
+    for (int i = 0; i < LmCfg::IB; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
-        if (m >= p.g.M || n >= p.g.N) continue;
-        float* o = p.dw + (int64_t)m * p.V + p.c0 + n;
-        *o = p.accumulate ? *o + acc[i][j][r] : acc[i][j][r];
+        if (!full && m >= p.g.M) continue;
+        float* o = p.dw + (int64_t)m * p.V + p.c0 + n0 + gemm_col<LmCfg>(wn, 0, lane);
+#pragma unroll
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          if (!full && n0 + gemm_col<LmCfg>(wn, j, lane) >= p.g.N) continue;
+          o[32 * j] = accumulate ? o[32 * j] + acc[i][j][r] : acc[i][j][r];
+        }
       }
-    }
+  };
+  typedef std::true_type Y;
+  typedef std::false_type N;
+  const bool full = m0 + TILE <= p.g.M && n0 + TILE <= p.g.N;
+  if (full) {
+    if (p.accumulate) store(Y(), Y());
+    else store(Y(), N());
+  } else {
+    if (p.accumulate) store(N(), Y());
+    else store(N(), N());
+  }
 }
 
 // ---- bf16 transpose: dst[c][r] = src[r][c] for r < R, 0 for R <= r < Rp ------------
@@ -295,7 +400,7 @@ __global__ void k_fill_f32(float* p, int64_t n, float v) {
 // ---- workspace --------------------------------------------------------------------
 struct LmWs {
   LossWs loss;
-  size_t wt, ht, part, za, rs, d, dt, acc, total;
+  size_t wt, ht, part, rs, d, dt, acc, total;
   int64_t Tp;
   int n_tiles, C;
 };
@@ -311,7 +416,6 @@ static LmWs lm_ws_layout(int64_t T, int64_t H, int64_t V, int32_t C, int32_t n_t
   l.wt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(V * H));
   l.ht = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(H * l.Tp));
   l.part = o; o = align_up(o + sizeof(float2) * (size_t)(T * l.n_tiles));
-  l.za = o;   o = align_up(o + sizeof(float) * (size_t)T);
   l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
   l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C));
   l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C));
@@ -357,7 +461,6 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);
   uint16_t* hT = reinterpret_cast<uint16_t*>(w + L.ht);
   float2* part = reinterpret_cast<float2*>(w + L.part);
-  float* za = reinterpret_cast<float*>(w + L.za);
   RowScale* rs = reinterpret_cast<RowScale*>(w + L.rs);
   uint16_t* D = reinterpret_cast<uint16_t*>(w + L.d);
   uint16_t* DT = reinterpret_cast<uint16_t*>(w + L.dt);
@@ -383,18 +486,18 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   // pass 1
   PartialArgs pa;
   pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
-  pa.actions = actions;
   pa.part = part;
-  pa.za = za;
   pa.n_tiles = L.n_tiles;
   hipLaunchKernelGGL(k_lm_partial, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
   // combine
   CombineArgs ca;
   ca.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
   ca.part = part;
-  ca.za = za;
+  ca.h = h16;
+  ca.WT = WT;
   ca.rs = rs;
   ca.T = (int)T;
+  ca.H = (int)H;
   ca.n_tiles = L.n_tiles;
   hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)Tp), dim3(256), 0, s, ca);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
