@@ -5,8 +5,8 @@
 // K is walked in slabs of BK = 64.  A slab goes from global memory straight into LDS (buffer_load_dwordx4 ...
 // lds: no staging registers), written as inline asm so that the compiler does not hold every LDS read back until
 // all LDS DMA in flight has landed; the explicit waits below order them instead.  Rows are 128 B, unpadded, and
-// the eight 16-byte vectors of row r sit at slot (vector ^ (r & 7)), so the 32 rows a fragment read touches
-// spread over all banks.  Two LDS buffers: the DMA of slab k + 2 is issued right after the single barrier of
+// the eight 16-byte vectors of a row are permuted (lds_swizzle) so that fragment reads are free of bank
+// conflicts.  Two LDS buffers: the DMA of slab k + 2 is issued right after the single barrier of
 // step k, so it has a whole step to land, and the MFMA fragments are double-buffered in registers.
 // Out-of-range rows and K columns read as zero through the buffer descriptor's range check.
 #pragma once
@@ -74,6 +74,11 @@ __device__ __forceinline__ g_u32x4 buffer_rsrc(const void* base, uint32_t bytes)
   return r;
 }
 
+// LDS slot permutation of a slab row (eight 16-byte slots per 128-byte row).  A fragment read takes
+// one slot from each of 32 consecutive rows; the LDS serves 16 lanes (256 bytes) at a time, so every 16
+// consecutive rows must spread over the 8 slots x 2 row parities, and every 8 over the 8 slots.
+__device__ __forceinline__ int lds_swizzle(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
 // 16 bytes per lane from rsrc + voff into LDS at lds_base + 16 * lane (lds_base wave-uniform).  M0 carries the
 // LDS address; nothing else in these kernels uses it.
 __device__ __forceinline__ void dma16(uint32_t lds_base, uint32_t voff, g_u32x4 rsrc) {
@@ -98,21 +103,27 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, int m0, int n0,
   const int rows_a = min(C::BM, g.M - m0), rows_b = min(C::BN, g.N - n0);
   const g_u32x4 ra = buffer_rsrc(g.A + (int64_t)m0 * g.lda, (uint32_t)(((int64_t)(rows_a - 1) * g.lda + g.K) * 2));
   const g_u32x4 rb = buffer_rsrc(g.B + (int64_t)n0 * g.ldb, (uint32_t)(((int64_t)(rows_b - 1) * g.ldb + g.K) * 2));
-  const int lrow = lane >> 3, kvec = (lane & 7) ^ lrow;
-  const uint32_t offa = (uint32_t)((wave * 8 + lrow) * g.lda + kvec * 8) * 2u;
-  const uint32_t offb = (uint32_t)((wave * 8 + lrow) * g.ldb + kvec * 8) * 2u;
-  const uint32_t stepa = (uint32_t)(C::NW * 8 * g.lda) * 2u, stepb = (uint32_t)(C::NW * 8 * g.ldb) * 2u;
+  // DMA instruction q of this wave fills slab rows 8 (q NW + wave) .. + 7; lane -> row lane / 8, LDS slot
+  // lane % 8, which holds global vector slot ^ swizzle(row)
+  const int lrow = lane >> 3;
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)lds);
   auto issue = [&](int buf, int k0) {
-    const bool kin = k0 + kvec * 8 < g.K;
     const uint32_t la = lds0 + (uint32_t)(buf * C::STAGE + wave * 8 * C::BK) * 2u;
     const uint32_t lb = la + (uint32_t)(C::BM * C::BK) * 2u;
 #pragma unroll
-    for (int q = 0; q < C::QA; ++q)
-      dma16(la + (uint32_t)(q * C::NW * 8 * C::BK) * 2u, kin ? offa + q * stepa + (uint32_t)k0 * 2u : 0x80000000u, ra);
+    for (int q = 0; q < C::QA; ++q) {
+      const int row = (q * C::NW + wave) * 8 + lrow, kv = (lane & 7) ^ lds_swizzle(row);
+      const bool kin = k0 + kv * 8 < g.K;  // vectors past K read as zero
+      dma16(la + (uint32_t)(q * C::NW * 8 * C::BK) * 2u,
+            kin ? (uint32_t)(row * g.lda + k0 + kv * 8) * 2u : 0x80000000u, ra);
+    }
 #pragma unroll
-    for (int q = 0; q < C::QB; ++q)
-      dma16(lb + (uint32_t)(q * C::NW * 8 * C::BK) * 2u, kin ? offb + q * stepb + (uint32_t)k0 * 2u : 0x80000000u, rb);
+    for (int q = 0; q < C::QB; ++q) {
+      const int row = (q * C::NW + wave) * 8 + lrow, kv = (lane & 7) ^ lds_swizzle(row);
+      const bool kin = k0 + kv * 8 < g.K;
+      dma16(lb + (uint32_t)(q * C::NW * 8 * C::BK) * 2u,
+            kin ? (uint32_t)(row * g.ldb + k0 + kv * 8) * 2u : 0x80000000u, rb);
+    }
   };
 #pragma unroll
   for (int i = 0; i < C::IB; ++i)
@@ -125,7 +136,7 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, int m0, int n0,
   const int arow = (wm * C::WTM + fr) * C::BK, brow = C::BM * C::BK + (wn * C::WTN + fr) * C::BK;
   int sw[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) sw[ks] = ((2 * ks + hi) ^ (lane & 7)) * 8;
+  for (int ks = 0; ks < 4; ++ks) sw[ks] = ((2 * ks + hi) ^ lds_swizzle(fr)) * 8;
 
   g_bf16x8 fa[2][C::IB], fb[2][C::JB];
   auto read = [&](int f, int buf, int ks) {
