@@ -161,6 +161,34 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRsrcWord3);
 }
 
+// 16 bytes per lane from the buffer (rsrc, voff + soff) into LDS at lds_base + 16 * lane, non-temporal.
+// Inline asm: the compiler's own handling of LDS DMA would hold every LDS read back until all LDS DMA in
+// flight has landed; the kernel orders them with explicit waits instead.  M0 carries the LDS address;
+// nothing else in this kernel uses it.
+__device__ __forceinline__ void dma16_nt(uint32_t lds_base, uint32_t voff, uint32_t soff, u32x4 rsrc) {
+  lds_base = __builtin_amdgcn_readfirstlane(lds_base);
+  soff = __builtin_amdgcn_readfirstlane(soff);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) rsrc[k] = __builtin_amdgcn_readfirstlane(rsrc[k]);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds" ::"s"(lds_base), "v"(voff), "s"(rsrc),
+               "s"(soff)
+               : "memory", "m0");
+}
+__device__ __forceinline__ u32x4 row_rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  u32x4 r = {(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, bytes, kRsrcWord3};
+  return r;
+}
+// waits until at most N vector-memory operations of this wave are outstanding (they complete in order)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Hides the register vectors' values from the optimiser, so that the widened
 // bf16 of one pass is recomputed in the next instead of kept live across it.
 template <int N>
@@ -184,18 +212,19 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
   __shared__ double sh_s[NW];
   __shared__ float sh_za;
   __shared__ RowScale sh_rs;
+  __shared__ TokenIn sh_in;  // inputs of the row about to start (wave 1 loads them during the previous row)
   const int wv = threadIdx.x >> 6;
   const int nvec = (int)(a.tok.V / 8);
   const int row_bytes = nvec * 16;
   const uint16_t* logits = static_cast<const uint16_t*>(a.logits);
   uint16_t* dlogits = static_cast<uint16_t*>(a.dlogits);
 
+  const uint32_t lds_stage =
+      (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) u32x4*)stage) + wv * 64 * 16;
   auto stage_row = [&](int r, int voff) {  // vectors 0..NP-1 of row r -> LDS, asynchronously
-    const __amdgpu_buffer_rsrc_t src = row_rsrc(logits + (int64_t)r * a.ld, row_bytes);
+    const u32x4 src = row_rsrc_words(logits + (int64_t)r * a.ld, (uint32_t)row_bytes);
 #pragma unroll
-    for (int j = 0; j < NP; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(src, (__attribute__((address_space(3))) void*)(stage + j * NT + wv * 64),
-                                               16, voff, j * VB, 0, kStream);
+    for (int j = 0; j < NP; ++j) dma16_nt(lds_stage + j * NT * 16, voff, j * VB, src);
   };
   auto load_regs = [&](u32x4 (&dst)[NR], int r, int voff) {
     const __amdgpu_buffer_rsrc_t src = row_rsrc(logits + (int64_t)r * a.ld, row_bytes);
@@ -206,9 +235,10 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
   int t = blockIdx.x;
   if (t >= a.T) return;
   u32x4 reg[NR];
+  if (threadIdx.x == 64) sh_in = token_load(a.tok, t);
   stage_row(t, threadIdx.x * 16);
   load_regs(reg, t, threadIdx.x * 16);
-  TokenIn in = token_load(a.tok, t);
+  wait_vmcnt<NR>();  // this wave's LDS part of row t has landed; the register loads may still be in flight
 
   for (; t < a.T; t += gridDim.x) {
     // The thread index is laundered per row so that nothing derived from it
@@ -218,18 +248,24 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
     const int voff = tid * 16;
     const bool last_full = tid < nvec - (NV - 1) * NT;
     const int tn = t + gridDim.x;
+    lds_barrier();  // every wave's LDS part of row t has landed, and sh_in holds row t's inputs
+    const TokenIn in = sh_in;
     const int act_vec = (in.act >= 0 && in.act < a.tok.V) ? in.act / 8 : -1;
     const int act_lane = in.act & 7;
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's loads of row t have landed
-    __syncthreads();                     // ... and every wave's LDS staging
 
-    float m = -INFINITY;
+    // (max, sum exp) over the LDS part first, while the register part is still landing
+    float m1 = -INFINITY;
 #pragma unroll 1
     for (int j = 0; j < NP; ++j) {
       const u32x4 x = stage[j * NT + tid];
-      m = vec_max<uint16_t>(x, m);
+      m1 = vec_max<uint16_t>(x, m1);
       if (j * NT + tid == act_vec) sh_za = vec_elem<uint16_t>(x, act_lane);
     }
+    const float nmb1 = (m1 == -INFINITY) ? 0.f : -m1 * kLog2e;
+    float s1 = 0.f;
+#pragma unroll 1
+    for (int j = 0; j < NP; ++j) s1 += vec_sumexp<uint16_t>(stage[j * NT + tid], nmb1);
+    float m = m1;
 #pragma unroll
     for (int q = 0; q < NR; ++q) {
       const int j = NP + q;
@@ -239,10 +275,8 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
       }
     }
     const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
-    float s = 0.f;
+    float s = (m1 == -INFINITY) ? 0.f : s1 * __builtin_amdgcn_exp2f((m1 - m) * kLog2e);
     fresh(reg);
-#pragma unroll 1
-    for (int j = 0; j < NP; ++j) s += vec_sumexp<uint16_t>(stage[j * NT + tid], nmb);
 #pragma unroll
     for (int q = 0; q < NR; ++q)
       if (NP + q < NV - 1 || last_full) s += vec_sumexp<uint16_t>(reg[q], nmb);
@@ -250,6 +284,9 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
     double M, S;
     block_combine<NW>(m, s, sh_m, sh_s, M, S);  // barrier: sh_za is visible
     if (tid == 0) sh_rs = token_finish(a.tok, t, in, M + log(S), (double)sh_za);
+    // wave 1 fetches the next row's token inputs meanwhile: its loads are the only memory operations it has
+    // in flight here, so waiting for them holds nothing else back
+    if (tid == 64) sh_in = token_load(a.tok, tn < a.T ? tn : t);
     __syncthreads();
 
     const RowScale rs = sh_rs;
@@ -264,9 +301,8 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
       __builtin_amdgcn_raw_buffer_store_b128(
           vec_dlogits<uint16_t>(stage[j * NT + tid], rs, smask, j * NT + tid == act_v, rs.act & 7), dst, voff, j * VB,
           kStream);
-    __syncthreads();  // every wave is done with stage[]
+    lds_barrier();  // every wave is done reading stage[] (the stores read registers)
     if (tn < a.T) stage_row(tn, voff);
-    const TokenIn in_next = token_load(a.tok, tn < a.T ? tn : t);  // lands during the register part
     // past the last row: a zero-sized source, every load returns 0
     const __amdgpu_buffer_rsrc_t nxt = row_rsrc(logits + (int64_t)(tn < a.T ? tn : t) * a.ld, tn < a.T ? row_bytes : 0);
 #pragma unroll
@@ -276,7 +312,9 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
           vec_dlogits<uint16_t>(reg[q], rs, smask, j * NT + tid == act_v, rs.act & 7), dst, voff, j * VB, kStream);
       reg[q] = __builtin_amdgcn_raw_buffer_load_b128(nxt, voff, j * VB, kStream);
     }
-    in = in_next;
+    // the 2 NR register stores and loads were issued after the LDS part of row tn, so this returns once
+    // that part has landed
+    wait_vmcnt<2 * NR>();
   }
 }
 
