@@ -57,6 +57,8 @@ def _load():
         lib.oracle_loss_rows.restype = ctypes.c_int
         lib.oracle_reduce.argtypes = [P, P, I64, I32, P]
         lib.oracle_reduce.restype = D
+        lib.oracle_logp_entropy.argtypes = [P, ctypes.c_int, I64, I64, P, I64, I64, P, P]
+        lib.oracle_logp_entropy.restype = ctypes.c_int
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
@@ -180,3 +182,38 @@ def loss_rows(logits: np.ndarray, actions, behave_logp, prox_logp, adv, seg: Seg
     tt = np.ascontiguousarray(seg.tok_traj[row_begin:row_end])
     total = lib.oracle_reduce(_ptr(contrib), _ptr(tt), n_rows, n_traj, _ptr(traj))
     return LossResult(float(total), traj, logp, contrib, g, st, dl, int(f))
+
+
+class LogpEntropy:
+    """Forward-only oracle results: per-row action log-prob, entropy and error flags."""
+
+    def __init__(self, token_logp, token_entropy, flags):
+        self.token_logp = token_logp
+        self.token_entropy = token_entropy
+        self.flags = flags
+
+
+def logp_entropy(logits: np.ndarray, actions, *, V: int | None = None, row_begin: int = 0,
+                 row_end: int | None = None, row_offset: int = 0) -> LogpEntropy:
+    """The sampled action's log-prob and the policy entropy -sum p log p for token rows [row_begin, row_end).
+
+    ``logits`` is [rows_held, ld] (float32, bfloat16 bit patterns as uint16, or float64) holding token rows
+    from ``row_offset`` on; ``actions`` is indexed by absolute token number, the outputs by t - row_begin.
+    """
+    lib = _load()
+    logits = np.ascontiguousarray(logits)
+    dt = _logits_dtype(logits)
+    ld = logits.shape[1]
+    V = ld if V is None else int(V)
+    assert 1 <= V <= ld
+    if row_end is None:
+        row_end = row_offset + logits.shape[0]
+    assert row_begin >= row_offset and row_end - row_offset <= logits.shape[0]
+    a = _c(actions, np.int32)
+    n = row_end - row_begin
+    logp = np.empty(n, np.float64)
+    ent = np.empty(n, np.float64)
+    base = logits.ctypes.data - row_offset * ld * logits.itemsize
+    f = lib.oracle_logp_entropy(ctypes.c_void_p(base), dt, V, ld, _ptr(a), row_begin, row_end, _ptr(logp),
+                                _ptr(ent))
+    return LogpEntropy(logp, ent, int(f))

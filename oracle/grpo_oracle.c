@@ -20,6 +20,9 @@
  * The per-token log-probability of the sampled action is the log-softmax of
  * the policy's vocabulary logits at that token (implied by Eq. 1; the paper
  * never spells the kernel out).  The loss handed to the optimiser is -J.
+ * Forward only (oracle_logp_entropy): that log-probability and the policy
+ * entropy -sum p log p per token, the quantity of the GRPO vs. RAFT++
+ * comparison (Sec. 5).
  *
  * Readings where the paper is silent are listed with the library's design
  * notes; the ones that matter here: std uses `ddof` (default 1) and a zero
@@ -253,4 +256,40 @@ double oracle_reduce(const double* token_contrib, const int32_t* tok_traj, int64
 }
 
 /* Threads the row loop runs on (for reporting the oracle's timing). */
+/* ---- forward only: the action's log-prob and the policy entropy ---------- */
+
+/* Per token row t in [row_begin, row_end): l_t = z[a_t] - lse(z) (the
+ * log-softmax at the sampled action; what a proximal-policy recompute
+ * produces, Table 5 "proximal logprobs recomputed") and the policy entropy
+ * H_t = -sum_v p_v log p_v with p = softmax(z), the per-token quantity the
+ * paper averages over the loss mask (Sec. 5, GRPO vs. RAFT++).  Written from
+ * the definitions: log p_v = z_v - lse, p_v = exp(log p_v); a term whose p_v
+ * underflows to zero contributes its limit, zero.  An action outside [0, V)
+ * gives l_t = 0 and ORACLE_ERR_ACTION; the entropy does not depend on it.
+ * Outputs are indexed by t - row_begin. */
+int oracle_logp_entropy(const void* logits, int dtype, int64_t V, int64_t ld, const int32_t* actions,
+                        int64_t row_begin, int64_t row_end, double* token_logp, double* token_entropy) {
+  int flags = 0;
+#pragma omp parallel for reduction(| : flags) schedule(static)
+  for (int64_t t = row_begin; t < row_end; ++t) {
+    const int64_t q = t - row_begin;
+    const int64_t base = t * ld;
+    const double lse = row_logsumexp(logits, dtype, base, V);
+    double H = 0.0;
+    for (int64_t v = 0; v < V; ++v) {
+      const double logp = load_elem(logits, dtype, base + v) - lse;
+      const double p = exp(logp);
+      if (p > 0.0) H -= p * logp;
+    }
+    const int32_t a = actions[t];
+    double l = 0.0;
+    if (a < 0 || (int64_t)a >= V) flags |= ORACLE_ERR_ACTION;
+    else l = load_elem(logits, dtype, base + a) - lse;
+    if (!isfinite(lse)) flags |= ORACLE_ERR_NONFINITE;
+    if (token_logp) token_logp[q] = l;
+    if (token_entropy) token_entropy[q] = H;
+  }
+  return flags;
+}
+
 int oracle_threads(void) { return omp_get_max_threads(); }
