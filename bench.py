@@ -65,6 +65,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (0 = skip)")
     ap.add_argument("--fused-steps", type=int, default=3, help="timed steps of the fused path (0 = skip)")
+    ap.add_argument("--logp-steps", type=int, default=10,
+                    help="timed steps of the forward-only log-prob + entropy path (0 = skip)")
     ap.add_argument("--skip-logits", action="store_true", help="measure only the fused path")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter calibration)")
@@ -111,6 +113,36 @@ def cpu_baseline(b: dict, adv64, budget_s: float) -> dict:
     return {"value": rows / el, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
             "sample": f"first {R} token rows of the same batch (loss + fp64 dlogits), cycled in blocks of "
                       f"{chunk}; {rows} rows in {el:.1f} s"}
+
+
+def bench_logp(b: dict, steps: int, warmup: int = 2) -> dict:
+    """Times grpo_token_logp (action log-prob + entropy, forward only) on the resident logits batch."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    T, V = b["logits"].shape
+    stream = torch.cuda.current_stream()
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for _ in range(warmup):
+        grpo.grpo_token_logp(b["logits"], b["actions"])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev0[i].record(stream)
+        grpo.grpo_token_logp(b["logits"], b["actions"])
+        ev1[i].record(stream)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(steps)) / steps
+    alg = T * (2.0 * V + 12.0)  # logits row read once, action id read, log-prob and entropy written
+    achieved = alg / (hot_ms * 1e-3) / 1e9
+    return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
+            "workload": f"forward only: action log-prob and entropy of the same {T} x {V} bf16 logits",
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                         "kernel": "k_logp_vec<bf16, 256, 4> (one workgroup per row)", "kernel_ms": hot_ms,
+                         "algorithmic_bytes_per_launch": alg}}
 
 
 def bench_fused(steps: int, warmup: int = 1) -> dict:
@@ -253,6 +285,8 @@ def main():
         import oracle
         A = oracle.advantages(st.rewards, cfg.G).astype(np.float32).astype(np.float64)
         out["cpu_baseline"] = cpu_baseline(b, A, args.cpu_seconds)
+    if args.logp_steps > 0:
+        out["token_logp"] = bench_logp(b, args.logp_steps)
     if args.fused_steps > 0:
         del b
         torch.cuda.empty_cache()

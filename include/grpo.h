@@ -181,6 +181,29 @@ int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T, int64_t H
                       float* dw_lm, int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
                       hipStream_t s);
 
+/*
+ * Forward only: the sampled action's log-prob and the policy entropy of each
+ * token row, with no loss and no dlogits -- the proximal log-probs recomputed
+ * before an update (Table 5: decoupled PPO, proximal logprobs recomputed) and
+ * the per-token entropy the paper averages over the loss mask (Sec. 5).
+ *   l_t = z_t[a_t] - log sum_v exp z_t[v],   H_t = -sum_v p_v log p_v,  p = softmax(z_t)
+ *   logits       device [T, ld] of `dt`, row t = token t; columns >= V unread
+ *   T >= 0, 1 <= V <= ld
+ *   actions      device int32 [T]
+ *   token_logp   device fp32 [T] or NULL   l_t (0 where a_t is outside [0, V))
+ *   token_entropy device fp32 [T] or NULL  H_t
+ *   error_flags  device int32 [1] or NULL: overwritten with GRPO_FLAG_ACTION when
+ *                some a_t is outside [0, V), GRPO_FLAG_NONFINITE when a row's
+ *                log-sum-exp is not finite
+ * Each row is read once (2V or 4V bytes); sums run in fp32 per thread and fp64
+ * across the row.
+ * Errors: GRPO_ERR_ARG (logits or actions NULL), GRPO_ERR_SHAPE (T < 0, V < 1,
+ *   ld < V, T >= 2^31), GRPO_ERR_DTYPE, GRPO_ERR_ALIGN (logits not aligned to
+ *   the element size), GRPO_ERR_HIP.
+ */
+int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const int32_t* actions,
+                    float* token_logp, float* token_entropy, int32_t* error_flags, hipStream_t s);
+
 /* A static, human-readable name for a grpo_status value. */
 const char* grpo_status_str(int status);
 

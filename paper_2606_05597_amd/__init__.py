@@ -18,7 +18,7 @@ from ._lib import (GRPO_BF16, GRPO_F32, GRPO_FLAG_ACTION, GRPO_FLAG_NONFINITE, G
                    GRPO_NORM_CONST_K, GRPO_NORM_TRAJ_STEPS, GrpoError)
 
 __all__ = ["grpo_advantages", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
-           "fused_lmhead_grpo", "grpo_status_str", "LossAux", "GrpoError"]
+           "fused_lmhead_grpo", "grpo_token_logp", "grpo_status_str", "LossAux", "GrpoError"]
 
 
 def _ptr(t):
@@ -232,3 +232,33 @@ def fused_lmhead_grpo(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.T
         ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "fused_lmhead_grpo")
     return loss_out, dhidden, dw_lm
+
+
+def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | None = None, entropy: bool = True,
+                    error_flags: torch.Tensor | None = None, stream=None):
+    """Forward only: each token row's action log-prob and (optionally) policy entropy, both fp32 [T].
+
+    ``logits`` is [T, ld] (bf16 or fp32, unit column stride); V defaults to the column count.
+    ``error_flags`` (int32 [1], optional) receives GRPO_FLAG_* bits.  Returns (logp, entropy or None).
+    """
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be [T, ld] with unit column stride")
+    if not logits.is_cuda:
+        raise ValueError("logits must be a GPU tensor (no CPU path)")
+    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
+    if dt is None:
+        raise TypeError("logits must be bfloat16 or float32")
+    T = logits.shape[0]
+    ld = logits.stride(0) if T > 0 else logits.shape[1]
+    Vv = logits.shape[1] if V is None else int(V)
+    _dev(actions, "actions")
+    if actions.dtype != torch.int32:
+        raise TypeError("actions must be int32")
+    logp = torch.empty(T, dtype=torch.float32, device=logits.device)
+    ent = torch.empty(T, dtype=torch.float32, device=logits.device) if entropy else None
+    if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
+        raise ValueError("error_flags must be an int32 GPU tensor")
+    st = _lib.load().grpo_token_logp(_ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(logp), _ptr(ent),
+                                     _ptr(error_flags), _stream(stream))
+    _check(st, "grpo_token_logp")
+    return logp, ent

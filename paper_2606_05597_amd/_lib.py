@@ -73,6 +73,8 @@ def load() -> ctypes.CDLL:
         lib.fused_lmhead_grpo.argtypes = [P, P, I64, I64, I64, I32, P, P, P, P, ctypes.POINTER(Segments),
                                           ctypes.POINTER(LossParams), P, P, P, I32, ctypes.POINTER(Aux), P, SZ, P]
         lib.fused_lmhead_grpo.restype = ctypes.c_int
+        lib.grpo_token_logp.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P, P]
+        lib.grpo_token_logp.restype = ctypes.c_int
         lib.grpo_status_str.argtypes = [ctypes.c_int]
         lib.grpo_status_str.restype = ctypes.c_char_p
         _lib = lib

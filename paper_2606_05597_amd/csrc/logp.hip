@@ -1,0 +1,204 @@
+// Forward only: the sampled action's log-prob and the policy entropy of each
+// token row (the proximal log-probs recomputed before an update, Table 5, and
+// the per-token entropy of Sec. 5), one workgroup per row.
+//
+// A row is read once.  Each thread walks its 16-byte vectors U at a time (all U
+// loads in flight together) and keeps, relative to its running shift m,
+//   s = sum e^(z - m)   and   t = sum e^(z - m) (z - m),
+// rescaling both when a chunk raises m.  For any shift m >= max z the row's
+// log-sum-exp is m + log s and its entropy -sum p log p = log s - t / s; both
+// terms of the entropy are >= 0, so it has no cancellation even when small.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "device.h"
+#include "host.h"
+
+namespace grpo {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct LogpArgs {
+  const void* logits;
+  int64_t ld, V;
+  int T;
+  const int32_t* actions;
+  float* logp;      // nullable
+  float* entropy;   // nullable
+  int32_t* flags;   // nullable
+};
+
+// One element folded into (s, t) at the current shift m.
+__device__ __forceinline__ void fold(float z, float m, float nmb, float& s, float& t) {
+  const float e = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, nmb));
+  s += e;
+  t = fmaf(e, z - m, t);
+}
+
+// Raises the shift to mn >= m: s and t are re-expressed relative to mn.
+__device__ __forceinline__ void rescale(float& m, float mn, float& s, float& t) {
+  if (mn > m) {
+    if (m != -INFINITY) {
+      const float d = mn - m, f = __builtin_amdgcn_exp2f(-d * kLog2e);
+      t = f * fmaf(-d, s, t);
+      s *= f;
+    }
+    m = mn;
+  }
+}
+
+// Combines every thread's (m, s, t) into the row's (M, S, T) in fp64, valid in thread 0.
+template <int NW>
+__device__ __forceinline__ void block_combine3(float m, float s, float t, float* sh_m, double* sh_s, double* sh_t,
+                                               double& M_out, double& S_out, double& T_out) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const float mw = wave_max(m);
+  const double f = (m == -INFINITY) ? 0.0 : (double)__builtin_amdgcn_exp2f((m - mw) * kLog2e);
+  const double sw = wave_sum(f * (double)s);
+  const double tw = wave_sum(m == -INFINITY ? 0.0 : f * ((double)t + ((double)m - (double)mw) * (double)s));
+  if (lane == 0) {
+    sh_m[wv] = mw;
+    sh_s[wv] = sw;
+    sh_t[wv] = tw;
+  }
+  __syncthreads();
+  if (wv == 0) {
+    const float mq = lane < NW ? sh_m[lane] : -INFINITY;
+    const float M = wave_max(mq);
+    const double g = (mq == -INFINITY) ? 0.0 : exp((double)mq - (double)M);
+    const int q = lane < NW ? lane : 0;
+    const double S = wave_sum(g * sh_s[q]);
+    const double T = wave_sum(mq == -INFINITY ? 0.0 : g * (sh_t[q] + ((double)mq - (double)M) * sh_s[q]));
+    M_out = (double)M;
+    S_out = S;
+    T_out = T;
+  }
+}
+
+// Element e of a 16-byte vector (8 bf16 or 4 fp32), widened to fp32.
+template <typename Tin>
+__device__ __forceinline__ float elem(const u32x4& x, int e) {
+  if constexpr (sizeof(Tin) == 2) {
+    const uint32_t w = x[e >> 1];
+    return (e & 1) ? bf16_hi(w) : bf16_lo(w);
+  } else {
+    return __uint_as_float(x[e]);
+  }
+}
+
+template <typename Tin>
+__device__ __forceinline__ void row_out(const LogpArgs& a, int t, double M, double S, double Tsum, double za,
+                                        bool act_ok) {
+  const double lse = M + log(S);
+  if (a.logp) a.logp[t] = act_ok ? (float)(za - lse) : 0.f;
+  if (a.entropy) a.entropy[t] = (float)(log(S) - Tsum / S);
+  if (a.flags) {
+    if (!act_ok) atomicOr(a.flags, GRPO_FLAG_ACTION);
+    if (!isfinite(lse)) atomicOr(a.flags, GRPO_FLAG_NONFINITE);
+  }
+}
+
+// Rows of 16-byte vectors (V a multiple of the vector width, 16-byte aligned rows).
+template <typename Tin, int NT, int U>
+__global__ __launch_bounds__(NT) void k_logp_vec(const LogpArgs a) {
+  constexpr int EPV = 16 / sizeof(Tin), NW = NT / 64;
+  __shared__ float sh_m[NW];
+  __shared__ double sh_s[NW], sh_t[NW];
+  __shared__ float sh_za;
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const int nvec = (int)(a.V / EPV);
+  const u32x4* row = reinterpret_cast<const u32x4*>(static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld);
+  const int act = a.actions[t];
+  const bool act_ok = act >= 0 && (int64_t)act < a.V;
+  const int act_vec = act_ok ? act / EPV : -1;
+  float m = -INFINITY, s = 0.f, tt = 0.f;
+  for (int base = tid; base < nvec; base += NT * U) {
+    u32x4 x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int vi = base + u * NT;
+      if (vi < nvec) x[u] = __builtin_nontemporal_load(row + vi);
+    }
+    float cm = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int vi = base + u * NT;
+      if (vi < nvec) {
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) cm = fmaxf(cm, elem<Tin>(x[u], e));
+        if (vi == act_vec) sh_za = elem<Tin>(x[u], act % EPV);
+      }
+    }
+    rescale(m, cm, s, tt);
+    const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int vi = base + u * NT;
+      if (vi < nvec) {
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) fold(elem<Tin>(x[u], e), m, nmb, s, tt);
+      }
+    }
+  }
+  double M, S, Tsum;
+  block_combine3<NW>(m, s, tt, sh_m, sh_s, sh_t, M, S, Tsum);  // its barrier publishes sh_za
+  if (tid == 0) row_out<Tin>(a, t, M, S, Tsum, act_ok ? (double)sh_za : 0.0, act_ok);
+}
+
+template <typename Tin>
+__device__ __forceinline__ float load_one(const Tin* p);
+template <>
+__device__ __forceinline__ float load_one<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_one<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+// Any V, ld and element alignment: element loads, the row read twice (shift, then sums).
+template <typename Tin>
+__global__ __launch_bounds__(256) void k_logp_generic(const LogpArgs a) {
+  constexpr int NT = 256, NW = NT / 64;
+  __shared__ float sh_m[NW];
+  __shared__ double sh_s[NW], sh_t[NW];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const Tin* row = static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld;
+  float m = -INFINITY;
+  for (int64_t v = tid; v < a.V; v += NT) m = fmaxf(m, load_one<Tin>(row + v));
+  const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
+  float s = 0.f, tt = 0.f;
+  if (m != -INFINITY)
+    for (int64_t v = tid; v < a.V; v += NT) fold(load_one<Tin>(row + v), m, nmb, s, tt);
+  double M, S, Tsum;
+  block_combine3<NW>(m, s, tt, sh_m, sh_s, sh_t, M, S, Tsum);
+  if (tid == 0) {
+    const int act = a.actions[t];
+    const bool act_ok = act >= 0 && (int64_t)act < a.V;
+    row_out<Tin>(a, t, M, S, Tsum, act_ok ? (double)load_one<Tin>(row + act) : 0.0, act_ok);
+  }
+}
+
+__global__ void k_clear_flag(int32_t* f) { *f = 0; }
+
+}  // namespace grpo
+
+using namespace grpo;
+
+extern "C" int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                               const int32_t* actions, float* token_logp, float* token_entropy, int32_t* error_flags,
+                               hipStream_t s) {
+  if (T < 0 || T >= ((int64_t)1 << 31) || V < 1 || ld < V) return GRPO_ERR_SHAPE;
+  if (T > 0 && (!logits || !actions)) return GRPO_ERR_ARG;
+  if (dt != GRPO_F32 && dt != GRPO_BF16) return GRPO_ERR_DTYPE;
+  const int esz = (dt == GRPO_BF16) ? 2 : 4;
+  if (!aligned(logits, esz)) return GRPO_ERR_ALIGN;
+  if (error_flags) hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, error_flags);
+  if (T > 0) {
+    LogpArgs a{logits, ld, V, (int)T, actions, token_logp, token_entropy, error_flags};
+    const int epv = 16 / esz;
+    const bool vec = V % epv == 0 && ld % epv == 0 && aligned(logits, 16);
+    const dim3 grid((unsigned)T);
+    if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_logp_vec<uint16_t, 256, 4>), grid, dim3(256), 0, s, a);
+    else if (vec) hipLaunchKernelGGL((k_logp_vec<float, 256, 4>), grid, dim3(256), 0, s, a);
+    else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_logp_generic<uint16_t>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_logp_generic<float>, grid, dim3(256), 0, s, a);
+  }
+  return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+}

@@ -33,7 +33,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["grpo_advantages", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd",
-                                           "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_status_str"])
+                                           "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_token_logp",
+                                           "grpo_status_str"])
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -152,3 +153,22 @@ def call_fused(lib, *, T=8, H=64, V=512, chunk=256, hidden=D, w=D, dh=D, dw=D, w
 ])
 def test_fused_rejects_bad_arguments(lib, kw, status):
     assert call_fused(lib, **kw) == status
+
+
+def call_logp(lib, *, logits=D, dt=_lib.GRPO_BF16, T=8, V=64, ld=64, actions=D):
+    return lib.grpo_token_logp(logits, dt, T, V, ld, actions, D, D, None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(logits=None), _lib.GRPO_ERR_ARG),
+    (dict(actions=None), _lib.GRPO_ERR_ARG),
+    (dict(T=-1), _lib.GRPO_ERR_SHAPE),
+    (dict(T=1 << 31), _lib.GRPO_ERR_SHAPE),
+    (dict(V=0), _lib.GRPO_ERR_SHAPE),
+    (dict(ld=63), _lib.GRPO_ERR_SHAPE),
+    (dict(dt=7), _lib.GRPO_ERR_DTYPE),
+    (dict(logits=ctypes.c_void_p(0x100001)), _lib.GRPO_ERR_ALIGN),
+    (dict(logits=ctypes.c_void_p(0x100002), dt=_lib.GRPO_F32), _lib.GRPO_ERR_ALIGN),
+])
+def test_token_logp_rejects_bad_arguments(lib, kw, status):
+    assert call_logp(lib, **kw) == status
