@@ -57,6 +57,10 @@ def _load():
         lib.oracle_loss_rows.restype = ctypes.c_int
         lib.oracle_reduce.argtypes = [P, P, I64, I32, P]
         lib.oracle_reduce.restype = D
+        lib.oracle_advantages_success_filter.argtypes = [P, I32, P]
+        lib.oracle_advantages_success_filter.restype = None
+        lib.oracle_mixed_groups.argtypes = [P, I32, I32, P]
+        lib.oracle_mixed_groups.restype = I32
         lib.oracle_logp_entropy.argtypes = [P, ctypes.c_int, I64, I64, P, I64, I64, P, P]
         lib.oracle_logp_entropy.restype = ctypes.c_int
         lib.oracle_threads.argtypes = []
@@ -104,13 +108,32 @@ def gather_index(T: int, ld: int, actions) -> np.ndarray:
     return np.arange(T, dtype=np.int64) * np.int64(ld) + np.asarray(actions, dtype=np.int64)
 
 
-def advantages(rewards, group_size: int, ddof: int = 1, std_eps: float = 0.0) -> np.ndarray:
-    """Group-relative advantage of Sec. 3.2, fp64."""
+ADV_GROUP_NORM = 0        # (r - mean) / (std + std_eps) per group (Sec. 3.2)
+ADV_SUCCESS_FILTER = 1    # RAFT++ / filtered BC: 1[r > 0], no group normalisation (Sec. 3.2, Table 5)
+
+
+def advantages(rewards, group_size: int, ddof: int = 1, std_eps: float = 0.0,
+               mode: int = ADV_GROUP_NORM) -> np.ndarray:
+    """Per-trajectory advantage, fp64: group-relative (Sec. 3.2) or the RAFT++ success filter."""
     lib = _load()
     r = _c(rewards, np.float32)
     out = np.empty(len(r), np.float64)
-    lib.oracle_advantages(_ptr(r), len(r), group_size, ddof, float(std_eps), _ptr(out))
+    if mode == ADV_GROUP_NORM:
+        lib.oracle_advantages(_ptr(r), len(r), group_size, ddof, float(std_eps), _ptr(out))
+    elif mode == ADV_SUCCESS_FILTER:
+        lib.oracle_advantages_success_filter(_ptr(r), len(r), _ptr(out))
+    else:
+        raise ValueError(f"unknown advantage mode {mode}")
     return out
+
+
+def mixed_groups(rewards, group_size: int):
+    """DAPO dynamic sampling (Sec. 3.2): per group, 1 when its rewards are not all equal; and their count."""
+    lib = _load()
+    r = _c(rewards, np.float32)
+    mixed = np.empty(len(r) // group_size, np.int32)
+    n = lib.oracle_mixed_groups(_ptr(r), len(r), group_size, _ptr(mixed))
+    return mixed, int(n)
 
 
 @dataclass

@@ -120,6 +120,30 @@ void oracle_advantages(const float* rewards, int32_t n_traj, int32_t G, int32_t 
   }
 }
 
+/* RAFT++ / filtered behaviour cloning (Sec. 3.2, "RAFT++ as a baseline";
+ * Table 5): group normalisation is off and the advantage is the success
+ * filter, A_i = 1 when r_i > 0 and 0 otherwise, so only successful
+ * trajectories carry gradient. */
+void oracle_advantages_success_filter(const float* rewards, int32_t n_traj, double* adv) {
+  for (int32_t i = 0; i < n_traj; ++i) adv[i] = (rewards[i] > 0.0f) ? 1.0 : 0.0;
+}
+
+/* DAPO dynamic sampling (Sec. 3.2): a group whose G rewards are all equal
+ * (all successes or all failures) carries no group-relative signal and is
+ * skipped.  mixed[g] = 1 when the rewards of group g are not all equal;
+ * returns the number of such groups. */
+int32_t oracle_mixed_groups(const float* rewards, int32_t n_traj, int32_t G, int32_t* mixed) {
+  int32_t n = 0;
+  for (int32_t g = 0; g * G < n_traj; ++g) {
+    int m = 0;
+    for (int32_t i = 1; i < G; ++i)
+      if (rewards[g * G + i] != rewards[g * G]) m = 1;
+    mixed[g] = m;
+    n += m;
+  }
+  return n;
+}
+
 /* ---- per-token log-probability: log-softmax over V, then gather --------- */
 
 /* lse = log sum_v exp(z_v), computed as m + log sum exp(z_v - m). */
