@@ -119,6 +119,28 @@ typedef struct {
 int grpo_advantages(const float* rewards, int32_t n_traj, int32_t group_size, int32_t ddof, float std_eps,
                     float* adv_out, hipStream_t s);
 
+/* Advantage modes of grpo_advantages_ex. */
+typedef enum {
+  GRPO_ADV_GROUP_NORM = 0,     /* (r_i - mean)/(std + std_eps) per group (Sec. 3.2)                    */
+  GRPO_ADV_SUCCESS_FILTER = 1  /* RAFT++ / filtered behaviour cloning: A_i = 1 if r_i > 0 else 0, no   */
+                               /* group normalisation (Sec. 3.2 "RAFT++ as a baseline", Table 5)       */
+} grpo_adv_mode;
+
+/*
+ * grpo_advantages with a mode and DAPO's dynamic-sampling mask (Sec. 3.2: groups
+ * whose rewards are all equal, all successes or all failures, carry no
+ * group-relative signal and are skipped when a training batch is gathered).
+ *   mode         grpo_adv_mode
+ *   group_mixed  device int32 [n_traj / group_size] or NULL: 1 when the
+ *                group's rewards are not all equal, else 0
+ *   n_mixed      device int32 [1] or NULL: the number of mixed groups (what a
+ *                caller that drops the other groups passes as n_groups_total)
+ * Other arguments and errors as grpo_advantages, plus GRPO_ERR_ARG for an
+ * unknown mode.  ddof and std_eps are checked but unused under the filter.
+ */
+int grpo_advantages_ex(const float* rewards, int32_t n_traj, int32_t group_size, int32_t mode, int32_t ddof,
+                       float std_eps, float* adv_out, int32_t* group_mixed, int32_t* n_mixed, hipStream_t s);
+
 /* Bytes of device workspace grpo_loss_fwd_bwd needs for T tokens and n_traj trajectories. */
 size_t grpo_loss_workspace_bytes(int64_t T, int32_t n_traj);
 

@@ -14,10 +14,11 @@ from dataclasses import dataclass, field
 import torch
 
 from . import _lib
-from ._lib import (GRPO_BF16, GRPO_F32, GRPO_FLAG_ACTION, GRPO_FLAG_NONFINITE, GRPO_FLAG_OFFSETS,  # noqa: F401
-                   GRPO_NORM_CONST_K, GRPO_NORM_TRAJ_STEPS, GrpoError)
+from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO_F32,  # noqa: F401
+                   GRPO_FLAG_ACTION, GRPO_FLAG_NONFINITE, GRPO_FLAG_OFFSETS, GRPO_NORM_CONST_K,
+                   GRPO_NORM_TRAJ_STEPS, GrpoError)
 
-__all__ = ["grpo_advantages", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
+__all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
            "fused_lmhead_grpo", "grpo_token_logp", "grpo_status_str", "LossAux", "GrpoError"]
 
 
@@ -58,6 +59,24 @@ def grpo_advantages(rewards: torch.Tensor, group_size: int, ddof: int = 1, std_e
                                      _ptr(out), _stream(stream))
     _check(st, "grpo_advantages")
     return out
+
+
+def grpo_advantages_ex(rewards: torch.Tensor, group_size: int, mode: int = GRPO_ADV_GROUP_NORM, ddof: int = 1,
+                       std_eps: float = 0.0, out: torch.Tensor | None = None, mixed: bool = True, stream=None):
+    """Advantages under ``mode`` (group-normalised, or the RAFT++ success filter) and, with ``mixed``, DAPO's
+    mixed-group mask (int32 [N / G]) and count (int32 [1]).  Returns (adv, group_mixed or None, n_mixed or None)."""
+    _dev(rewards, "rewards")
+    if rewards.dtype != torch.float32:
+        raise TypeError("rewards must be float32")
+    out = torch.empty_like(rewards) if out is None else _dev(out, "out")
+    gm = nm = None
+    if mixed:
+        gm = torch.empty(max(rewards.numel() // max(int(group_size), 1), 1), dtype=torch.int32, device=rewards.device)
+        nm = torch.empty(1, dtype=torch.int32, device=rewards.device)
+    st = _lib.load().grpo_advantages_ex(_ptr(rewards), rewards.numel(), int(group_size), int(mode), int(ddof),
+                                        float(std_eps), _ptr(out), _ptr(gm), _ptr(nm), _stream(stream))
+    _check(st, "grpo_advantages_ex")
+    return out, gm, nm
 
 
 def grpo_loss_workspace_bytes(T: int, n_traj: int) -> int:

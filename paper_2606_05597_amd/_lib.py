@@ -19,6 +19,8 @@ GRPO_F32 = 0
 GRPO_BF16 = 1
 GRPO_NORM_TRAJ_STEPS = 0
 GRPO_NORM_CONST_K = 1
+GRPO_ADV_GROUP_NORM = 0
+GRPO_ADV_SUCCESS_FILTER = 1
 
 GRPO_FLAG_ACTION = 1
 GRPO_FLAG_OFFSETS = 2
@@ -62,6 +64,8 @@ def load() -> ctypes.CDLL:
         I32, I64, SZ = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
         lib.grpo_advantages.argtypes = [P, I32, I32, I32, ctypes.c_float, P, P]
         lib.grpo_advantages.restype = ctypes.c_int
+        lib.grpo_advantages_ex.argtypes = [P, I32, I32, I32, I32, ctypes.c_float, P, P, P, P]
+        lib.grpo_advantages_ex.restype = ctypes.c_int
         lib.grpo_loss_workspace_bytes.argtypes = [I64, I32]
         lib.grpo_loss_workspace_bytes.restype = SZ
         lib.grpo_loss_fwd_bwd.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P,

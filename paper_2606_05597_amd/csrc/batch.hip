@@ -225,10 +225,24 @@ hipError_t launch_reduce(int64_t T, int32_t n_traj, char* ws, const LossWs& L, d
 // ---- group advantages (Sec. 3.2) -------------------------------------------------
 // One workgroup per group; the moments are summed serially in fp64 so the
 // result does not depend on the launch shape.
-__global__ __launch_bounds__(64) void k_advantages(const float* __restrict__ r, int G, int ddof, double std_eps,
-                                                   float* __restrict__ adv) {
+// mode GRPO_ADV_SUCCESS_FILTER: A_i = 1[r_i > 0] (RAFT++, Sec. 3.2 / Table 5).
+// mixed (nullable): 1 when the group's rewards are not all equal (DAPO dynamic
+// sampling, Sec. 3.2); n_mixed (nullable, cleared beforehand) counts them.
+__global__ __launch_bounds__(64) void k_advantages(const float* __restrict__ r, int G, int mode, int ddof,
+                                                   double std_eps, float* __restrict__ adv,
+                                                   int32_t* __restrict__ mixed, int32_t* __restrict__ n_mixed) {
   __shared__ double sh_mean, sh_den;
   const int64_t base = (int64_t)blockIdx.x * G;
+  if (threadIdx.x == 0 && (mixed || n_mixed)) {
+    int m = 0;
+    for (int q = 1; q < G; ++q) m |= (r[base + q] != r[base]);
+    if (mixed) mixed[blockIdx.x] = m;
+    if (n_mixed && m) atomicAdd(n_mixed, 1);
+  }
+  if (mode == GRPO_ADV_SUCCESS_FILTER) {
+    for (int q = threadIdx.x; q < G; q += 64) adv[base + q] = (r[base + q] > 0.f) ? 1.f : 0.f;
+    return;
+  }
   if (threadIdx.x == 0) {
     double mean = 0.0;
     for (int q = 0; q < G; ++q) mean += (double)r[base + q];
@@ -250,15 +264,28 @@ __global__ __launch_bounds__(64) void k_advantages(const float* __restrict__ r, 
 
 }  // namespace grpo
 
-extern "C" int grpo_advantages(const float* rewards, int32_t n_traj, int32_t group_size, int32_t ddof,
-                               float std_eps, float* adv_out, hipStream_t s) {
+namespace grpo {
+__global__ void k_clear_i32(int32_t* p) { *p = 0; }
+}  // namespace grpo
+
+extern "C" int grpo_advantages_ex(const float* rewards, int32_t n_traj, int32_t group_size, int32_t mode,
+                                  int32_t ddof, float std_eps, float* adv_out, int32_t* group_mixed,
+                                  int32_t* n_mixed, hipStream_t s) {
   if (!rewards || !adv_out) return GRPO_ERR_ARG;
+  if (mode != GRPO_ADV_GROUP_NORM && mode != GRPO_ADV_SUCCESS_FILTER) return GRPO_ERR_ARG;
   if (ddof != 0 && ddof != 1) return GRPO_ERR_ARG;
   if (!(std_eps >= 0.f) || !isfinite(std_eps)) return GRPO_ERR_ARG;
   if (n_traj < 1 || group_size < 1 || n_traj % group_size != 0) return GRPO_ERR_SHAPE;
-  hipLaunchKernelGGL(grpo::k_advantages, dim3(n_traj / group_size), dim3(64), 0, s, rewards, group_size, ddof,
-                     (double)std_eps, adv_out);
+  if (n_mixed) hipLaunchKernelGGL(grpo::k_clear_i32, dim3(1), dim3(1), 0, s, n_mixed);
+  hipLaunchKernelGGL(grpo::k_advantages, dim3(n_traj / group_size), dim3(64), 0, s, rewards, group_size, mode, ddof,
+                     (double)std_eps, adv_out, group_mixed, n_mixed);
   return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+}
+
+extern "C" int grpo_advantages(const float* rewards, int32_t n_traj, int32_t group_size, int32_t ddof,
+                               float std_eps, float* adv_out, hipStream_t s) {
+  return grpo_advantages_ex(rewards, n_traj, group_size, GRPO_ADV_GROUP_NORM, ddof, std_eps, adv_out, nullptr,
+                            nullptr, s);
 }
 
 extern "C" const char* grpo_status_str(int status) {

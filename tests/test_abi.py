@@ -32,7 +32,8 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == sorted(["grpo_advantages", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd",
+    assert declared_functions() == sorted(["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes",
+                                           "grpo_loss_fwd_bwd",
                                            "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_token_logp",
                                            "grpo_status_str"])
 
@@ -172,3 +173,14 @@ def call_logp(lib, *, logits=D, dt=_lib.GRPO_BF16, T=8, V=64, ld=64, actions=D):
 ])
 def test_token_logp_rejects_bad_arguments(lib, kw, status):
     assert call_logp(lib, **kw) == status
+
+
+def test_advantages_ex_rejects_bad_arguments(lib):
+    f = lib.grpo_advantages_ex
+    assert f(D, 8, 8, 2, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_ARG       # unknown mode
+    assert f(D, 8, 8, -1, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_ARG
+    assert f(None, 8, 8, 0, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_ARG
+    assert f(D, 8, 8, 1, 1, 0.0, None, None, None, None) == _lib.GRPO_ERR_ARG
+    assert f(D, 8, 8, 1, 3, 0.0, D, None, None, None) == _lib.GRPO_ERR_ARG      # ddof checked under the filter too
+    assert f(D, 12, 8, 1, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_SHAPE
+    assert f(D, 0, 1, 1, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_SHAPE
