@@ -101,6 +101,10 @@ typedef struct {
   int64_t* gather_idx;   /* [T] flat element index t*ld + a_t of each action logit         */
   double* traj_loss;     /* [n_traj] -sum over the trajectory's tokens of w_i s_t          */
   int64_t* clip_counts;  /* [2] tokens whose gradient the eps clip / the dual clip cut     */
+  double* ratio_stats;   /* [8] over the tokens that enter the loss: sum r, min r, max r,   */
+                         /*   sum rho, min rho, max rho (r = pi/pi_prox, rho = pi/pi_behave, */
+                         /*   Sec. 3.2), the number of tokens with r outside               */
+                         /*   [1 - eps_low, 1 + eps_high], and the number of such tokens   */
   int32_t* error_flags;  /* [1] GRPO_FLAG_* bits seen by this call                         */
   hipEvent_t hot_begin;  /* host handles: when both are set, recorded on `s` right before  */
   hipEvent_t hot_end;    /*   and after the dominant kernel (for timing)                   */

@@ -96,12 +96,14 @@ class LossAux:
     gather_idx: torch.Tensor | None = None
     traj_loss: torch.Tensor | None = None
     clip_counts: torch.Tensor | None = None
+    ratio_stats: torch.Tensor | None = None
     error_flags: torch.Tensor | None = None
     hot_events: tuple | None = field(default=None)  # (begin, end) raw hipEvent_t handles
 
     @staticmethod
     def alloc(T: int, n_traj: int, device, which=("token_logp", "tok_traj", "traj_tok_off", "gather_idx",
-                                                   "traj_loss", "clip_counts", "error_flags")) -> "LossAux":
+                                                   "traj_loss", "clip_counts", "ratio_stats",
+                                                   "error_flags")) -> "LossAux":
         mk = {
             "token_logp": lambda: torch.empty(T, dtype=torch.float32, device=device),
             "tok_traj": lambda: torch.empty(T, dtype=torch.int32, device=device),
@@ -109,6 +111,7 @@ class LossAux:
             "gather_idx": lambda: torch.empty(T, dtype=torch.int64, device=device),
             "traj_loss": lambda: torch.empty(n_traj, dtype=torch.float64, device=device),
             "clip_counts": lambda: torch.empty(2, dtype=torch.int64, device=device),
+            "ratio_stats": lambda: torch.empty(8, dtype=torch.float64, device=device),
             "error_flags": lambda: torch.empty(1, dtype=torch.int32, device=device),
         }
         return LossAux(**{k: mk[k]() for k in which})
@@ -116,7 +119,7 @@ class LossAux:
     def _c(self):
         a = _lib.Aux()
         for name in ("token_logp", "tok_traj", "traj_tok_off", "gather_idx", "traj_loss", "clip_counts",
-                     "error_flags"):
+                     "ratio_stats", "error_flags"):
             t = getattr(self, name)
             setattr(a, name, None if t is None else _dev(t, name).data_ptr())
         if self.hot_events is not None:

@@ -42,7 +42,7 @@ class LossParams(ctypes.Structure):
 
 class Aux(ctypes.Structure):
     _fields_ = [("token_logp", P), ("tok_traj", P), ("traj_tok_off", P), ("gather_idx", P), ("traj_loss", P),
-                ("clip_counts", P), ("error_flags", P), ("hot_begin", P), ("hot_end", P)]
+                ("clip_counts", P), ("ratio_stats", P), ("error_flags", P), ("hot_begin", P), ("hot_end", P)]
 
 
 class GrpoError(RuntimeError):

@@ -53,8 +53,7 @@ __global__ __launch_bounds__(256) void k_segments(const SegArgs a) {
   if (tid == 0) {
     a.hdr->flags = bad ? GRPO_FLAG_OFFSETS : 0;
     a.hdr->done = 0;
-    a.hdr->counts[0] = 0;
-    a.hdr->counts[1] = 0;
+    for (int q = 0; q < 4; ++q) a.hdr->counts[q] = 0;
   }
 }
 
@@ -115,6 +114,7 @@ TokenArgs make_token_args(int64_t V, const int32_t* actions, const float* behave
   a.hdr = reinterpret_cast<WsHeader*>(ws + L.hdr);
   a.contrib = reinterpret_cast<double*>(ws + L.contrib);
   a.state = reinterpret_cast<int8_t*>(ws + L.state);
+  a.tok_ratio = reinterpret_cast<double2*>(ws + L.tok_ratio);
   a.token_logp = aux ? aux->token_logp : nullptr;
   a.lo = 1.0 - (double)p->eps_low;
   a.hi = 1.0 + (double)p->eps_high;
@@ -133,10 +133,13 @@ struct ReduceArgs {
   const int32_t* traj_tok_off;
   const double* contrib;
   const int8_t* state;
-  double* traj_loss;  // ws
+  const double2* tok_ratio;  // ws [T]: (r, rho), NaN outside the loss
+  double* traj_loss;         // ws
+  double* traj_rstats;       // ws [n_traj][6]: sum r, min r, max r, sum rho, min rho, max rho
   double* loss_out;
   double* aux_traj_loss;
   int64_t* aux_clip_counts;
+  double* aux_ratio_stats;
   int32_t* aux_error_flags;
 };
 
@@ -153,30 +156,73 @@ __device__ __forceinline__ double block_sum(double v, double* sh) {
   return r;  // valid in thread 0
 }
 
+template <int NT, bool MAX>
+__device__ __forceinline__ double block_ext(double v, double* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const double u = __shfl_xor(v, o, 64);
+    v = MAX ? fmax(v, u) : fmin(v, u);
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) sh[wv] = v;
+  __syncthreads();
+  double r = v;
+  if (threadIdx.x == 0)
+    for (int q = 0; q < NT / 64; ++q) r = MAX ? fmax(r, sh[q]) : fmin(r, sh[q]);
+  __syncthreads();
+  return r;  // valid in thread 0
+}
+
 __global__ __launch_bounds__(256) void k_reduce(const ReduceArgs a) {
   __shared__ double sh[4];
   __shared__ int is_last;
   const int i = blockIdx.x, tid = threadIdx.x;
   const int64_t t0 = min(max((int64_t)a.traj_tok_off[i], (int64_t)0), a.T);
   const int64_t t1 = min(max((int64_t)a.traj_tok_off[i + 1], t0), a.T);
-  double acc = 0.0;
-  int64_t c_eps = 0, c_dual = 0;
+  double acc = 0.0, sr = 0.0, srho = 0.0;
+  double rmin = INFINITY, rmax = -INFINITY, pmin = INFINITY, pmax = -INFINITY;
+  int64_t c_eps = 0, c_dual = 0, c_out = 0, c_valid = 0;
   for (int64_t t = t0 + tid; t < t1; t += 256) {
     acc += a.contrib[t];
     const int st = a.state[t];
-    c_eps += st & 1;
-    c_dual += (st >> 1) & 1;
+    c_eps += (st & kStateEpsCut) != 0;
+    c_dual += (st & kStateDualCut) != 0;
+    c_out += (st & kStateOutside) != 0;
+    if (st & kStateValid) {
+      ++c_valid;
+      const double2 q = a.tok_ratio[t];
+      sr += q.x;
+      srho += q.y;
+      rmin = fmin(rmin, q.x);
+      rmax = fmax(rmax, q.x);
+      pmin = fmin(pmin, q.y);
+      pmax = fmax(pmax, q.y);
+    }
   }
   const double tot = block_sum<256>(acc, sh);
+  const double tsr = block_sum<256>(sr, sh), tsrho = block_sum<256>(srho, sh);
+  const double trmin = block_ext<256, false>(rmin, sh), trmax = block_ext<256, true>(rmax, sh);
+  const double tpmin = block_ext<256, false>(pmin, sh), tpmax = block_ext<256, true>(pmax, sh);
   c_eps = wave_sum_i64(c_eps);
   c_dual = wave_sum_i64(c_dual);
-  if ((tid & 63) == 0 && (c_eps | c_dual)) {
+  c_out = wave_sum_i64(c_out);
+  c_valid = wave_sum_i64(c_valid);
+  if ((tid & 63) == 0 && (c_eps | c_dual | c_out | c_valid)) {
     atomicAdd((unsigned long long*)&a.hdr->counts[0], (unsigned long long)c_eps);
     atomicAdd((unsigned long long*)&a.hdr->counts[1], (unsigned long long)c_dual);
+    atomicAdd((unsigned long long*)&a.hdr->counts[2], (unsigned long long)c_out);
+    atomicAdd((unsigned long long*)&a.hdr->counts[3], (unsigned long long)c_valid);
   }
   __syncthreads();  // every wave's counter update is performed before the block reports done
   if (tid == 0) {
     a.traj_loss[i] = tot;
+    double* rs = a.traj_rstats + 6 * (int64_t)i;
+    rs[0] = tsr;
+    rs[1] = trmin;
+    rs[2] = trmax;
+    rs[3] = tsrho;
+    rs[4] = tpmin;
+    rs[5] = tpmax;
     __threadfence();
     const unsigned prev = atomicAdd(&a.hdr->done, 1u);
     is_last = (prev == (unsigned)gridDim.x - 1);
@@ -194,6 +240,36 @@ __global__ __launch_bounds__(256) void k_reduce(const ReduceArgs a) {
     for (int q = tid; q < a.n_traj; q += 256)
       a.aux_traj_loss[q] =
           bad ? (double)NAN : __hip_atomic_load(&a.traj_loss[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (a.aux_ratio_stats) {
+    // per-trajectory partials in index order (sums through the same fixed-shape tree as the loss)
+    auto ld = [&](int q, int k) {
+      return __hip_atomic_load(&a.traj_rstats[6 * (int64_t)q + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    double p_sr = 0.0, p_srho = 0.0, p_rmin = INFINITY, p_rmax = -INFINITY, p_pmin = INFINITY, p_pmax = -INFINITY;
+    for (int q = tid; q < a.n_traj; q += 256) {
+      p_sr += ld(q, 0);
+      p_rmin = fmin(p_rmin, ld(q, 1));
+      p_rmax = fmax(p_rmax, ld(q, 2));
+      p_srho += ld(q, 3);
+      p_pmin = fmin(p_pmin, ld(q, 4));
+      p_pmax = fmax(p_pmax, ld(q, 5));
+    }
+    const double v0 = block_sum<256>(p_sr, sh), v3 = block_sum<256>(p_srho, sh);
+    const double v1 = block_ext<256, false>(p_rmin, sh), v2 = block_ext<256, true>(p_rmax, sh);
+    const double v4 = block_ext<256, false>(p_pmin, sh), v5 = block_ext<256, true>(p_pmax, sh);
+    if (tid == 0) {
+      double* o = a.aux_ratio_stats;
+      const double nan = (double)NAN;
+      o[0] = bad ? nan : v0;
+      o[1] = bad ? nan : v1;
+      o[2] = bad ? nan : v2;
+      o[3] = bad ? nan : v3;
+      o[4] = bad ? nan : v4;
+      o[5] = bad ? nan : v5;
+      o[6] = (double)__hip_atomic_load(&a.hdr->counts[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      o[7] = (double)__hip_atomic_load(&a.hdr->counts[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
   if (tid == 0) {
     *a.loss_out = bad ? (double)NAN : loss;
     if (a.aux_clip_counts) {
@@ -213,10 +289,13 @@ hipError_t launch_reduce(int64_t T, int32_t n_traj, char* ws, const LossWs& L, d
   a.traj_tok_off = reinterpret_cast<const int32_t*>(ws + L.traj_tok_off);
   a.contrib = reinterpret_cast<const double*>(ws + L.contrib);
   a.state = reinterpret_cast<const int8_t*>(ws + L.state);
+  a.tok_ratio = reinterpret_cast<const double2*>(ws + L.tok_ratio);
   a.traj_loss = reinterpret_cast<double*>(ws + L.traj_loss);
+  a.traj_rstats = reinterpret_cast<double*>(ws + L.traj_rstats);
   a.loss_out = loss_out;
   a.aux_traj_loss = aux ? aux->traj_loss : nullptr;
   a.aux_clip_counts = aux ? aux->clip_counts : nullptr;
+  a.aux_ratio_stats = aux ? aux->ratio_stats : nullptr;
   a.aux_error_flags = aux ? aux->error_flags : nullptr;
   hipLaunchKernelGGL(k_reduce, dim3(n_traj), dim3(256), 0, s, a);
   return hipGetLastError();

@@ -12,7 +12,7 @@ namespace grpo {
 struct WsHeader {
   int32_t flags;      // GRPO_FLAG_* of this call (set by the segment pass, OR-ed by the row pass)
   uint32_t done;      // reduction workgroups finished (last-block pattern)
-  int64_t counts[2];  // eps-clip / dual-clip cut counts
+  int64_t counts[4];  // eps-clip cut, dual-clip cut, ratio outside the clip range, valid tokens
 };
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -55,10 +55,17 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 }
 
 // ---- per-token surrogate (Eq. 1 with the dual clip of Eq. 2) ----------------
+// Bits of the per-token state.
+constexpr int kStateEpsCut = 1;     // the eps clip held the term (its gradient is cut)
+constexpr int kStateDualCut = 2;    // the dual clip held it
+constexpr int kStateOutside = 4;    // r = pi/pi_prox lies outside [1 - eps_low, 1 + eps_high]
+constexpr int kStateValid = 8;      // the token entered the loss (action in range, offsets valid)
+
 struct TokenOut {
   double contrib;  // -w * s   (this token's share of the loss)
   double g;        // grad_scale * w * ds/dl
-  int state;       // bit 0: eps clip held the term, bit 1: dual clip held it
+  double rho, r;   // pi/pi_behave and pi/pi_prox
+  int state;       // kState* bits
 };
 
 // l: new log-prob, b: behave, p: prox, A: advantage, w: trajectory weight.
@@ -82,18 +89,20 @@ __device__ __forceinline__ TokenOut token_surrogate(double l, double b, double p
     s = u2;
     if (!inside) {
       ds = 0.0;
-      state = 1;
+      state = kStateEpsCut;
     }
   }
   if (c > 0.0 && A < 0.0 && s < c * A) {
     s = c * A;
     ds = 0.0;
-    state |= 2;
+    state |= kStateDualCut;
   }
   TokenOut o;
   o.contrib = -w * s;
   o.g = grad_scale * w * ds;
-  o.state = state;
+  o.rho = rho;
+  o.r = r;
+  o.state = state | (inside ? 0 : kStateOutside) | kStateValid;
   return o;
 }
 
@@ -121,6 +130,7 @@ struct TokenArgs {
   WsHeader* hdr;            // ws
   double* contrib;          // ws [T]
   int8_t* state;            // ws [T]
+  double2* tok_ratio;       // ws [T]: (r, rho) of each token, NaN for tokens outside the loss
   float* token_logp;        // aux, nullable
   double lo, hi, c, grad_scale;
 };
@@ -163,6 +173,7 @@ __device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn
     if (bad_act && !in.bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
     a.contrib[t] = in.bad_off ? (double)NAN : 0.0;
     a.state[t] = 0;
+    a.tok_ratio[t] = make_double2((double)NAN, (double)NAN);
     if (a.token_logp) a.token_logp[t] = 0.f;
     rs.nc = -INFINITY;  // every d_v = 0
     rs.sign = 1.f;
@@ -176,6 +187,7 @@ __device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn
   if (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) atomicOr(&a.hdr->flags, GRPO_FLAG_NONFINITE);
   a.contrib[t] = o.contrib;
   a.state[t] = (int8_t)o.state;
+  a.tok_ratio[t] = make_double2(o.r, o.rho);
   if (a.token_logp) a.token_logp[t] = (float)l;
   // d_v = g exp(z_v - lse) = sign(g) 2^(z_v L - lse L + log2|g|), with L = log2(e) as rounded on the device
   rs.nc = (float)(-lse * (double)kLog2e + log2(fabs(o.g)));

@@ -17,7 +17,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
 // Workspace of the loss: per-trajectory and per-token scratch.
 struct LossWs {
-  size_t hdr, traj_tok_off, w, traj_loss, tok_adv, tok_w, contrib, state, total;
+  size_t hdr, traj_tok_off, w, traj_loss, traj_rstats, tok_adv, tok_w, contrib, state, tok_ratio, total;
 };
 
 inline LossWs loss_ws_layout(int64_t T, int32_t n_traj) {
@@ -27,10 +27,12 @@ inline LossWs loss_ws_layout(int64_t T, int32_t n_traj) {
   l.traj_tok_off = o; o = align_up(o + sizeof(int32_t) * ((size_t)n_traj + 1));
   l.w = o;            o = align_up(o + sizeof(double) * (size_t)n_traj);
   l.traj_loss = o;    o = align_up(o + sizeof(double) * (size_t)n_traj);
+  l.traj_rstats = o;  o = align_up(o + 6 * sizeof(double) * (size_t)n_traj);
   l.tok_adv = o;      o = align_up(o + sizeof(float) * (size_t)(T > 0 ? T : 0));
   l.tok_w = o;        o = align_up(o + sizeof(double) * (size_t)(T > 0 ? T : 0));
   l.contrib = o;      o = align_up(o + sizeof(double) * (size_t)(T > 0 ? T : 0));
   l.state = o;        o = align_up(o + sizeof(int8_t) * (size_t)(T > 0 ? T : 0));
+  l.tok_ratio = o;    o = align_up(o + 2 * sizeof(double) * (size_t)(T > 0 ? T : 0));
   l.total = o;
   return l;
 }
