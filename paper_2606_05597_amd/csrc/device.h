@@ -72,38 +72,53 @@ struct TokenOut {
 // The min of Eq. 1 picks the unclipped term rho*A unless the clipped term is
 // smaller; inside the clip range both terms equal rho*A, so the derivative is
 // rho*A except when the clip (or the dual-clip floor) holds the term fixed.
-__device__ __forceinline__ TokenOut token_surrogate(double l, double b, double p, double A, double w,
-                                                    double lo, double hi, double c, double grad_scale) {
+// The log-prob differences are formed in fp64 and the ratios, the min and the
+// clips in fp32 (native exp2): one rounding of each ratio, far below the loss
+// and dlogits tolerances; the token's share of the loss and its coefficient are
+// scaled by the fp64 weight.
+__device__ __forceinline__ float exp_f32(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
+
+__device__ __forceinline__ TokenOut token_surrogate(double l, double b, double p, double A_, double w,
+                                                    double lo_, double hi_, double c_, double grad_scale) {
   // rho = pi / pi_behave, r = pi / pi_prox, omega = pi_prox / pi_behave; with
   // pi_prox = pi_behave (the coupled ratio) omega = 1 and r = rho exactly.
-  const double rho = exp(l - b);
-  const double r = (p == b) ? rho : exp(l - p);
-  const double omega = (p == b) ? 1.0 : exp(p - b);
+  const float A = (float)A_, lo = (float)lo_, hi = (float)hi_, c = (float)c_;
+  const float rho = exp_f32((float)(l - b));
+  const float r = (p == b) ? rho : exp_f32((float)(l - p));
+  const float omega = (p == b) ? 1.f : exp_f32((float)(p - b));
   const bool inside = (r >= lo) && (r <= hi);
-  const double r_cl = fmin(fmax(r, lo), hi);
-  const double u1 = rho * A;
-  const double u2 = omega * r_cl * A;
-  double s = u1, ds = u1;
+  const float r_cl = fminf(fmaxf(r, lo), hi);
+  const float u1 = rho * A;
+  const float u2 = omega * r_cl * A;
+  float s = u1, ds = u1;
   int state = 0;
   if (u2 < u1) {
     s = u2;
     if (!inside) {
-      ds = 0.0;
+      ds = 0.f;
       state = kStateEpsCut;
     }
   }
-  if (c > 0.0 && A < 0.0 && s < c * A) {
+  if (c > 0.f && A < 0.f && s < c * A) {
     s = c * A;
-    ds = 0.0;
+    ds = 0.f;
     state |= kStateDualCut;
   }
   TokenOut o;
-  o.contrib = -w * s;
-  o.g = grad_scale * w * ds;
+  o.contrib = -w * (double)s;
+  o.g = grad_scale * w * (double)ds;
   o.rho = rho;
   o.r = r;
   o.state = state | (inside ? 0 : kStateOutside) | kStateValid;
   return o;
+}
+
+// Log-sum-exp of a row from its shift M and fp64 sum S = sum e^(z - M) >= 1:
+// S = f 2^e with f in [0.5, 1), and log2 f in fp32 (v_log_f32) is good to ~1e-7.
+__device__ __forceinline__ double row_lse(double M, double S) {
+  int e;
+  const double f = frexp(S, &e);
+  return M + ((double)e + (double)__builtin_amdgcn_logf((float)f)) * kLn2;
 }
 
 // Trajectory of token t: the largest i with traj_tok_off[i] <= t (trajectories
@@ -190,9 +205,9 @@ __device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn
   a.tok_ratio[t] = make_double2(o.r, o.rho);
   if (a.token_logp) a.token_logp[t] = (float)l;
   // d_v = g exp(z_v - lse) = sign(g) 2^(z_v L - lse L + log2|g|), with L = log2(e) as rounded on the device
-  rs.nc = (float)(-lse * (double)kLog2e + log2(fabs(o.g)));
+  rs.nc = (float)(-lse * (double)kLog2e) + __builtin_amdgcn_logf(fabsf((float)o.g));
   rs.sign = (o.g < 0.0) ? -1.f : 1.f;
-  rs.d_a = (float)(o.g * expm1(l));  // g (p_a - 1), without cancellation
+  rs.d_a = (float)o.g * expm1f((float)l);  // g (p_a - 1), without cancellation
   if (isnan(o.g)) rs.nc = NAN;
   return rs;
 }

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
     const double S = sh_s[0] + sh_s[1] + sh_s[2] + sh_s[3];
     const double za = sh_z[0] + sh_z[1] + sh_z[2] + sh_z[3];
     const TokenIn in = token_load(a.tok, t);
-    a.rs[t] = token_finish(a.tok, t, in, (double)M + log(S), za);
+    a.rs[t] = token_finish(a.tok, t, in, row_lse((double)M, S), za);
   }
 }
 

@@ -283,7 +283,7 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
 
     double M, S;
     block_combine<NW>(m, s, sh_m, sh_s, M, S);  // barrier: sh_za is visible
-    if (tid == 0) sh_rs = token_finish(a.tok, t, in, M + log(S), (double)sh_za);
+    if (tid == 0) sh_rs = token_finish(a.tok, t, in, row_lse(M, S), (double)sh_za);
     // wave 1 fetches the next row's token inputs meanwhile: its loads are the only memory operations it has
     // in flight here, so waiting for them holds nothing else back
     if (tid == 64) sh_in = token_load(a.tok, tn < a.T ? tn : t);
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
 
   double M, S;
   block_combine<NW>(m, s, sh_m, sh_s, M, S);
-  if (tid == 0) sh_rs = token_finish(a.tok, t, in, M + log(S), (double)sh_za);
+  if (tid == 0) sh_rs = token_finish(a.tok, t, in, row_lse(M, S), (double)sh_za);
   __syncthreads();
   if (!a.dlogits) return;
 
@@ -399,7 +399,7 @@ __global__ __launch_bounds__(256) void k_rows_generic(const RowArgs a) {
   block_combine<NW>(m, s, sh_m, sh_s, M, S);
   if (tid == 0) {
     const bool ok = in.act >= 0 && (int64_t)in.act < a.tok.V;
-    sh_rs = token_finish(a.tok, t, in, M + log(S), ok ? (double)load_elem<Tin>(row + in.act) : 0.0);
+    sh_rs = token_finish(a.tok, t, in, row_lse(M, S), ok ? (double)load_elem<Tin>(row + in.act) : 0.0);
   }
   __syncthreads();
   if (!a.dlogits) return;
