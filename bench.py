@@ -277,7 +277,7 @@ def main():
                    "normalizer": "1/k (k=10)", "eps": 0.2, "dual_clip_c": 3.0, "loss": float(loss.item())},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_rows_pipe<19, 9> (bf16, 1024 threads, one workgroup per CU)", "kernel_ms": hot_ms,
+                     "kernel": "k_rows_pipe<19, 5> (bf16, 1024 threads, one workgroup per CU)", "kernel_ms": hot_ms,
                      "algorithmic_bytes_per_launch": alg_bytes},
     }
     del dlogits

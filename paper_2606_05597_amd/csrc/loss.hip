@@ -440,7 +440,7 @@ static const Variant kVariants[] = {
 static const RowKernel kPipe[] = {
     k_rows_pipe<7, 4>,   k_rows_pipe<8, 4>,   k_rows_pipe<9, 5>,   k_rows_pipe<10, 5>, k_rows_pipe<11, 6>,
     k_rows_pipe<12, 6>,  k_rows_pipe<13, 7>,  k_rows_pipe<14, 7>,  k_rows_pipe<15, 8>, k_rows_pipe<16, 8>,
-    k_rows_pipe<17, 9>,  k_rows_pipe<18, 9>,  k_rows_pipe<19, 9>,
+    k_rows_pipe<17, 9>,  k_rows_pipe<18, 9>,  k_rows_pipe<19, 5>,
 };
 constexpr int kPipeMinNV = 7, kPipeMaxNV = 19;
 
