@@ -205,8 +205,18 @@ struct DlogitsArgs {
   int c0, C, Tp;
 };
 
+// Per-wave LDS staging of the dlogits epilogue: 64 rows x 64 columns of the wave's
+// output, once row-major (stride 72 bf16: the two 32-lane halves of a 2-byte store
+// land on different banks) for D, once column-major for D^T (64 rows per column,
+// the eight 16-byte row chunks of column c permuted by (c ^ c >> 3) & 7, which
+// keeps the 16-byte column reads free of bank conflicts).
+constexpr int kLdr = 72;
+constexpr int kStageD = 64 * kLdr, kStageT = 64 * 64;
+__device__ __forceinline__ int dt_chunk(int c, int rc) { return rc ^ ((c ^ (c >> 3)) & 7); }
+
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
-  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  constexpr int kMain = 2 * LmCfg::STAGE, kEpi = LmCfg::NW * (kStageD + kStageT);
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kMain > kEpi ? kMain : kEpi];
   __shared__ RowScale sh_rs[TILE];
   int tm, tn;
   if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.Tp), tiles_of(p.g.N), tm, tn)) return;
@@ -215,14 +225,13 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   if (tid < TILE) sh_rs[tid] = p.rs[m0 + tid];  // m0 + tid < Tp: Tp is a multiple of the tile
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);  // its first barrier publishes sh_rs
+  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, smem);  // its first barrier publishes sh_rs
   // Columns past the chunk's width (last tile of the last chunk) are written too: they
   // stay inside D's C columns and D^T's C rows, and no product reads them.
-  // D^T straight from the registers: a lane holds 4 consecutive rows of one column.
-  // D through LDS: each wave stages 64 of its rows (row stride 72 bf16: the two
-  // 32-lane halves of a store land on different banks), then stores 16-byte rows.
-  constexpr int LDR = 72;
-  uint16_t* stage = sm.s + wave * 64 * LDR;
+  // Both layouts go through LDS so that every global store is a 16-byte vector and
+  // eight lanes fill one 128-byte line.
+  uint16_t* stD = smem + wave * (kStageD + kStageT);
+  uint16_t* stT = stD + kStageD;
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
 #pragma unroll
@@ -235,31 +244,37 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
         for (int e = 0; e < 4; ++e) rs[e] = sh_rs[gemm_row<LmCfg>(wm, i, 4 * q + e, lane)];
 #pragma unroll
         for (int j = 0; j < LmCfg::JB; ++j) {
-          const int n = n0 + gemm_col<LmCfg>(wn, j, lane);
-          const int vcol = p.c0 + n;
+          const int vcol = p.c0 + n0 + gemm_col<LmCfg>(wn, j, lane);
           float d[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e)
             d[e] = (vcol == rs[e].act) ? rs[e].d_a
                                        : rs[e].sign * __builtin_amdgcn_exp2f(fmaf(acc[i][j][4 * q + e], kLog2e, rs[e].nc));
           const uint32_t lo = pack_bf16(d[0], d[1]), hi = pack_bf16(d[2], d[3]);
-          const int row0 = m0 + gemm_row<LmCfg>(wm, i, 4 * q, lane);
-          *reinterpret_cast<u32x2*>(p.DT + (int64_t)n * p.Tp + row0) = u32x2{lo, hi};
+          // local row of the 4 values (in this half) and local column
           const int lr = ii * 32 + 8 * q + 4 * (lane >> 5), lc = j * 32 + (lane & 31);
-          stage[(lr + 0) * LDR + lc] = (uint16_t)(lo & 0xffffu);
-          stage[(lr + 1) * LDR + lc] = (uint16_t)(lo >> 16);
-          stage[(lr + 2) * LDR + lc] = (uint16_t)(hi & 0xffffu);
-          stage[(lr + 3) * LDR + lc] = (uint16_t)(hi >> 16);
+          stD[(lr + 0) * kLdr + lc] = (uint16_t)(lo & 0xffffu);
+          stD[(lr + 1) * kLdr + lc] = (uint16_t)(lo >> 16);
+          stD[(lr + 2) * kLdr + lc] = (uint16_t)(hi & 0xffffu);
+          stD[(lr + 3) * kLdr + lc] = (uint16_t)(hi >> 16);
+          *reinterpret_cast<u32x2*>(stT + lc * 64 + dt_chunk(lc, lr >> 3) * 8 + (lr & 7)) = u32x2{lo, hi};
         }
       }
     }
-    // this wave's 64 staged rows x 64 columns, 8 lanes per row (LDS runs a wave's accesses in order)
+    // LDS runs a wave's accesses in order: the staged values are read back by the same wave
 #pragma unroll
-    for (int it = 0; it < 8; ++it) {
+    for (int it = 0; it < 8; ++it) {  // D: 8 rows per pass, 8 lanes per 64-column row
       const int lr = it * 8 + (lane >> 3), cv = (lane & 7) * 8;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(stage + lr * LDR + cv);
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stD + lr * kLdr + cv);
       const int grow = m0 + wm * LmCfg::WTM + half * 64 + lr;
       *reinterpret_cast<u32x4*>(p.D + (int64_t)grow * p.C + n0 + wn * LmCfg::WTN + cv) = v;
+    }
+#pragma unroll
+    for (int it = 0; it < 8; ++it) {  // D^T: 8 columns per pass, 8 lanes per 64-row column
+      const int lc = it * 8 + (lane >> 3), rc = lane & 7;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stT + lc * 64 + dt_chunk(lc, rc) * 8);
+      const int64_t col = n0 + wn * LmCfg::WTN + lc;
+      *reinterpret_cast<u32x4*>(p.DT + col * p.Tp + m0 + wm * LmCfg::WTM + half * 64 + rc * 8) = v;
     }
   }
 }
