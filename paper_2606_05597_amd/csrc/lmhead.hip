@@ -7,9 +7,10 @@
 //                                      log-prob, token epilogue, dlogits scale
 //   pass 2  for each vocabulary chunk c of `vocab_chunk` columns:
 //             z_c = h W_c (recomputed), D_c = g (softmax - onehot) in bf16,
-//             stored as D_c [Tp, C] and its transpose D_c^T [C, Tp]
-//             dhidden += D_c W_c^T       (fp32 accumulator, bf16 at the end)
+//             stored as D_c (one half of a [Tp, 2C] pair buffer) and its transpose D_c^T [C, Tp]
 //             dW[:, c] = h^T D_c
+//           after every second chunk (and the last):
+//             dhidden += [D_c-1 D_c] [W_c-1 W_c]^T   (fp32 accumulator, bf16 at the end)
 // Every product is one GEMM core (gemm.h) with both operands K-contiguous
 // (C[m, n] = sum_k A[m, k] B[n, k]); W and h are transposed once so that this
 // holds for all four.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16, slabs
@@ -200,9 +201,9 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
 struct DlogitsArgs {
   GemmArgs g;            // A = h [T, H] (M = Tp), B = W^T rows of the chunk [Cw, H]
   const RowScale* rs;    // [Tp]
-  uint16_t* D;           // [Tp, C]
-  uint16_t* DT;          // [C, Tp]
-  int c0, C, Tp;
+  uint16_t* D;           // the chunk's columns of the pair buffer, row stride C
+  uint16_t* DT;          // [chunk width, Tp]
+  int c0, C, Tp;         // C: D's row stride (twice the chunk when chunks are paired)
 };
 
 // Per-wave LDS staging of the dlogits epilogue: 64 rows x 64 columns of the wave's
@@ -281,7 +282,7 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
 
 // ---- pass 2b: dhidden += D_c W_c^T --------------------------------------------------
 struct DhArgs {
-  GemmArgs g;        // A = D_c [Tp, C] (M = T, K = Cw), B = W[:, chunk] as [H, Cw] with ldb = V
+  GemmArgs g;        // A = the pair buffer (M = T, K = the pair's width), B = W[:, pair] as [H, K], ldb = V
   float* acc;        // [Tp, H] fp32 accumulator (unused with a single chunk)
   uint16_t* dh;      // [T, H] bf16 output
   int first, last;
@@ -432,7 +433,7 @@ static LmWs lm_ws_layout(int64_t T, int64_t H, int64_t V, int32_t C, int32_t n_t
   l.ht = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(H * l.Tp));
   l.part = o; o = align_up(o + sizeof(float2) * (size_t)(T * l.n_tiles));
   l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
-  l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C));
+  l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C * (n_chunks > 1 ? 2 : 1)));  // a pair of chunks
   l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C));
   l.acc = o;  o = align_up(o + (n_chunks > 1 ? sizeof(float) * (size_t)(l.Tp * H) : 0));
   l.total = o;
@@ -516,27 +517,32 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   ca.n_tiles = L.n_tiles;
   hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)Tp), dim3(256), 0, s, ca);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
-  // pass 2, chunk by chunk
+  // pass 2, chunk by chunk; dhidden takes the chunks in pairs (D holds two, side by side),
+  // which halves the passes over its fp32 accumulator
   const int n_chunks = (int)((V + C - 1) / C);
+  const int ldD = n_chunks > 1 ? 2 * C : C;
   for (int c = 0; c < n_chunks; ++c) {
     const int c0 = c * C;
     const int Cw = (int)((V - c0) < C ? (V - c0) : C);
     DlogitsArgs da;
     da.g = GemmArgs{h16, WT + (int64_t)c0 * H, H, H, (int)T, Cw, (int)H};
     da.rs = rs;
-    da.D = D;
+    da.D = D + (c & 1) * C;
     da.DT = DT;
     da.c0 = c0;
-    da.C = C;
+    da.C = ldD;
     da.Tp = Tp;
     hipLaunchKernelGGL(k_lm_dlogits, gemm_grid(Tp, Cw), dim3(LmCfg::NT), 0, s, da);
-    DhArgs ha;
-    ha.g = GemmArgs{D, W16 + c0, C, V, (int)T, (int)H, Cw};
-    ha.acc = acc;
-    ha.dh = static_cast<uint16_t*>(dhidden);
-    ha.first = (c == 0);
-    ha.last = (c == n_chunks - 1);
-    hipLaunchKernelGGL(k_lm_dh, gemm_grid(T, H), dim3(LmCfg::NT), 0, s, ha);
+    if ((c & 1) || c == n_chunks - 1) {
+      const int p0 = c & ~1;  // first chunk of the pair
+      DhArgs ha;
+      ha.g = GemmArgs{D, W16 + (int64_t)p0 * C, ldD, V, (int)T, (int)H, (c & 1) ? C + Cw : Cw};
+      ha.acc = acc;
+      ha.dh = static_cast<uint16_t*>(dhidden);
+      ha.first = (p0 == 0);
+      ha.last = (c == n_chunks - 1);
+      hipLaunchKernelGGL(k_lm_dh, gemm_grid(T, H), dim3(LmCfg::NT), 0, s, ha);
+    }
     DwArgs wa;
     wa.g = GemmArgs{hT, DT, Tp, Tp, (int)H, Cw, Tp};
     wa.dw = dw_lm;
