@@ -202,7 +202,7 @@ def bench_fused(steps: int, warmup: int = 1) -> dict:
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
               "the path shards by whole task groups, see the design notes", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
