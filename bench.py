@@ -203,7 +203,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py: the benchmark runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the path shards by whole task groups, see the design notes", file=sys.stderr)
+              "the loss shards by whole task groups, one process per GPU, with one fp64 all-reduce of the loss", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
