@@ -24,8 +24,8 @@
  * entropy -sum p log p per token, the quantity of the GRPO vs. RAFT++
  * comparison (Sec. 5).
  *
- * Readings where the paper is silent are listed with the library's design
- * notes; the ones that matter here: std uses `ddof` (default 1) and a zero
+ * Readings where the paper is silent, as this file takes them: std uses
+ * `ddof` (default 1) and a zero
  * group std gives A = 0; groups combine by their mean, so the per-token weight
  * is w_i = 1/(n_groups * G * |tau_i|) or 1/(n_groups * G * k); the eps clip is
  * inclusive (gradient flows at r = 1 +- eps); the dual clip is active only
