@@ -25,8 +25,8 @@
  * comparison (Sec. 5).
  *
  * Readings where the paper is silent, as this file takes them: std uses
- * `ddof` (default 1) and a zero
- * group std gives A = 0; groups combine by their mean, so the per-token weight
+ * `ddof` (default 1) and a zero group std gives A = 0; groups combine by
+ * their mean, so the per-token weight
  * is w_i = 1/(n_groups * G * |tau_i|) or 1/(n_groups * G * k); the eps clip is
  * inclusive (gradient flows at r = 1 +- eps); the dual clip is active only
  * when s < c*A strictly.
