@@ -6,7 +6,7 @@
 // across the workgroup, and dlogits are formed from the same registers and
 // written once: V*s bytes read and V*s written per token.
 //
-//  k_rows_pipe      long bf16 rows (V up to 155,648): persistent, one
+//  k_rows_pipe      long bf16 rows (V up to 188,416): persistent, one
 //                   workgroup of 1024 threads per CU.  Row t+G streams in
 //                   while row t's dlogits are written: part of each row lives
 //                   in LDS (global_load_lds), the rest in registers.
@@ -439,10 +439,11 @@ static const Variant kVariants[] = {
 // that only each thread's last vector can be partial; NP vectors in LDS.
 static const RowKernel kPipe[] = {
     k_rows_pipe<7, 4>,   k_rows_pipe<8, 4>,   k_rows_pipe<9, 5>,   k_rows_pipe<10, 5>, k_rows_pipe<11, 6>,
-    k_rows_pipe<12, 6>,  k_rows_pipe<13, 7>,  k_rows_pipe<14, 7>,  k_rows_pipe<15, 8>, k_rows_pipe<16, 8>,
-    k_rows_pipe<17, 9>,  k_rows_pipe<18, 9>,  k_rows_pipe<19, 5>,
-};
-constexpr int kPipeMinNV = 7, kPipeMaxNV = 19;
+    k_rows_pipe<12, 6>,  k_rows_pipe<13, 7>,  k_rows_pipe<14, 7>,  k_rows_pipe<15, 1>, k_rows_pipe<16, 2>,
+    k_rows_pipe<17, 3>,  k_rows_pipe<18, 4>,  k_rows_pipe<19, 5>,  k_rows_pipe<20, 9>, k_rows_pipe<21, 9>,
+    k_rows_pipe<22, 9>,  k_rows_pipe<23, 9>,
+};  // from 15 vectors on, 14 in registers (what fits in 128 VGPRs) and the rest in LDS
+constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 14 register vectors and 9 LDS vectors per thread
 
 struct Launch {
   RowKernel k;

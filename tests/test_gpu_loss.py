@@ -225,10 +225,12 @@ def _edge_batch(V, dtype="bf16", n_groups=2, G=4, ld=None, seed=5):
 
 
 @pytest.mark.parametrize("V,dtype", [(7, "bf16"), (7, "f32"), (1000, "bf16"), (4093, "f32"), (33, "bf16"),
-                                     (151936, "bf16"), (163840, "bf16"), (200000, "bf16")])
+                                     (122880, "bf16"), (128256, "bf16"), (151936, "bf16"), (163840, "bf16"),
+                                     (184320, "bf16"), (200000, "bf16")])
 def test_ragged_vocab_and_kernel_variants(V, dtype):
-    # odd V uses the generic row kernel; V = 151,936 the 1024x19 resident kernel; 200,000 exceeds
-    # the resident limit and falls back to the generic kernel
+    # odd V uses the generic row kernel; bf16 rows of 56K to 188K take the pipelined kernel (122,880: one LDS
+    # vector per thread; 128,256: two; 151,936: five; 163,840 and 184,320: nine); 200,000 exceeds it and falls
+    # back to the generic kernel
     b = _edge_batch(V, dtype)
     _full_parity(b, oracle.NORM_TRAJ_STEPS, 3.0)
 
