@@ -7,9 +7,10 @@
 //                                      log-prob, token epilogue, dlogits scale
 //   pass 2  for each vocabulary chunk c of `vocab_chunk` columns:
 //             z_c = h W_c (recomputed), D_c = g (softmax - onehot) in bf16,
-//             stored as D_c (one half of a [Tp, 2C] pair buffer) and its transpose D_c^T [C, Tp]
-//             dW[:, c] = h^T D_c
-//           after every second chunk (and the last):
+//             stored as D_c (one half of a [Tp, 2C] pair buffer) and its transpose
+//             D_c^T (one half of a [2C, Tp] pair buffer)
+//           after every second chunk (and the last), in one launch:
+//             dW[:, c-1..c] = h^T [D_c-1 D_c]
 //             dhidden += [D_c-1 D_c] [W_c-1 W_c]^T   (fp32 accumulator, bf16 at the end)
 // Every product is one GEMM core (gemm.h) with both operands K-contiguous
 // (C[m, n] = sum_k A[m, k] B[n, k]); W and h are transposed once so that this
@@ -288,10 +289,10 @@ struct DhArgs {
   int first, last;
 };
 
-__global__ __launch_bounds__(LmCfg::NT) void k_lm_dh(const DhArgs p) {
-  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+// One tile of the dhidden product: block bid of nblocks (a multiple of 8, for the XCD order).
+__device__ __forceinline__ void lm_dh_tile(const DhArgs& p, int bid, int nblocks, GemmSmem& sm) {
   int tm, tn;
-  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  if (!gemm_tile_of(bid, nblocks, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
   const int m0 = tm * TILE, n0 = tn * TILE;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
@@ -334,18 +335,18 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh(const DhArgs p) {
   }
 }
 
-// ---- pass 2c: dW[:, chunk] = h^T D_c ----------------------------------------------
+// ---- pass 2c: dW[:, chunks] = h^T D -------------------------------------------------
 struct DwArgs {
-  GemmArgs g;     // A = h^T [H, Tp], B = D_c^T [Cw, Tp], K = Tp
+  GemmArgs g;     // A = h^T [H, Tp], B = D^T of the pair [width, Tp], K = Tp
   float* dw;      // [H, V]
   int64_t V;
   int c0, accumulate;
 };
 
-__global__ __launch_bounds__(LmCfg::NT) void k_lm_dw(const DwArgs p) {
-  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+// One tile of the dW product: block bid of nblocks (a multiple of 8).
+__device__ __forceinline__ void lm_dw_tile(const DwArgs& p, int bid, int nblocks, GemmSmem& sm) {
   int tm, tn;
-  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  if (!gemm_tile_of(bid, nblocks, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
   const int m0 = tm * TILE, n0 = tn * TILE;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
@@ -376,6 +377,23 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dw(const DwArgs p) {
     if (p.accumulate) store(N(), Y());
     else store(N(), N());
   }
+}
+
+// Both backward products of a pair of chunks in one launch.  A dW tile runs over K = Tp, four to eight times
+// longer than a dhidden tile (K = the pair's width), and a chunk's dW alone has 1.75 tiles per CU at the
+// benchmark's shape; launched first, the long dW tiles are followed on every CU by short dhidden tiles, which
+// fill the round the dW tiles leave ragged.
+struct DhDwArgs {
+  DhArgs dh;
+  DwArgs dw;
+  int dw_blocks;  // blocks [0, dw_blocks) take dW tiles, the rest dhidden tiles; a multiple of 8
+};
+
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_dw(const DhDwArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  const int b = blockIdx.x;
+  if (b < p.dw_blocks) lm_dw_tile(p.dw, b, p.dw_blocks, sm);
+  else lm_dh_tile(p.dh, b - p.dw_blocks, (int)gridDim.x - p.dw_blocks, sm);
 }
 
 // ---- bf16 transpose: dst[c][r] = src[r][c] for r < R, 0 for R <= r < Rp ------------
@@ -434,7 +452,7 @@ static LmWs lm_ws_layout(int64_t T, int64_t H, int64_t V, int32_t C, int32_t n_t
   l.part = o; o = align_up(o + sizeof(float2) * (size_t)(T * l.n_tiles));
   l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
   l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C * (n_chunks > 1 ? 2 : 1)));  // a pair of chunks
-  l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C));
+  l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tp * C * (n_chunks > 1 ? 2 : 1)));  // a pair too
   l.acc = o;  o = align_up(o + (n_chunks > 1 ? sizeof(float) * (size_t)(l.Tp * H) : 0));
   l.total = o;
   return l;
@@ -517,8 +535,8 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   ca.n_tiles = L.n_tiles;
   hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)Tp), dim3(256), 0, s, ca);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
-  // pass 2, chunk by chunk; dhidden takes the chunks in pairs (D holds two, side by side),
-  // which halves the passes over its fp32 accumulator
+  // pass 2, chunk by chunk; the backward products take the chunks in pairs (D holds two side by side, D^T one
+  // above the other), which halves the passes over dhidden's fp32 accumulator and gives one dW launch per pair
   const int n_chunks = (int)((V + C - 1) / C);
   const int ldD = n_chunks > 1 ? 2 * C : C;
   for (int c = 0; c < n_chunks; ++c) {
@@ -528,28 +546,28 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
     da.g = GemmArgs{h16, WT + (int64_t)c0 * H, H, H, (int)T, Cw, (int)H};
     da.rs = rs;
     da.D = D + (c & 1) * C;
-    da.DT = DT;
+    da.DT = DT + (int64_t)(c & 1) * C * Tp;
     da.c0 = c0;
     da.C = ldD;
     da.Tp = Tp;
     hipLaunchKernelGGL(k_lm_dlogits, gemm_grid(Tp, Cw), dim3(LmCfg::NT), 0, s, da);
     if ((c & 1) || c == n_chunks - 1) {
-      const int p0 = c & ~1;  // first chunk of the pair
-      DhArgs ha;
-      ha.g = GemmArgs{D, W16 + (int64_t)p0 * C, ldD, V, (int)T, (int)H, (c & 1) ? C + Cw : Cw};
-      ha.acc = acc;
-      ha.dh = static_cast<uint16_t*>(dhidden);
-      ha.first = (p0 == 0);
-      ha.last = (c == n_chunks - 1);
-      hipLaunchKernelGGL(k_lm_dh, gemm_grid(T, H), dim3(LmCfg::NT), 0, s, ha);
+      const int p0 = c & ~1;                  // first chunk of the pair
+      const int width = (c & 1) ? C + Cw : Cw;  // the pair's vocabulary columns
+      DhDwArgs ba;
+      ba.dh.g = GemmArgs{D, W16 + (int64_t)p0 * C, ldD, V, (int)T, (int)H, width};
+      ba.dh.acc = acc;
+      ba.dh.dh = static_cast<uint16_t*>(dhidden);
+      ba.dh.first = (p0 == 0);
+      ba.dh.last = (c == n_chunks - 1);
+      ba.dw.g = GemmArgs{hT, DT, Tp, Tp, (int)H, width, Tp};
+      ba.dw.dw = dw_lm;
+      ba.dw.V = V;
+      ba.dw.c0 = p0 * C;
+      ba.dw.accumulate = accumulate_dw;
+      ba.dw_blocks = (int)gemm_grid(H, width).x;
+      hipLaunchKernelGGL(k_lm_dh_dw, dim3((unsigned)ba.dw_blocks + gemm_grid(T, H).x), dim3(LmCfg::NT), 0, s, ba);
     }
-    DwArgs wa;
-    wa.g = GemmArgs{hT, DT, Tp, Tp, (int)H, Cw, Tp};
-    wa.dw = dw_lm;
-    wa.V = V;
-    wa.c0 = c0;
-    wa.accumulate = accumulate_dw;
-    hipLaunchKernelGGL(k_lm_dw, gemm_grid(H, Cw), dim3(LmCfg::NT), 0, s, wa);
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   }
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
