@@ -63,6 +63,8 @@ def _load():
         lib.oracle_mixed_groups.restype = I32
         lib.oracle_logp_entropy.argtypes = [P, ctypes.c_int, I64, I64, P, I64, I64, P, P]
         lib.oracle_logp_entropy.restype = ctypes.c_int
+        lib.oracle_vocab_shard_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, P, I64, I64, P, P, P]
+        lib.oracle_vocab_shard_stats.restype = None
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
@@ -240,3 +242,50 @@ def logp_entropy(logits: np.ndarray, actions, *, V: int | None = None, row_begin
     f = lib.oracle_logp_entropy(ctypes.c_void_p(base), dt, V, ld, _ptr(a), row_begin, row_end, _ptr(logp),
                                 _ptr(ent))
     return LogpEntropy(logp, ent, int(f))
+
+
+class ShardStats:
+    """Per-row statistics of one vocabulary shard: max m, sum s of exp(z - m), the action's logit z_a (-inf when
+    the action lies outside the shard)."""
+
+    def __init__(self, m, s, za):
+        self.m = m
+        self.s = s
+        self.za = za
+
+
+def vocab_shard_stats(logits_shard: np.ndarray, actions, v_begin: int, *, V: int | None = None, row_begin: int = 0,
+                      row_end: int | None = None, row_offset: int = 0) -> ShardStats:
+    """Statistics of the shard holding global vocabulary columns [v_begin, v_begin + V) for token rows
+    [row_begin, row_end).  ``logits_shard`` is [rows_held, ld] with the shard's columns only, holding token rows
+    from ``row_offset`` on; ``actions`` are global column ids indexed by absolute token number."""
+    lib = _load()
+    logits_shard = np.ascontiguousarray(logits_shard)
+    dt = _logits_dtype(logits_shard)
+    ld = logits_shard.shape[1]
+    V = ld if V is None else int(V)
+    assert 1 <= V <= ld
+    if row_end is None:
+        row_end = row_offset + logits_shard.shape[0]
+    assert row_begin >= row_offset and row_end - row_offset <= logits_shard.shape[0]
+    a = _c(actions, np.int32)
+    n = row_end - row_begin
+    m, s, za = np.empty(n, np.float64), np.empty(n, np.float64), np.empty(n, np.float64)
+    base = logits_shard.ctypes.data - row_offset * ld * logits_shard.itemsize
+    lib.oracle_vocab_shard_stats(ctypes.c_void_p(base), dt, V, ld, int(v_begin), _ptr(a), row_begin, row_end,
+                                 _ptr(m), _ptr(s), _ptr(za))
+    return ShardStats(m, s, za)
+
+
+def vocab_merge(stats: list) -> tuple[np.ndarray, np.ndarray]:
+    """Merges the shards' statistics of the same rows into each row's (log-sum-exp, action logit):
+    lse = M + log sum_g s_g exp(m_g - M) with M = max_g m_g, and z_a = max_g z_a_g (only the owner's is finite)."""
+    m = np.stack([x.m for x in stats])
+    M = m.max(axis=0)
+    with np.errstate(invalid="ignore"):
+        w = np.where(m == -np.inf, 0.0, np.exp(m - M))
+    S = (np.stack([x.s for x in stats]) * w).sum(axis=0)
+    with np.errstate(divide="ignore"):
+        lse = M + np.log(S)
+    za = np.stack([x.za for x in stats]).max(axis=0)
+    return lse, za

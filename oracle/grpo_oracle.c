@@ -23,6 +23,10 @@
  * Forward only (oracle_logp_entropy): that log-probability and the policy
  * entropy -sum p log p per token, the quantity of the GRPO vs. RAFT++
  * comparison (Sec. 5).
+ * Vocabulary split over devices (oracle_vocab_shard_stats): one shard's max,
+ * sum of exponentials and action logit per token, by their plain definitions;
+ * the paper trains on one node per update and does not split the vocabulary,
+ * so this serves the sharded variant of the same loss.
  *
  * Readings where the paper is silent, as this file takes them: std uses
  * `ddof` (default 1) and a zero group std gives A = 0; groups combine by
@@ -314,6 +318,39 @@ int oracle_logp_entropy(const void* logits, int dtype, int64_t V, int64_t ld, co
     if (token_entropy) token_entropy[q] = H;
   }
   return flags;
+}
+
+/* ---- one shard of a vocabulary split over devices ----------------------- */
+
+/* For a vocabulary split into column ranges held by different devices, each
+ * range (a shard: global columns [v_begin, v_begin + V_shard)) reduces its own
+ * part of every row to m = max_v z_v, s = sum_v exp(z_v - m) over its columns,
+ * and z_a = the action's logit when the action falls in the range (-inf
+ * otherwise).  These are plain definitions; any split of the row merges back to
+ * the row's log-sum-exp through lse = M + log sum_g s_g exp(m_g - M) with
+ * M = max_g m_g, and to z_a as the largest of the shards' values (only the
+ * owner's is finite).  `logits` holds the shard's columns only (row stride ld).
+ * Outputs are indexed by t - row_begin. */
+void oracle_vocab_shard_stats(const void* logits, int dtype, int64_t V_shard, int64_t ld, int64_t v_begin,
+                              const int32_t* actions, int64_t row_begin, int64_t row_end, double* m_out,
+                              double* s_out, double* za_out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t t = row_begin; t < row_end; ++t) {
+    const int64_t q = t - row_begin;
+    const int64_t base = t * ld;
+    double m = -INFINITY;
+    for (int64_t v = 0; v < V_shard; ++v) {
+      const double z = load_elem(logits, dtype, base + v);
+      if (z > m || isnan(z)) m = z;
+    }
+    double s = 0.0;
+    if (m != -INFINITY) /* a shard of -inf logits holds no mass */
+      for (int64_t v = 0; v < V_shard; ++v) s += exp(load_elem(logits, dtype, base + v) - m);
+    const int64_t a = (int64_t)actions[t] - v_begin;
+    m_out[q] = m;
+    s_out[q] = s;
+    za_out[q] = (a >= 0 && a < V_shard) ? load_elem(logits, dtype, base + a) : -INFINITY;
+  }
 }
 
 int oracle_threads(void) { return omp_get_max_threads(); }
