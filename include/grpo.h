@@ -230,6 +230,70 @@ int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T, int64_t H
 int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const int32_t* actions,
                     float* token_logp, float* token_entropy, int32_t* error_flags, hipStream_t s);
 
+/*
+ * The vocabulary split over devices (tensor-parallel LM head; the extension of
+ * the loss of Eq. 1 to a sharded vocabulary): the calls one device makes for the
+ * shard it holds, logits [T, V_shard] of global columns [v_begin, v_begin +
+ * V_shard).  The exchange between the two calls (gathering every shard's
+ * records on every device) is the caller's.
+ *
+ * One shard's per-token record, 16 bytes:
+ *   m    max over the shard's columns of the row (-inf for a row of -inf)
+ *   z_a  the action's logit if a_t is one of the shard's columns, else -inf
+ *   s    sum over the shard's columns of exp(z - m), in fp64
+ * Any split of a row merges back to its log-sum-exp M + log sum_g s_g exp(m_g - M),
+ * M = max_g m_g, and to its action logit max_g z_a_g.
+ */
+typedef struct {
+  float m;
+  float z_a;
+  double s;
+} grpo_vocab_stats;
+
+/*
+ * Step 1 of the sharded loss: every row of the shard reduced to its record.
+ *   logits       device [T, ld] of `dt`, the shard's columns; columns >= V_shard unread
+ *   T >= 0, 1 <= V_shard <= ld, v_begin >= 0, v_begin + V_shard < 2^31
+ *   actions      device int32 [T]  global token ids
+ *   stats        device grpo_vocab_stats [T], 16-byte aligned (written)
+ *   error_flags  device int32 [1] or NULL: overwritten with GRPO_FLAG_NONFINITE
+ *                when a row's shard log-sum-exp is NaN or +inf (an action outside
+ *                the shard is not an error here; step 2 checks a_t against V_total)
+ * Each row is read once; the record's sums run in fp32 per thread and fp64 across the row.
+ * Errors: GRPO_ERR_ARG (logits, actions or stats NULL), GRPO_ERR_SHAPE, GRPO_ERR_DTYPE,
+ *   GRPO_ERR_ALIGN, GRPO_ERR_HIP.
+ */
+int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+                           int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats, int32_t* error_flags,
+                           hipStream_t s);
+
+/*
+ * Step 2 of the sharded loss: the loss and the shard's columns of dlogits.
+ *   logits, dt, T, V_shard, ld, v_begin: the shard, as in step 1
+ *   V_total      the whole vocabulary (actions outside [0, V_total) are flagged and
+ *                their tokens leave the loss, as in grpo_loss_fwd_bwd)
+ *   stats        device grpo_vocab_stats [n_shards][T]: every shard's records from
+ *                step 1, in the same shard order on every device; 16-byte aligned
+ *   n_shards     1 .. 65536
+ *   actions, behave_logp, prox_logp, adv, seg, p, loss_out, aux, ws, ws_bytes: as
+ *                grpo_loss_fwd_bwd (workspace from grpo_loss_workspace_bytes; the
+ *                loss and every per-token output are the whole row's, the same on
+ *                every shard; aux->gather_idx gets t*ld + a_t with the global a_t)
+ *   dlogits      device [T, ld] of `dt`, the shard's columns of dloss/dz * grad_scale;
+ *                NULL = forward only; may alias `logits`
+ * Per row the records are merged in shard order (so every shard computes the same
+ * bits), then the row's d_v = g_t (exp(z_v - lse) - [v = a_t]) over the shard's
+ * columns.  Errors: as grpo_loss_fwd_bwd, plus GRPO_ERR_SHAPE for v_begin < 0,
+ * v_begin + V_shard > V_total, V_total >= 2^31 or n_shards outside 1..65536, and
+ * GRPO_ERR_ARG for stats NULL with T > 0.
+ */
+int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+                                  int64_t v_begin, int64_t V_total, const grpo_vocab_stats* stats, int32_t n_shards,
+                                  const int32_t* actions, const float* behave_logp, const float* prox_logp,
+                                  const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
+                                  double* loss_out, void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes,
+                                  hipStream_t s);
+
 /* A static, human-readable name for a grpo_status value. */
 const char* grpo_status_str(int status);
 

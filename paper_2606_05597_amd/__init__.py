@@ -19,7 +19,8 @@ from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO
                    GRPO_NORM_TRAJ_STEPS, GrpoError)
 
 __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
-           "fused_lmhead_grpo", "grpo_token_logp", "grpo_status_str", "LossAux", "GrpoError"]
+           "fused_lmhead_grpo", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
+           "vocab_stats_fields", "grpo_status_str", "LossAux", "GrpoError"]
 
 
 def _ptr(t):
@@ -284,3 +285,95 @@ def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | Non
                                      _ptr(error_flags), _stream(stream))
     _check(st, "grpo_token_logp")
     return logp, ent
+
+
+VOCAB_STATS_BYTES = 16  # one grpo_vocab_stats record: fp32 m, fp32 z_a, fp64 s
+
+
+def vocab_stats_fields(stats: torch.Tensor):
+    """Views of a uint8 [..., T, 16] record tensor as (m fp32, z_a fp32, s fp64), each [..., T]."""
+    f32 = stats.view(torch.float32)
+    return f32[..., 0], f32[..., 1], stats.view(torch.float64)[..., 1]
+
+
+def _logits2d(logits, name="logits"):
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError(f"{name} must be [T, ld] with unit column stride")
+    if not logits.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (no CPU path)")
+    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
+    if dt is None:
+        raise TypeError(f"{name} must be bfloat16 or float32")
+    T = logits.shape[0]
+    ld = logits.stride(0) if T > 0 else logits.shape[1]
+    return dt, T, ld
+
+
+def grpo_vocab_shard_stats(logits: torch.Tensor, actions: torch.Tensor, v_begin: int, *, V: int | None = None,
+                           stats: torch.Tensor | None = None, error_flags: torch.Tensor | None = None, stream=None):
+    """Step 1 of the vocabulary-sharded loss: each row of the shard (global columns [v_begin, v_begin + V)) reduced
+    to its record.  Returns uint8 [T, 16] records (read them with ``vocab_stats_fields``)."""
+    dt, T, ld = _logits2d(logits)
+    Vv = logits.shape[1] if V is None else int(V)
+    _dev(actions, "actions")
+    if actions.dtype != torch.int32:
+        raise TypeError("actions must be int32")
+    if stats is None:
+        stats = torch.empty((T, VOCAB_STATS_BYTES), dtype=torch.uint8, device=logits.device)
+    _dev(stats, "stats")
+    if stats.dtype != torch.uint8 or tuple(stats.shape) != (T, VOCAB_STATS_BYTES):
+        raise ValueError("stats must be uint8 [T, 16]")
+    if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
+        raise ValueError("error_flags must be an int32 GPU tensor")
+    st = _lib.load().grpo_vocab_shard_stats(_ptr(logits), dt, T, Vv, ld, int(v_begin), _ptr(actions), _ptr(stats),
+                                            _ptr(error_flags), _stream(stream))
+    _check(st, "grpo_vocab_shard_stats")
+    return stats
+
+
+def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor, v_begin: int, V_total: int,
+                                  actions: torch.Tensor, behave_logp: torch.Tensor, adv: torch.Tensor,
+                                  step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *,
+                                  V: int | None = None, prox_logp: torch.Tensor | None = None,
+                                  norm: int = GRPO_NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2,
+                                  eps_high: float = 0.2, dual_clip_c: float = 0.0, grad_scale: float = 1.0,
+                                  n_groups_total: float = 0.0, dlogits=True, aux: LossAux | None = None,
+                                  workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None,
+                                  stream=None):
+    """Step 2 of the vocabulary-sharded loss: the loss (fp64 [1], the whole rows') and this shard's dlogits, from
+    the shard's logits and every shard's records ``stats_all`` (uint8 [n_shards, T, 16], in shard order).
+
+    ``dlogits``: True allocates a tensor like ``logits``; None/False is forward only; a tensor is written in place.
+    Returns (loss, dlogits or None).
+    """
+    dt, T, ld = _logits2d(logits)
+    Vv = logits.shape[1] if V is None else int(V)
+    _dev(actions, "actions")
+    if actions.dtype != torch.int32:
+        raise TypeError("actions must be int32")
+    _dev(stats_all, "stats_all")
+    if stats_all.dtype != torch.uint8 or stats_all.dim() != 3 or tuple(stats_all.shape[1:]) != (T, VOCAB_STATS_BYTES):
+        raise ValueError("stats_all must be uint8 [n_shards, T, 16]")
+    n_shards = stats_all.shape[0]
+    seg = _segments(step_tok_off, traj_step_off, group_size)
+    par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
+    if dlogits is True:
+        dlogits = torch.empty_like(logits)
+    elif dlogits is False:
+        dlogits = None
+    if dlogits is not None and (dlogits.shape != logits.shape or dlogits.stride() != logits.stride()
+                                or dlogits.dtype != logits.dtype):
+        raise ValueError("dlogits must match logits in shape, stride and dtype")
+    need = grpo_loss_workspace_bytes(T, seg.n_traj)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=logits.device)
+    if loss_out is None:
+        loss_out = torch.empty(1, dtype=torch.float64, device=logits.device)
+    ca = aux._c() if aux is not None else None
+    st = _lib.load().grpo_loss_fwd_bwd_vocab_shard(
+        _ptr(logits), dt, T, Vv, ld, int(v_begin), int(V_total), _ptr(stats_all), int(n_shards), _ptr(actions),
+        _ptr(_f32(behave_logp, "behave_logp")), _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")),
+        ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dlogits),
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "grpo_loss_fwd_bwd_vocab_shard")
+    return loss_out, dlogits

@@ -79,6 +79,12 @@ def load() -> ctypes.CDLL:
         lib.fused_lmhead_grpo.restype = ctypes.c_int
         lib.grpo_token_logp.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P, P]
         lib.grpo_token_logp.restype = ctypes.c_int
+        lib.grpo_vocab_shard_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, I64, P, P, P, P]
+        lib.grpo_vocab_shard_stats.restype = ctypes.c_int
+        lib.grpo_loss_fwd_bwd_vocab_shard.argtypes = [P, ctypes.c_int, I64, I64, I64, I64, I64, P, I32, P, P, P, P,
+                                                      ctypes.POINTER(Segments), ctypes.POINTER(LossParams), P, P,
+                                                      ctypes.POINTER(Aux), P, SZ, P]
+        lib.grpo_loss_fwd_bwd_vocab_shard.restype = ctypes.c_int
         lib.grpo_status_str.argtypes = [ctypes.c_int]
         lib.grpo_status_str.restype = ctypes.c_char_p
         _lib = lib

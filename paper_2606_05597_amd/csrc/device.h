@@ -212,4 +212,45 @@ __device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn
   return rs;
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// dlogits of one vector: |d_v| = 2^(z_v*log2e + nc), the row's sign applied to
+// the packed result, and the action column (when it falls in this vector)
+// replaced by d_a.
+template <typename Tin>
+__device__ __forceinline__ u32x4 vec_dlogits(const u32x4& x, const RowScale& rs, uint32_t signmask, bool has_act,
+                                             int act_lane) {
+  u32x4 o;
+  if constexpr (sizeof(Tin) == 2) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float lo = __builtin_amdgcn_exp2f(fmaf(bf16_lo(x[q]), kLog2e, rs.nc));
+      const float hi = __builtin_amdgcn_exp2f(fmaf(bf16_hi(x[q]), kLog2e, rs.nc));
+      o[q] = pack_bf16(lo, hi) ^ signmask;
+    }
+    if (has_act) {
+      const uint32_t da = pack_bf16(rs.d_a, 0.f) & 0xffffu;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((act_lane >> 1) == q) o[q] = (act_lane & 1) ? ((o[q] & 0xffffu) | (da << 16)) : ((o[q] & 0xffff0000u) | da);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      o[q] = __float_as_uint(__builtin_amdgcn_exp2f(fmaf(__uint_as_float(x[q]), kLog2e, rs.nc))) ^ signmask;
+    if (has_act) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (act_lane == q) o[q] = __float_as_uint(rs.d_a);
+    }
+  }
+  return o;
+}
+
+template <typename Tin>
+__device__ __forceinline__ uint32_t sign_mask(const RowScale& rs) {
+  if (rs.sign >= 0.f) return 0u;
+  return sizeof(Tin) == 2 ? 0x80008000u : 0x80000000u;
+}
+
 }  // namespace grpo

@@ -1,6 +1,8 @@
 // Forward only: the sampled action's log-prob and the policy entropy of each
 // token row (the proximal log-probs recomputed before an update, Table 5, and
-// the per-token entropy of Sec. 5), one workgroup per row.
+// the per-token entropy of Sec. 5), one workgroup per row.  The same kernels
+// also reduce one shard of a vocabulary split over devices to its per-token
+// record (max, sum exp, action logit; grpo_vocab_shard_stats).
 //
 // A row is read once.  Each thread walks its 16-byte vectors U at a time (all U
 // loads in flight together) and keeps, relative to its running shift m,
@@ -21,11 +23,13 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 struct LogpArgs {
   const void* logits;
   int64_t ld, V;
+  int64_t v_begin;  // global id of column 0 (a shard's first column; 0 otherwise)
   int T;
   const int32_t* actions;
   float* logp;      // nullable
   float* entropy;   // nullable
   int32_t* flags;   // nullable
+  grpo_vocab_stats* stats;  // non-null: write each row's shard record instead of logp / entropy
 };
 
 // One element folded into (s, t) at the current shift m.
@@ -89,6 +93,15 @@ __device__ __forceinline__ float elem(const u32x4& x, int e) {
 template <typename Tin>
 __device__ __forceinline__ void row_out(const LogpArgs& a, int t, double M, double S, double Tsum, double za,
                                         bool act_ok) {
+  if (a.stats) {
+    grpo_vocab_stats r;
+    r.m = (float)M;  // the maximum of stored values: exact
+    r.z_a = act_ok ? (float)za : -INFINITY;
+    r.s = S;
+    a.stats[t] = r;
+    if (a.flags && (isnan(M) || isnan(S) || M == INFINITY)) atomicOr(a.flags, GRPO_FLAG_NONFINITE);
+    return;
+  }
   const double lse = M + log(S);
   if (a.logp) a.logp[t] = act_ok ? (float)(za - lse) : 0.f;
   if (a.entropy) a.entropy[t] = (float)(log(S) - Tsum / S);
@@ -108,8 +121,9 @@ __global__ __launch_bounds__(NT) void k_logp_vec(const LogpArgs a) {
   const int t = blockIdx.x, tid = threadIdx.x;
   const int nvec = (int)(a.V / EPV);
   const u32x4* row = reinterpret_cast<const u32x4*>(static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld);
-  const int act = a.actions[t];
-  const bool act_ok = act >= 0 && (int64_t)act < a.V;
+  const int64_t act64 = (int64_t)a.actions[t] - a.v_begin;
+  const bool act_ok = act64 >= 0 && act64 < a.V;
+  const int act = act_ok ? (int)act64 : 0;
   const int act_vec = act_ok ? act / EPV : -1;
   float m = -INFINITY, s = 0.f, tt = 0.f;
   for (int base = tid; base < nvec; base += NT * U) {
@@ -169,13 +183,24 @@ __global__ __launch_bounds__(256) void k_logp_generic(const LogpArgs a) {
   double M, S, Tsum;
   block_combine3<NW>(m, s, tt, sh_m, sh_s, sh_t, M, S, Tsum);
   if (tid == 0) {
-    const int act = a.actions[t];
-    const bool act_ok = act >= 0 && (int64_t)act < a.V;
+    const int64_t act = (int64_t)a.actions[t] - a.v_begin;
+    const bool act_ok = act >= 0 && act < a.V;
     row_out<Tin>(a, t, M, S, Tsum, act_ok ? (double)load_one<Tin>(row + act) : 0.0, act_ok);
   }
 }
 
 __global__ void k_clear_flag(int32_t* f) { *f = 0; }
+
+// One workgroup per row: the vector kernel when rows are whole 16-byte vectors, else the element kernel.
+static void launch_logp(const LogpArgs& a, grpo_dtype dt, hipStream_t s) {
+  const int esz = (dt == GRPO_BF16) ? 2 : 4, epv = 16 / esz;
+  const bool vec = a.V % epv == 0 && a.ld % epv == 0 && aligned(a.logits, 16);
+  const dim3 grid((unsigned)a.T);
+  if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_logp_vec<uint16_t, 256, 4>), grid, dim3(256), 0, s, a);
+  else if (vec) hipLaunchKernelGGL((k_logp_vec<float, 256, 4>), grid, dim3(256), 0, s, a);
+  else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_logp_generic<uint16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_logp_generic<float>, grid, dim3(256), 0, s, a);
+}
 
 }  // namespace grpo
 
@@ -191,14 +216,26 @@ extern "C" int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int
   if (!aligned(logits, esz)) return GRPO_ERR_ALIGN;
   if (error_flags) hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, error_flags);
   if (T > 0) {
-    LogpArgs a{logits, ld, V, (int)T, actions, token_logp, token_entropy, error_flags};
-    const int epv = 16 / esz;
-    const bool vec = V % epv == 0 && ld % epv == 0 && aligned(logits, 16);
-    const dim3 grid((unsigned)T);
-    if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_logp_vec<uint16_t, 256, 4>), grid, dim3(256), 0, s, a);
-    else if (vec) hipLaunchKernelGGL((k_logp_vec<float, 256, 4>), grid, dim3(256), 0, s, a);
-    else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_logp_generic<uint16_t>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_logp_generic<float>, grid, dim3(256), 0, s, a);
+    LogpArgs a{logits, ld, V, 0, (int)T, actions, token_logp, token_entropy, error_flags, nullptr};
+    launch_logp(a, dt, s);
+  }
+  return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+}
+
+extern "C" int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+                                      int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats,
+                                      int32_t* error_flags, hipStream_t s) {
+  if (T < 0 || T >= ((int64_t)1 << 31) || V_shard < 1 || ld < V_shard || v_begin < 0 ||
+      v_begin + V_shard >= ((int64_t)1 << 31))
+    return GRPO_ERR_SHAPE;
+  if (T > 0 && (!logits || !actions || !stats)) return GRPO_ERR_ARG;
+  if (dt != GRPO_F32 && dt != GRPO_BF16) return GRPO_ERR_DTYPE;
+  const int esz = (dt == GRPO_BF16) ? 2 : 4;
+  if (!aligned(logits, esz) || !aligned(stats, 16)) return GRPO_ERR_ALIGN;
+  if (error_flags) hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, error_flags);
+  if (T > 0) {
+    LogpArgs a{logits, ld, V_shard, v_begin, (int)T, actions, nullptr, nullptr, error_flags, stats};
+    launch_logp(a, dt, s);
   }
   return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
 }

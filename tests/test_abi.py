@@ -35,6 +35,7 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes",
                                            "grpo_loss_fwd_bwd",
                                            "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_token_logp",
+                                           "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
                                            "grpo_status_str"])
 
 
@@ -173,6 +174,57 @@ def call_logp(lib, *, logits=D, dt=_lib.GRPO_BF16, T=8, V=64, ld=64, actions=D):
 ])
 def test_token_logp_rejects_bad_arguments(lib, kw, status):
     assert call_logp(lib, **kw) == status
+
+
+def call_shard_stats(lib, *, logits=D, dt=_lib.GRPO_BF16, T=8, V=64, ld=64, v_begin=0, actions=D, stats=D):
+    return lib.grpo_vocab_shard_stats(logits, dt, T, V, ld, v_begin, actions, stats, None, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(logits=None), _lib.GRPO_ERR_ARG),
+    (dict(actions=None), _lib.GRPO_ERR_ARG),
+    (dict(stats=None), _lib.GRPO_ERR_ARG),
+    (dict(T=-1), _lib.GRPO_ERR_SHAPE),
+    (dict(V=0), _lib.GRPO_ERR_SHAPE),
+    (dict(ld=63), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=-8), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=(1 << 31) - 64), _lib.GRPO_ERR_SHAPE),  # the shard's last column past 2^31
+    (dict(dt=3), _lib.GRPO_ERR_DTYPE),
+    (dict(logits=ctypes.c_void_p(0x100001)), _lib.GRPO_ERR_ALIGN),
+    (dict(stats=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),  # records are 16-byte aligned
+])
+def test_shard_stats_rejects_bad_arguments(lib, kw, status):
+    assert call_shard_stats(lib, **kw) == status
+
+
+def call_shard_loss(lib, *, T=8, V=64, ld=64, v_begin=0, V_total=128, stats=D, n_shards=2, logits=D, dlogits=D,
+                    dt=_lib.GRPO_BF16, ws=D, ws_bytes=1 << 30):
+    seg = _lib.Segments()
+    seg.n_traj, seg.group_size, seg.n_steps = 4, 4, 4
+    seg.step_tok_off, seg.traj_step_off = D, D
+    p = _lib.LossParams()
+    p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale = 1, 10.0, 0.2, 0.2, 0.0, 1.0
+    return lib.grpo_loss_fwd_bwd_vocab_shard(logits, dt, T, V, ld, v_begin, V_total, stats, n_shards, D, D, None, D,
+                                             ctypes.byref(seg), ctypes.byref(p), D, dlogits, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(logits=None), _lib.GRPO_ERR_ARG),
+    (dict(stats=None), _lib.GRPO_ERR_ARG),
+    (dict(V=0), _lib.GRPO_ERR_SHAPE),
+    (dict(ld=63), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=-1), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=72), _lib.GRPO_ERR_SHAPE),          # v_begin + V_shard > V_total
+    (dict(V_total=1 << 31), _lib.GRPO_ERR_SHAPE),
+    (dict(n_shards=0), _lib.GRPO_ERR_SHAPE),
+    (dict(n_shards=65537), _lib.GRPO_ERR_SHAPE),
+    (dict(dt=9), _lib.GRPO_ERR_DTYPE),
+    (dict(stats=ctypes.c_void_p(0x100004)), _lib.GRPO_ERR_ALIGN),
+    (dict(dlogits=ctypes.c_void_p(0x100001)), _lib.GRPO_ERR_ALIGN),
+    (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
+])
+def test_shard_loss_rejects_bad_arguments(lib, kw, status):
+    assert call_shard_loss(lib, **kw) == status
 
 
 def test_advantages_ex_rejects_bad_arguments(lib):
