@@ -7,6 +7,10 @@ row pass with dlogits, loss reduction).  Workload: 16 task groups x G = 8
 trajectories, T = 120,000 action tokens, V = 151,936, bf16 logits (the
 realistic-vocabulary rollout batch), synthetic and seeded.
 
+One device's share of the vocabulary-parallel loss (the same batch's vocabulary
+split 8 ways, 18,992 columns) is reported under "vocab_shard", and the
+forward-only log-prob + entropy pass under "token_logp".
+
 The fused LM-head path is measured in the same run on its own workload
 (hidden bf16 [65,536, 3,584], W bf16 [3,584, 151,936], vocabulary chunks of
 8192) and reported under "fused_lmhead" against the bf16 dense MFMA peak, with
@@ -67,6 +71,8 @@ def parse():
     ap.add_argument("--fused-steps", type=int, default=3, help="timed steps of the fused path (0 = skip)")
     ap.add_argument("--logp-steps", type=int, default=10,
                     help="timed steps of the forward-only log-prob + entropy path (0 = skip)")
+    ap.add_argument("--shard-steps", type=int, default=10,
+                    help="timed steps of one device's share of the vocabulary-parallel loss (0 = skip)")
     ap.add_argument("--skip-logits", action="store_true", help="measure only the fused path")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter calibration)")
@@ -143,6 +149,73 @@ def bench_logp(b: dict, steps: int, warmup: int = 2) -> dict:
                          "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                          "kernel": "k_logp_vec<bf16, 256, 4> (one workgroup per row)", "kernel_ms": hot_ms,
                          "algorithmic_bytes_per_launch": alg}}
+
+
+def bench_vocab_shard(b: dict, steps: int, n_shards: int = 8, warmup: int = 2) -> dict:
+    """Times one device's share of the vocabulary-parallel loss: the vocabulary of the resident batch split
+    n_shards ways, the first shard held contiguous [T, V / n_shards].  A step is that shard's statistics pass and
+    its loss/dlogits pass, with every shard's records already gathered (they are computed once, untimed, from
+    the other column ranges of the same logits)."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    cfg, st = b["cfg"], b["structure"]
+    T, V = b["logits"].shape
+    Vs = V // n_shards
+    dev = b["logits"].device
+    N = len(st.rewards)
+    stats = torch.empty((n_shards, T, grpo.VOCAB_STATS_BYTES), dtype=torch.uint8, device=dev)
+    for g in range(n_shards):
+        grpo.grpo_vocab_shard_stats(b["logits"][:, g * Vs:(g + 1) * Vs], b["actions"], g * Vs, stats=stats[g])
+    shard = b["logits"][:, :Vs].contiguous()
+    dshard = torch.empty_like(shard)
+    sto = torch.from_numpy(st.step_tok_off).to(dev)
+    tso = torch.from_numpy(st.traj_step_off).to(dev)
+    adv = grpo.grpo_advantages(b["rewards"], cfg.G)
+    ws = torch.empty(grpo.grpo_loss_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    el = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e in [x for pair in es + el for x in pair]:
+        e.record(stream)  # creates the underlying hipEvent_t
+    torch.cuda.synchronize()
+
+    def step(i=None):
+        if i is not None:
+            es[i][0].record(stream)
+        grpo.grpo_vocab_shard_stats(shard, b["actions"], 0, stats=stats[0])
+        if i is not None:
+            es[i][1].record(stream)
+        aux = grpo.LossAux(hot_events=(el[i][0].cuda_event, el[i][1].cuda_event)) if i is not None else None
+        grpo.grpo_loss_fwd_bwd_vocab_shard(shard, stats, 0, V, b["actions"], b["behave"], adv, sto, tso, cfg.G,
+                                           norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, dual_clip_c=3.0, dlogits=dshard,
+                                           aux=aux, workspace=ws, loss_out=loss)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    stats_ms = sum(a.elapsed_time(c) for a, c in es) / steps
+    rows_ms = sum(a.elapsed_time(c) for a, c in el) / steps
+    alg_stats = T * (2.0 * Vs + 4 + 16)  # the shard's row read once, the action id, one record written
+    alg_rows = T * (4.0 * Vs + 16 + 16.0 * n_shards)  # read + dlogits written, token inputs, every shard's record
+
+    def roof(alg, kms, kernel):
+        a = alg / (kms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a / HBM_PEAK_GBS,
+                "traffic": None, "kernel": kernel, "kernel_ms": kms, "algorithmic_bytes_per_launch": alg}
+
+    return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
+            "workload": f"one device's share of the {V}-column vocabulary split {n_shards} ways: bf16 [{T}, {Vs}], "
+                        f"statistics pass + loss/dlogits pass",
+            "loss": float(loss.item()),
+            "roofline_stats": roof(alg_stats, stats_ms, "k_logp_vec<bf16, 256, 4> in record mode"),
+            "roofline_rows": roof(alg_rows, rows_ms, "k_shard_rows_vec<bf16, 256, 4>")}
 
 
 def bench_fused(steps: int, warmup: int = 1) -> dict:
@@ -287,6 +360,8 @@ def main():
         out["cpu_baseline"] = cpu_baseline(b, A, args.cpu_seconds)
     if args.logp_steps > 0:
         out["token_logp"] = bench_logp(b, args.logp_steps)
+    if args.shard_steps > 0:
+        out["vocab_shard"] = bench_vocab_shard(b, args.shard_steps)
     if args.fused_steps > 0:
         del b
         torch.cuda.empty_cache()
