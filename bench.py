@@ -215,7 +215,7 @@ def bench_vocab_shard(b: dict, steps: int, n_shards: int = 8, warmup: int = 2) -
                         f"statistics pass + loss/dlogits pass",
             "loss": float(loss.item()),
             "roofline_stats": roof(alg_stats, stats_ms, "k_logp_vec<bf16, 256, 4> in record mode"),
-            "roofline_rows": roof(alg_rows, rows_ms, "k_shard_rows_vec<bf16, 256, 4>")}
+            "roofline_rows": roof(alg_rows, rows_ms, "k_shard_rows_vec<bf16, 512, 5>")}
 
 
 def bench_fused(steps: int, warmup: int = 1) -> dict:

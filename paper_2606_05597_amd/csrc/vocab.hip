@@ -178,8 +178,8 @@ extern "C" int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, 
     const dim3 grid((unsigned)T);
     const bool timed = aux && aux->hot_begin && aux->hot_end;
     if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
-    if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_shard_rows_vec<uint16_t, 256, 4>), grid, dim3(256), 0, s, a);
-    else if (vec) hipLaunchKernelGGL((k_shard_rows_vec<float, 256, 4>), grid, dim3(256), 0, s, a);
+    if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_shard_rows_vec<uint16_t, 512, 5>), grid, dim3(512), 0, s, a);
+    else if (vec) hipLaunchKernelGGL((k_shard_rows_vec<float, 512, 5>), grid, dim3(512), 0, s, a);
     else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_shard_rows_generic<uint16_t>, grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL(k_shard_rows_generic<float>, grid, dim3(256), 0, s, a);
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
