@@ -202,8 +202,9 @@ def bench_vocab_shard(b: dict, steps: int, n_shards: int = 8, warmup: int = 2) -
     ms = (time.perf_counter() - t0) * 1e3 / steps
     stats_ms = sum(a.elapsed_time(c) for a, c in es) / steps
     rows_ms = sum(a.elapsed_time(c) for a, c in el) / steps
-    alg_stats = T * (2.0 * Vs + 4 + 16)  # the shard's row read once, the action id, one record written
-    alg_rows = T * (4.0 * Vs + 16 + 16.0 * n_shards)  # read + dlogits written, token inputs, every shard's record
+    rec = grpo.VOCAB_STATS_BYTES
+    alg_stats = T * (2.0 * Vs + 4 + rec)  # the shard's row read once, the action id, one record written
+    alg_rows = T * (4.0 * Vs + 16 + rec * n_shards)  # read + dlogits written, token inputs, every shard's record
 
     def roof(alg, kms, kernel):
         a = alg / (kms * 1e-3) / 1e9

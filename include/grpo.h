@@ -237,17 +237,18 @@ int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int
  * V_shard).  The exchange between the two calls (gathering every shard's
  * records on every device) is the caller's.
  *
- * One shard's per-token record, 16 bytes:
+ * One shard's per-token record, 24 bytes, all fp64 (no rounding between the
+ * shard's reduction and the merge):
  *   m    max over the shard's columns of the row (-inf for a row of -inf)
+ *   s    sum over the shard's columns of exp(z - m)
  *   z_a  the action's logit if a_t is one of the shard's columns, else -inf
- *   s    sum over the shard's columns of exp(z - m), in fp64
  * Any split of a row merges back to its log-sum-exp M + log sum_g s_g exp(m_g - M),
  * M = max_g m_g, and to its action logit max_g z_a_g.
  */
 typedef struct {
-  float m;
-  float z_a;
+  double m;
   double s;
+  double z_a;
 } grpo_vocab_stats;
 
 /*
@@ -255,7 +256,7 @@ typedef struct {
  *   logits       device [T, ld] of `dt`, the shard's columns; columns >= V_shard unread
  *   T >= 0, 1 <= V_shard <= ld, v_begin >= 0, v_begin + V_shard < 2^31
  *   actions      device int32 [T]  global token ids
- *   stats        device grpo_vocab_stats [T], 16-byte aligned (written)
+ *   stats        device grpo_vocab_stats [T], 8-byte aligned (written)
  *   error_flags  device int32 [1] or NULL: overwritten with GRPO_FLAG_NONFINITE
  *                when a row's shard log-sum-exp is NaN or +inf (an action outside
  *                the shard is not an error here; step 2 checks a_t against V_total)
@@ -273,7 +274,7 @@ int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t T, int64_t
  *   V_total      the whole vocabulary (actions outside [0, V_total) are flagged and
  *                their tokens leave the loss, as in grpo_loss_fwd_bwd)
  *   stats        device grpo_vocab_stats [n_shards][T]: every shard's records from
- *                step 1, in the same shard order on every device; 16-byte aligned
+ *                step 1, in the same shard order on every device; 8-byte aligned
  *   n_shards     1 .. 65536
  *   actions, behave_logp, prox_logp, adv, seg, p, loss_out, aux, ws, ws_bytes: as
  *                grpo_loss_fwd_bwd (workspace from grpo_loss_workspace_bytes; the
@@ -293,6 +294,54 @@ int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, int64_t T, 
                                   const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
                                   double* loss_out, void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes,
                                   hipStream_t s);
+
+/* Bytes of device workspace fused_lmhead_vocab_shard_stats needs (the shard's W^T and pass-1 partials). */
+size_t fused_lmhead_vocab_shard_stats_workspace_bytes(int64_t T, int64_t H, int64_t V_shard);
+
+/*
+ * Step 1 of the sharded fused LM head: the device holding W's columns
+ * [v_begin, v_begin + V_shard) reduces every row of z = h W_shard to its
+ * grpo_vocab_stats record (m and s from the matrix-core logits; z_a = h_t .
+ * W[:, a_t] in fp64, rounded to fp32, when a_t is one of the shard's columns).
+ *   hidden       device bf16 [T, H] row-major       w_shard device bf16 [H, V_shard] row-major
+ *   T >= 0, H >= 64 and a multiple of 64, V_shard >= 8 and a multiple of 8,
+ *   v_begin >= 0, v_begin + V_shard < 2^31
+ *   actions      device int32 [T]  global token ids
+ *   stats        device grpo_vocab_stats [T] (written)
+ *   ws, ws_bytes device workspace of at least fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, V_shard)
+ * hidden and w_shard must be 16-byte aligned, stats 8-byte aligned.
+ * Errors: GRPO_ERR_ARG, GRPO_ERR_SHAPE, GRPO_ERR_ALIGN, GRPO_ERR_WORKSPACE, GRPO_ERR_HIP.
+ */
+int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_shard, int64_t T, int64_t H, int64_t V_shard,
+                                   int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats, void* ws,
+                                   size_t ws_bytes, hipStream_t s);
+
+/*
+ * Step 2 of the sharded fused LM head: given every shard's records (gathered by the
+ * caller, the same shard order on every device), the loss (the whole rows', the same
+ * on every shard), this shard's dW columns and its partial dhidden.
+ *   hidden, w_shard, T, H, V_shard, v_begin: as in step 1
+ *   V_total      the whole vocabulary; vocab_chunk as in fused_lmhead_grpo
+ *   stats        device grpo_vocab_stats [n_shards][T], 8-byte aligned; n_shards 1 .. 65536
+ *   actions, behave_logp, prox_logp, adv, seg, p, loss_out, aux: as grpo_loss_fwd_bwd
+ *   dhidden_partial device fp32 [T, H] (written): D_shard W_shard^T, the shard's share of
+ *                dhidden; the caller sums the shards' partials (a reduce-scatter across
+ *                devices) and rounds as it needs
+ *   dw_shard     device fp32 [H, V_shard]: this shard's dW columns, written or
+ *                accumulated into (accumulate_dw != 0)
+ *   ws, ws_bytes device workspace of at least fused_lmhead_workspace_bytes(T, H, V_shard,
+ *                vocab_chunk, n_traj)
+ * D = grad_scale * dloss/dz is rounded to bf16 per chunk before the two products, as in
+ * fused_lmhead_grpo.  Errors: as fused_lmhead_grpo, plus GRPO_ERR_SHAPE for v_begin < 0,
+ * v_begin + V_shard > V_total, V_total >= 2^31 or n_shards outside 1..65536, and GRPO_ERR_ARG
+ * for stats or dhidden_partial NULL with T > 0.
+ */
+int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_shard, int64_t T, int64_t H, int64_t V_shard,
+                                  int64_t v_begin, int64_t V_total, int32_t vocab_chunk, const grpo_vocab_stats* stats,
+                                  int32_t n_shards, const int32_t* actions, const float* behave_logp,
+                                  const float* prox_logp, const float* adv, const grpo_segments* seg,
+                                  const grpo_loss_params* p, double* loss_out, float* dhidden_partial, float* dw_shard,
+                                  int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
 
 /* A static, human-readable name for a grpo_status value. */
 const char* grpo_status_str(int status);

@@ -20,7 +20,8 @@ from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO
 
 __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
            "fused_lmhead_grpo", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
-           "vocab_stats_fields", "grpo_status_str", "LossAux", "GrpoError"]
+           "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
+           "grpo_status_str", "LossAux", "GrpoError"]
 
 
 def _ptr(t):
@@ -287,13 +288,13 @@ def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | Non
     return logp, ent
 
 
-VOCAB_STATS_BYTES = 16  # one grpo_vocab_stats record: fp32 m, fp32 z_a, fp64 s
+VOCAB_STATS_BYTES = 24  # one grpo_vocab_stats record: fp64 m, s, z_a
 
 
 def vocab_stats_fields(stats: torch.Tensor):
-    """Views of a uint8 [..., T, 16] record tensor as (m fp32, z_a fp32, s fp64), each [..., T]."""
-    f32 = stats.view(torch.float32)
-    return f32[..., 0], f32[..., 1], stats.view(torch.float64)[..., 1]
+    """Views of a uint8 [..., T, 24] record tensor as (m, z_a, s), each fp64 [..., T]."""
+    f64 = stats.view(torch.float64)
+    return f64[..., 0], f64[..., 2], f64[..., 1]
 
 
 def _logits2d(logits, name="logits"):
@@ -312,7 +313,7 @@ def _logits2d(logits, name="logits"):
 def grpo_vocab_shard_stats(logits: torch.Tensor, actions: torch.Tensor, v_begin: int, *, V: int | None = None,
                            stats: torch.Tensor | None = None, error_flags: torch.Tensor | None = None, stream=None):
     """Step 1 of the vocabulary-sharded loss: each row of the shard (global columns [v_begin, v_begin + V)) reduced
-    to its record.  Returns uint8 [T, 16] records (read them with ``vocab_stats_fields``)."""
+    to its record.  Returns uint8 [T, 24] records (read them with ``vocab_stats_fields``)."""
     dt, T, ld = _logits2d(logits)
     Vv = logits.shape[1] if V is None else int(V)
     _dev(actions, "actions")
@@ -322,7 +323,7 @@ def grpo_vocab_shard_stats(logits: torch.Tensor, actions: torch.Tensor, v_begin:
         stats = torch.empty((T, VOCAB_STATS_BYTES), dtype=torch.uint8, device=logits.device)
     _dev(stats, "stats")
     if stats.dtype != torch.uint8 or tuple(stats.shape) != (T, VOCAB_STATS_BYTES):
-        raise ValueError("stats must be uint8 [T, 16]")
+        raise ValueError(f"stats must be uint8 [T, {VOCAB_STATS_BYTES}]")
     if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
         raise ValueError("error_flags must be an int32 GPU tensor")
     st = _lib.load().grpo_vocab_shard_stats(_ptr(logits), dt, T, Vv, ld, int(v_begin), _ptr(actions), _ptr(stats),
@@ -341,7 +342,7 @@ def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor,
                                   workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None,
                                   stream=None):
     """Step 2 of the vocabulary-sharded loss: the loss (fp64 [1], the whole rows') and this shard's dlogits, from
-    the shard's logits and every shard's records ``stats_all`` (uint8 [n_shards, T, 16], in shard order).
+    the shard's logits and every shard's records ``stats_all`` (uint8 [n_shards, T, 24], in shard order).
 
     ``dlogits``: True allocates a tensor like ``logits``; None/False is forward only; a tensor is written in place.
     Returns (loss, dlogits or None).
@@ -353,7 +354,7 @@ def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor,
         raise TypeError("actions must be int32")
     _dev(stats_all, "stats_all")
     if stats_all.dtype != torch.uint8 or stats_all.dim() != 3 or tuple(stats_all.shape[1:]) != (T, VOCAB_STATS_BYTES):
-        raise ValueError("stats_all must be uint8 [n_shards, T, 16]")
+        raise ValueError(f"stats_all must be uint8 [n_shards, T, {VOCAB_STATS_BYTES}]")
     n_shards = stats_all.shape[0]
     seg = _segments(step_tok_off, traj_step_off, group_size)
     par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
@@ -377,3 +378,83 @@ def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor,
         ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "grpo_loss_fwd_bwd_vocab_shard")
     return loss_out, dlogits
+
+
+def fused_lmhead_vocab_shard_stats(hidden: torch.Tensor, w_shard: torch.Tensor, actions: torch.Tensor, v_begin: int,
+                                   *, stats: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                                   stream=None):
+    """Step 1 of the vocabulary-sharded fused LM head: each row of h W_shard (W's columns [v_begin, v_begin +
+    V_shard)) reduced to its record.  Returns uint8 [T, 24] records (read them with ``vocab_stats_fields``)."""
+    _dev(hidden, "hidden")
+    _dev(w_shard, "w_shard")
+    if hidden.dtype != torch.bfloat16 or w_shard.dtype != torch.bfloat16:
+        raise TypeError("hidden and w_shard must be bfloat16")
+    T, H = hidden.shape
+    H2, Vs = w_shard.shape
+    if H2 != H:
+        raise ValueError("hidden and w_shard disagree on H")
+    _dev(actions, "actions")
+    if stats is None:
+        stats = torch.empty((T, VOCAB_STATS_BYTES), dtype=torch.uint8, device=hidden.device)
+    _dev(stats, "stats")
+    if stats.dtype != torch.uint8 or tuple(stats.shape) != (T, VOCAB_STATS_BYTES):
+        raise ValueError(f"stats must be uint8 [T, {VOCAB_STATS_BYTES}]")
+    lib = _lib.load()
+    need = lib.fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    st = lib.fused_lmhead_vocab_shard_stats(_ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), _ptr(actions),
+                                            _ptr(stats), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "fused_lmhead_vocab_shard_stats")
+    return stats
+
+
+def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, stats_all: torch.Tensor, v_begin: int,
+                                  V_total: int, actions: torch.Tensor, behave_logp: torch.Tensor, adv: torch.Tensor,
+                                  step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *,
+                                  vocab_chunk: int = 8192, prox_logp: torch.Tensor | None = None,
+                                  norm: int = GRPO_NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2,
+                                  eps_high: float = 0.2, dual_clip_c: float = 0.0, grad_scale: float = 1.0,
+                                  n_groups_total: float = 0.0, dhidden_partial: torch.Tensor | None = None,
+                                  dw_shard: torch.Tensor | None = None, accumulate_dw: bool = False,
+                                  aux: LossAux | None = None, workspace: torch.Tensor | None = None,
+                                  loss_out: torch.Tensor | None = None, stream=None):
+    """Step 2 of the vocabulary-sharded fused LM head: the loss (fp64 [1]), this shard's partial dhidden (fp32
+    [T, H], to be summed over the shards) and its dW columns (fp32 [H, V_shard]), from every shard's records
+    ``stats_all`` (uint8 [n_shards, T, 24], in shard order).  Returns (loss, dhidden_partial, dw_shard)."""
+    _dev(hidden, "hidden")
+    _dev(w_shard, "w_shard")
+    if hidden.dtype != torch.bfloat16 or w_shard.dtype != torch.bfloat16:
+        raise TypeError("hidden and w_shard must be bfloat16")
+    T, H = hidden.shape
+    H2, Vs = w_shard.shape
+    if H2 != H:
+        raise ValueError("hidden and w_shard disagree on H")
+    _dev(actions, "actions")
+    _dev(stats_all, "stats_all")
+    if stats_all.dtype != torch.uint8 or stats_all.dim() != 3 or tuple(stats_all.shape[1:]) != (T, VOCAB_STATS_BYTES):
+        raise ValueError(f"stats_all must be uint8 [n_shards, T, {VOCAB_STATS_BYTES}]")
+    seg = _segments(step_tok_off, traj_step_off, group_size)
+    par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
+    if dhidden_partial is None:
+        dhidden_partial = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
+    if dw_shard is None:
+        dw_shard = torch.empty((H, Vs), dtype=torch.float32, device=hidden.device)
+    _dev(dhidden_partial, "dhidden_partial")
+    _dev(dw_shard, "dw_shard")
+    if dhidden_partial.dtype != torch.float32 or dw_shard.dtype != torch.float32:
+        raise TypeError("dhidden_partial and dw_shard must be float32")
+    need = fused_lmhead_workspace_bytes(T, H, Vs, vocab_chunk, seg.n_traj)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    if loss_out is None:
+        loss_out = torch.empty(1, dtype=torch.float64, device=hidden.device)
+    ca = aux._c() if aux is not None else None
+    st = _lib.load().fused_lmhead_grpo_vocab_shard(
+        _ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), int(V_total), int(vocab_chunk), _ptr(stats_all),
+        int(stats_all.shape[0]), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
+        _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
+        _ptr(loss_out), _ptr(dhidden_partial), _ptr(dw_shard), int(bool(accumulate_dw)),
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "fused_lmhead_grpo_vocab_shard")
+    return loss_out, dhidden_partial, dw_shard

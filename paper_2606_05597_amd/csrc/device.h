@@ -212,6 +212,28 @@ __device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn
   return rs;
 }
 
+// A row's log-sum-exp and action logit from the per-token records of every shard
+// of a vocabulary split over devices (stats [n_shards][T]), merged in shard order
+// so that every device gets the same bits: lse = M + log sum_g s_g e^(m_g - M),
+// M = max_g m_g, and z_a = max_g z_a_g (only the owner's is finite).  A NaN
+// maximum propagates.
+__device__ inline void merge_vocab_stats(const grpo_vocab_stats* stats, int n_shards, int T, int t, double& lse,
+                                         double& za) {
+  double M = -INFINITY, z = -INFINITY;
+  for (int g = 0; g < n_shards; ++g) {
+    const grpo_vocab_stats r = stats[(int64_t)g * T + t];
+    if (r.m > M || isnan(r.m)) M = r.m;
+    z = fmax(z, r.z_a);
+  }
+  double S = 0.0;
+  for (int g = 0; g < n_shards; ++g) {
+    const grpo_vocab_stats r = stats[(int64_t)g * T + t];
+    if (r.m != -INFINITY) S += r.s * exp(r.m - M);
+  }
+  lse = row_lse(M, S);
+  za = z;
+}
+
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // dlogits of one vector: |d_v| = 2^(z_v*log2e + nc), the row's sign applied to

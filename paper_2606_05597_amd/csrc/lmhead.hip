@@ -145,26 +145,23 @@ struct CombineArgs {
   int T, H, n_tiles;
 };
 
-__global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
-  __shared__ float sh_m[4];
-  __shared__ double sh_s[4], sh_z[4];
-  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  if (t >= a.T) {
-    if (tid == 0) a.rs[t] = RowScale{-INFINITY, 1.f, 0.f, -1};
-    return;
-  }
-  const float2* pr = a.part + (int64_t)t * a.n_tiles;
+// Row t of 256 threads: the row's shift M and S = sum over its tiles of the partials rescaled to M, and the
+// action logit z_a = h_t . W[:, act] (row act of the transposed weight) in fp64, or 0 when act < 0.  The
+// results are valid in thread 0.
+struct RowStatsSmem {
+  float m[4];
+  double s[4], z[4];
+};
+__device__ inline void lm_row_stats(const float2* pr, int n_tiles, const uint16_t* hr, const uint16_t* WT, int act,
+                                    int H, RowStatsSmem& sh, float& M_out, double& S_out, double& z_out) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   float m = -INFINITY;
-  for (int j = tid; j < a.n_tiles; j += 256) m = fmaxf(m, pr[j].x);
+  for (int j = tid; j < n_tiles; j += 256) m = fmaxf(m, pr[j].x);
   m = wave_max(m);
-  // the action logit z_a = h_t . W[:, a] (row a of the transposed weight), in fp64
-  const int act = a.tok.actions[t];
-  const bool ok = act >= 0 && (int64_t)act < a.tok.V;
   double z = 0.0;
-  if (ok) {
-    const uint16_t* hr = a.h + (int64_t)t * a.H;
-    const uint16_t* wr = a.WT + (int64_t)act * a.H;
-    for (int k = tid * 8; k < a.H; k += 256 * 8) {
+  if (act >= 0) {
+    const uint16_t* wr = WT + (int64_t)act * H;
+    for (int k = tid * 8; k < H; k += 256 * 8) {
       const u32x4 x = *reinterpret_cast<const u32x4*>(hr + k);
       const u32x4 y = *reinterpret_cast<const u32x4*>(wr + k);
 #pragma unroll
@@ -176,26 +173,96 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   }
   z = wave_sum(z);
   if (lane == 0) {
-    sh_m[wv] = m;
-    sh_z[wv] = z;
+    sh.m[wv] = m;
+    sh.z[wv] = z;
   }
   __syncthreads();
-  const float M = fmaxf(fmaxf(sh_m[0], sh_m[1]), fmaxf(sh_m[2], sh_m[3]));
+  const float M = fmaxf(fmaxf(sh.m[0], sh.m[1]), fmaxf(sh.m[2], sh.m[3]));
   double s = 0.0;
   if (M != -INFINITY)
-    for (int j = tid; j < a.n_tiles; j += 256) {
+    for (int j = tid; j < n_tiles; j += 256) {
       const float2 q = pr[j];
       if (q.x != -INFINITY) s += (double)q.y * (double)__builtin_amdgcn_exp2f((q.x - M) * kLog2e);
     }
   s = wave_sum(s);
-  if (lane == 0) sh_s[wv] = s;
+  if (lane == 0) sh.s[wv] = s;
   __syncthreads();
+  M_out = M;
+  S_out = sh.s[0] + sh.s[1] + sh.s[2] + sh.s[3];
+  z_out = sh.z[0] + sh.z[1] + sh.z[2] + sh.z[3];
+}
+
+__global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
+  __shared__ RowStatsSmem sh;
+  const int t = blockIdx.x, tid = threadIdx.x;
+  if (t >= a.T) {
+    if (tid == 0) a.rs[t] = RowScale{-INFINITY, 1.f, 0.f, -1};
+    return;
+  }
+  const int act = a.tok.actions[t];
+  const bool ok = act >= 0 && (int64_t)act < a.tok.V;
+  float M;
+  double S, za;
+  lm_row_stats(a.part + (int64_t)t * a.n_tiles, a.n_tiles, a.h + (int64_t)t * a.H, a.WT, ok ? act : -1, a.H, sh, M,
+               S, za);
   if (tid == 0) {
-    const double S = sh_s[0] + sh_s[1] + sh_s[2] + sh_s[3];
-    const double za = sh_z[0] + sh_z[1] + sh_z[2] + sh_z[3];
     const TokenIn in = token_load(a.tok, t);
     a.rs[t] = token_finish(a.tok, t, in, row_lse((double)M, S), za);
   }
+}
+
+// ---- a vocabulary shard's per-token record (the first call of the sharded fused path) --
+struct RecordArgs {
+  const float2* part;
+  const uint16_t* h;       // [T, H]
+  const uint16_t* WT;      // [V_shard, H]
+  const int32_t* actions;  // global ids
+  grpo_vocab_stats* stats; // [T]
+  int64_t v_begin, V;      // the shard's first global column and width
+  int T, H, n_tiles;
+};
+
+__global__ __launch_bounds__(256) void k_lm_record(const RecordArgs a) {
+  __shared__ RowStatsSmem sh;
+  const int t = blockIdx.x;
+  const int64_t al = (int64_t)a.actions[t] - a.v_begin;
+  const bool own = al >= 0 && al < a.V;
+  float M;
+  double S, za;
+  lm_row_stats(a.part + (int64_t)t * a.n_tiles, a.n_tiles, a.h + (int64_t)t * a.H, a.WT, own ? (int)al : -1, a.H, sh,
+               M, S, za);
+  if (threadIdx.x == 0) {
+    grpo_vocab_stats r;
+    r.m = M;
+    r.s = S;
+    r.z_a = own ? za : -INFINITY;
+    a.stats[t] = r;
+  }
+}
+
+// ---- the sharded fused path's row scales: every shard's records merged, token epilogue, one thread per row
+struct ShardScaleArgs {
+  TokenArgs tok;                  // tok.V: the whole vocabulary
+  const grpo_vocab_stats* stats;  // [n_shards][T]
+  RowScale* rs;                   // [Tp]; rows >= T get the zero scale; act is the column within the shard
+  int64_t v_begin, V;             // the shard's first global column and width
+  int T, Tp, n_shards;
+};
+
+__global__ __launch_bounds__(256) void k_lm_shard_scale(const ShardScaleArgs a) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= a.Tp) return;
+  if (t >= a.T) {
+    a.rs[t] = RowScale{-INFINITY, 1.f, 0.f, -1};
+    return;
+  }
+  double lse, za;
+  merge_vocab_stats(a.stats, a.n_shards, a.T, t, lse, za);
+  const TokenIn in = token_load(a.tok, t);
+  RowScale rs = token_finish(a.tok, t, in, lse, za);
+  const int64_t al = rs.act >= 0 ? (int64_t)rs.act - a.v_begin : -1;
+  rs.act = (al >= 0 && al < a.V) ? (int)al : -1;
+  a.rs[t] = rs;
 }
 
 // ---- pass 2a: recompute z_c, form D_c = g (softmax - onehot), store D_c and D_c^T --
@@ -464,6 +531,97 @@ static dim3 gemm_grid(int64_t M, int64_t N) {
   return dim3((unsigned)((tiles + 7) / 8 * 8));
 }
 
+// W^T [V, H] from W [H, V], and (when hT is set) h^T [H, Tp] with zero columns T..Tp.
+static void lm_transpose(const uint16_t* W16, const uint16_t* h16, int64_t T, int64_t H, int64_t V, int Tp,
+                         uint16_t* WT, uint16_t* hT, hipStream_t s) {
+  hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((V + 63) / 64), (unsigned)((H + 63) / 64)), dim3(256), 0, s,
+                     W16, V, (int)H, (int)V, WT, H, (int)H);
+  if (hT)
+    hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((H + 63) / 64), (unsigned)((Tp + 63) / 64)), dim3(256), 0,
+                       s, h16, H, (int)T, (int)H, hT, (int64_t)Tp, Tp);
+}
+
+static void lm_pass1(const uint16_t* h16, const uint16_t* WT, int64_t T, int64_t H, int64_t V, float2* part,
+                     int n_tiles, hipStream_t s) {
+  PartialArgs pa;
+  pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
+  pa.part = part;
+  pa.n_tiles = n_tiles;
+  hipLaunchKernelGGL(k_lm_partial, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
+}
+
+// Pass 2 over the vocabulary chunks of W [H, V] (a whole LM head or one shard's columns), given every row's
+// scale in rs.  dhidden: bf16 [T, H] through the fp32 accumulator acc [Tp, H]; or, when dh16 is null, the
+// fp32 sum over this W's chunks written straight into acc (a shard's partial dhidden, [T, H]).
+struct Pass2 {
+  const uint16_t *h16, *W16, *WT, *hT;
+  const RowScale* rs;
+  uint16_t *D, *DT;
+  float* acc;
+  uint16_t* dh16;  // null: fp32 partial in acc
+  float* dw;       // [H, V]
+  int64_t T, H, V;
+  int Tp, C, accumulate_dw;
+};
+
+static void lm_pass2(const Pass2& q, hipStream_t s) {
+  // the backward products take the chunks in pairs (D holds two side by side, D^T one above the other), which
+  // halves the passes over dhidden's fp32 accumulator and gives one dW launch per pair
+  const int C = q.C;
+  const int n_chunks = (int)((q.V + C - 1) / C);
+  const int ldD = n_chunks > 1 ? 2 * C : C;
+  for (int c = 0; c < n_chunks; ++c) {
+    const int c0 = c * C;
+    const int Cw = (int)((q.V - c0) < C ? (q.V - c0) : C);
+    DlogitsArgs da;
+    da.g = GemmArgs{q.h16, q.WT + (int64_t)c0 * q.H, q.H, q.H, (int)q.T, Cw, (int)q.H};
+    da.rs = q.rs;
+    da.D = q.D + (c & 1) * C;
+    da.DT = q.DT + (int64_t)(c & 1) * C * q.Tp;
+    da.c0 = c0;
+    da.C = ldD;
+    da.Tp = q.Tp;
+    hipLaunchKernelGGL(k_lm_dlogits, gemm_grid(q.Tp, Cw), dim3(LmCfg::NT), 0, s, da);
+    if ((c & 1) || c == n_chunks - 1) {
+      const int p0 = c & ~1;                  // first chunk of the pair
+      const int width = (c & 1) ? C + Cw : Cw;  // the pair's vocabulary columns
+      DhDwArgs ba;
+      ba.dh.g = GemmArgs{q.D, q.W16 + (int64_t)p0 * C, ldD, q.V, (int)q.T, (int)q.H, width};
+      ba.dh.acc = q.acc;
+      ba.dh.dh = q.dh16;
+      ba.dh.first = (p0 == 0);
+      ba.dh.last = q.dh16 != nullptr && c == n_chunks - 1;
+      ba.dw.g = GemmArgs{q.hT, q.DT, q.Tp, q.Tp, (int)q.H, width, q.Tp};
+      ba.dw.dw = q.dw;
+      ba.dw.V = q.V;
+      ba.dw.c0 = p0 * C;
+      ba.dw.accumulate = q.accumulate_dw;
+      ba.dw_blocks = (int)gemm_grid(q.H, width).x;
+      hipLaunchKernelGGL(k_lm_dh_dw, dim3((unsigned)ba.dw_blocks + gemm_grid(q.T, q.H).x), dim3(LmCfg::NT), 0, s, ba);
+    }
+  }
+}
+
+// The shard statistics call needs W^T of the shard and the pass-1 partials only.
+struct LmStatsWs {
+  size_t wt, part, total;
+};
+static LmStatsWs lm_stats_ws_layout(int64_t T, int64_t H, int64_t V) {
+  LmStatsWs l;
+  size_t o = 0;
+  l.wt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(V * H));
+  l.part = o; o = align_up(o + sizeof(float2) * (size_t)(T * ((V + TILE - 1) / TILE)));
+  l.total = o;
+  return l;
+}
+
+static int check_fused_shapes(int64_t T, int64_t H, int64_t V) {
+  if (T < 0 || T >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
+  if (H < 64 || H % 64 != 0 || H >= (1 << 30)) return GRPO_ERR_SHAPE;
+  if (V < 8 || V % 8 != 0 || V >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
+  return GRPO_OK;
+}
+
 }  // namespace grpo
 
 using namespace grpo;
@@ -499,7 +657,6 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   uint16_t* D = reinterpret_cast<uint16_t*>(w + L.d);
   uint16_t* DT = reinterpret_cast<uint16_t*>(w + L.dt);
   float* acc = reinterpret_cast<float*>(w + L.acc);
-  const int C = vocab_chunk;
   const int Tp = (int)L.Tp;
 
   if (launch_segments(seg, T, V, actions, adv, p, w, L.loss, aux, s) != hipSuccess) return GRPO_ERR_HIP;
@@ -508,21 +665,12 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
     return launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
   }
-  // W^T [V, H] and h^T [H, Tp] (zero columns T..Tp)
-  hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((V + 63) / 64), (unsigned)((H + 63) / 64)), dim3(256), 0, s,
-                     W16, V, (int)H, (int)V, WT, H, (int)H);
-  hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((H + 63) / 64), (unsigned)((Tp + 63) / 64)), dim3(256), 0, s,
-                     h16, H, (int)T, (int)H, hT, (int64_t)Tp, Tp);
+  lm_transpose(W16, h16, T, H, V, Tp, WT, hT, s);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
 
   const bool timed = aux && aux->hot_begin && aux->hot_end;
   if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
-  // pass 1
-  PartialArgs pa;
-  pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
-  pa.part = part;
-  pa.n_tiles = L.n_tiles;
-  hipLaunchKernelGGL(k_lm_partial, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
+  lm_pass1(h16, WT, T, H, V, part, L.n_tiles, s);
   // combine
   CombineArgs ca;
   ca.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
@@ -535,41 +683,101 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   ca.n_tiles = L.n_tiles;
   hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)Tp), dim3(256), 0, s, ca);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
-  // pass 2, chunk by chunk; the backward products take the chunks in pairs (D holds two side by side, D^T one
-  // above the other), which halves the passes over dhidden's fp32 accumulator and gives one dW launch per pair
-  const int n_chunks = (int)((V + C - 1) / C);
-  const int ldD = n_chunks > 1 ? 2 * C : C;
-  for (int c = 0; c < n_chunks; ++c) {
-    const int c0 = c * C;
-    const int Cw = (int)((V - c0) < C ? (V - c0) : C);
-    DlogitsArgs da;
-    da.g = GemmArgs{h16, WT + (int64_t)c0 * H, H, H, (int)T, Cw, (int)H};
-    da.rs = rs;
-    da.D = D + (c & 1) * C;
-    da.DT = DT + (int64_t)(c & 1) * C * Tp;
-    da.c0 = c0;
-    da.C = ldD;
-    da.Tp = Tp;
-    hipLaunchKernelGGL(k_lm_dlogits, gemm_grid(Tp, Cw), dim3(LmCfg::NT), 0, s, da);
-    if ((c & 1) || c == n_chunks - 1) {
-      const int p0 = c & ~1;                  // first chunk of the pair
-      const int width = (c & 1) ? C + Cw : Cw;  // the pair's vocabulary columns
-      DhDwArgs ba;
-      ba.dh.g = GemmArgs{D, W16 + (int64_t)p0 * C, ldD, V, (int)T, (int)H, width};
-      ba.dh.acc = acc;
-      ba.dh.dh = static_cast<uint16_t*>(dhidden);
-      ba.dh.first = (p0 == 0);
-      ba.dh.last = (c == n_chunks - 1);
-      ba.dw.g = GemmArgs{hT, DT, Tp, Tp, (int)H, width, Tp};
-      ba.dw.dw = dw_lm;
-      ba.dw.V = V;
-      ba.dw.c0 = p0 * C;
-      ba.dw.accumulate = accumulate_dw;
-      ba.dw_blocks = (int)gemm_grid(H, width).x;
-      hipLaunchKernelGGL(k_lm_dh_dw, dim3((unsigned)ba.dw_blocks + gemm_grid(T, H).x), dim3(LmCfg::NT), 0, s, ba);
-    }
+  lm_pass2(Pass2{h16, W16, WT, hT, rs, D, DT, acc, static_cast<uint16_t*>(dhidden), dw_lm, T, H, V, Tp,
+                 vocab_chunk, accumulate_dw},
+           s);
+  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
+  if (launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;
+  return GRPO_OK;
+}
+
+extern "C" size_t fused_lmhead_vocab_shard_stats_workspace_bytes(int64_t T, int64_t H, int64_t V_shard) {
+  if (T < 0 || H < 1 || V_shard < 1) return 0;
+  return lm_stats_ws_layout(T, H, V_shard).total;
+}
+
+extern "C" int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_shard, int64_t T, int64_t H,
+                                              int64_t V_shard, int64_t v_begin, const int32_t* actions,
+                                              grpo_vocab_stats* stats, void* ws, size_t ws_bytes, hipStream_t s) {
+  int st = check_fused_shapes(T, H, V_shard);
+  if (st != GRPO_OK) return st;
+  if (v_begin < 0 || v_begin + V_shard >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
+  if (!w_shard || (T > 0 && (!hidden || !actions || !stats))) return GRPO_ERR_ARG;
+  if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(stats, 8)) return GRPO_ERR_ALIGN;
+  const LmStatsWs L = lm_stats_ws_layout(T, H, V_shard);
+  if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
+  if (T == 0) return GRPO_OK;
+  char* w = static_cast<char*>(ws);
+  const uint16_t* h16 = static_cast<const uint16_t*>(hidden);
+  uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);
+  float2* part = reinterpret_cast<float2*>(w + L.part);
+  const int n_tiles = (int)((V_shard + TILE - 1) / TILE);
+  lm_transpose(static_cast<const uint16_t*>(w_shard), h16, T, H, V_shard, 0, WT, nullptr, s);
+  lm_pass1(h16, WT, T, H, V_shard, part, n_tiles, s);
+  RecordArgs ra{part, h16, WT, actions, stats, v_begin, V_shard, (int)T, (int)H, n_tiles};
+  hipLaunchKernelGGL(k_lm_record, dim3((unsigned)T), dim3(256), 0, s, ra);
+  return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+}
+
+extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_shard, int64_t T, int64_t H,
+                                             int64_t V_shard, int64_t v_begin, int64_t V_total, int32_t vocab_chunk,
+                                             const grpo_vocab_stats* stats, int32_t n_shards, const int32_t* actions,
+                                             const float* behave_logp, const float* prox_logp, const float* adv,
+                                             const grpo_segments* seg, const grpo_loss_params* p, double* loss_out,
+                                             float* dhidden_partial, float* dw_shard, int32_t accumulate_dw,
+                                             grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s) {
+  int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
+  if (st != GRPO_OK) return st;
+  if (!w_shard || !dw_shard || (T > 0 && (!hidden || !dhidden_partial || !stats))) return GRPO_ERR_ARG;
+  st = check_fused_shapes(T, H, V_shard);
+  if (st != GRPO_OK) return st;
+  if (vocab_chunk < 256 || vocab_chunk % 256 != 0) return GRPO_ERR_SHAPE;
+  if (v_begin < 0 || V_total >= ((int64_t)1 << 31) || v_begin + V_shard > V_total || n_shards < 1 ||
+      n_shards > 65536)
+    return GRPO_ERR_SHAPE;
+  if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(dhidden_partial, 16) || !aligned(dw_shard, 16) ||
+      !aligned(stats, 8))
+    return GRPO_ERR_ALIGN;
+  const LmWs L = lm_ws_layout(T, H, V_shard, vocab_chunk, seg->n_traj);
+  if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
+  char* w = static_cast<char*>(ws);
+  const uint16_t* h16 = static_cast<const uint16_t*>(hidden);
+  const uint16_t* W16 = static_cast<const uint16_t*>(w_shard);
+  uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);
+  uint16_t* hT = reinterpret_cast<uint16_t*>(w + L.ht);
+  RowScale* rs = reinterpret_cast<RowScale*>(w + L.rs);
+  uint16_t* D = reinterpret_cast<uint16_t*>(w + L.d);
+  uint16_t* DT = reinterpret_cast<uint16_t*>(w + L.dt);
+  const int Tp = (int)L.Tp;
+
+  if (launch_segments(seg, T, V_total, actions, adv, p, w, L.loss, aux, s) != hipSuccess) return GRPO_ERR_HIP;
+  if (T == 0) {
+    if (!accumulate_dw) hipLaunchKernelGGL(k_fill_f32, dim3(1024), dim3(256), 0, s, dw_shard, H * V_shard, 0.f);
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+    return launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
   }
+  lm_transpose(W16, h16, T, H, V_shard, Tp, WT, hT, s);
+  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  const bool timed = aux && aux->hot_begin && aux->hot_end;
+  if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
+  ShardScaleArgs sa;
+  sa.tok = make_token_args(V_total, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
+  sa.stats = stats;
+  sa.rs = rs;
+  sa.v_begin = v_begin;
+  sa.V = V_shard;
+  sa.T = (int)T;
+  sa.Tp = Tp;
+  sa.n_shards = n_shards;
+  hipLaunchKernelGGL(k_lm_shard_scale, dim3((unsigned)((Tp + 255) / 256)), dim3(256), 0, s, sa);
+  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  lm_pass2(Pass2{h16, W16, WT, hT, rs, D, DT, dhidden_partial, nullptr, dw_shard, T, H, V_shard, Tp, vocab_chunk,
+                 accumulate_dw},
+           s);
+  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   if (launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;
   return GRPO_OK;

@@ -95,9 +95,9 @@ __device__ __forceinline__ void row_out(const LogpArgs& a, int t, double M, doub
                                         bool act_ok) {
   if (a.stats) {
     grpo_vocab_stats r;
-    r.m = (float)M;  // the maximum of stored values: exact
-    r.z_a = act_ok ? (float)za : -INFINITY;
+    r.m = M;  // the maximum of stored values: exact
     r.s = S;
+    r.z_a = act_ok ? za : -INFINITY;
     a.stats[t] = r;
     if (a.flags && (isnan(M) || isnan(S) || M == INFINITY)) atomicOr(a.flags, GRPO_FLAG_NONFINITE);
     return;
@@ -231,7 +231,7 @@ extern "C" int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t
   if (T > 0 && (!logits || !actions || !stats)) return GRPO_ERR_ARG;
   if (dt != GRPO_F32 && dt != GRPO_BF16) return GRPO_ERR_DTYPE;
   const int esz = (dt == GRPO_BF16) ? 2 : 4;
-  if (!aligned(logits, esz) || !aligned(stats, 16)) return GRPO_ERR_ALIGN;
+  if (!aligned(logits, esz) || !aligned(stats, 8)) return GRPO_ERR_ALIGN;
   if (error_flags) hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, error_flags);
   if (T > 0) {
     LogpArgs a{logits, ld, V_shard, v_begin, (int)T, actions, nullptr, nullptr, error_flags, stats};

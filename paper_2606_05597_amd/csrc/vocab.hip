@@ -4,8 +4,8 @@
 //
 //   1. grpo_vocab_shard_stats (logp.hip): each shard reduces its columns of
 //      every row to (max m, sum s of e^(z - m), the action logit z_a if the
-//      action is one of its columns), 16 bytes per token.
-//   2. the caller gathers every shard's records on every device (T x 16 bytes
+//      action is one of its columns), 24 bytes per token.
+//   2. the caller gathers every shard's records on every device (T x 24 bytes
 //      per shard);
 //   3. grpo_loss_fwd_bwd_vocab_shard (here): per row, the records are merged in
 //      shard order into the row's log-sum-exp M + log sum_g s_g e^(m_g - M) and
@@ -36,29 +36,11 @@ struct ShardArgs {
   TokenArgs tok;                  // tok.V: the whole vocabulary
 };
 
-// The row's log-sum-exp and action logit from every shard's record, merged in
-// shard order (so every shard gets the same bits).  A NaN maximum propagates.
-__device__ inline void merge_stats(const ShardArgs& a, int t, double& lse, double& za) {
-  float M = -INFINITY, z = -INFINITY;
-  for (int g = 0; g < a.n_shards; ++g) {
-    const grpo_vocab_stats r = a.stats[(int64_t)g * a.T + t];
-    if (r.m > M || isnan(r.m)) M = r.m;
-    z = fmaxf(z, r.z_a);
-  }
-  double S = 0.0;
-  for (int g = 0; g < a.n_shards; ++g) {
-    const grpo_vocab_stats r = a.stats[(int64_t)g * a.T + t];
-    if (r.m != -INFINITY) S += r.s * exp((double)r.m - (double)M);
-  }
-  lse = row_lse((double)M, S);
-  za = (double)z;
-}
-
 // Thread 0: merge, token epilogue, the action's column within this shard (-1 if
 // another shard holds it).
 __device__ inline void shard_row_head(const ShardArgs& a, int t, RowScale& rs, int& act_local) {
   double lse, za;
-  merge_stats(a, t, lse, za);
+  merge_vocab_stats(a.stats, a.n_shards, a.T, t, lse, za);
   const TokenIn in = token_load(a.tok, t);
   rs = token_finish(a.tok, t, in, lse, za);
   const int64_t al = rs.act >= 0 ? (int64_t)rs.act - a.v_begin : -1;
@@ -155,7 +137,7 @@ extern "C" int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, 
     return GRPO_ERR_SHAPE;
   if (T > 0 && (!logits || !stats)) return GRPO_ERR_ARG;
   const size_t esz = (dt == GRPO_BF16) ? 2 : 4;
-  if (!aligned(logits, esz) || !aligned(dlogits, esz) || !aligned(stats, 16)) return GRPO_ERR_ALIGN;
+  if (!aligned(logits, esz) || !aligned(dlogits, esz) || !aligned(stats, 8)) return GRPO_ERR_ALIGN;
   const LossWs L = loss_ws_layout(T, seg->n_traj);
   if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;

@@ -36,6 +36,8 @@ def test_header_declares_the_boundary():
                                            "grpo_loss_fwd_bwd",
                                            "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_token_logp",
                                            "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
+                                           "fused_lmhead_vocab_shard_stats_workspace_bytes",
+                                           "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
                                            "grpo_status_str"])
 
 
@@ -191,7 +193,7 @@ def call_shard_stats(lib, *, logits=D, dt=_lib.GRPO_BF16, T=8, V=64, ld=64, v_be
     (dict(v_begin=(1 << 31) - 64), _lib.GRPO_ERR_SHAPE),  # the shard's last column past 2^31
     (dict(dt=3), _lib.GRPO_ERR_DTYPE),
     (dict(logits=ctypes.c_void_p(0x100001)), _lib.GRPO_ERR_ALIGN),
-    (dict(stats=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),  # records are 16-byte aligned
+    (dict(stats=ctypes.c_void_p(0x100004)), _lib.GRPO_ERR_ALIGN),  # records are 8-byte aligned
 ])
 def test_shard_stats_rejects_bad_arguments(lib, kw, status):
     assert call_shard_stats(lib, **kw) == status
@@ -225,6 +227,65 @@ def call_shard_loss(lib, *, T=8, V=64, ld=64, v_begin=0, V_total=128, stats=D, n
 ])
 def test_shard_loss_rejects_bad_arguments(lib, kw, status):
     assert call_shard_loss(lib, **kw) == status
+
+
+def call_fused_shard_stats(lib, *, T=8, H=64, V=512, v_begin=0, hidden=D, w=D, stats=D, ws=D, ws_bytes=1 << 30):
+    return lib.fused_lmhead_vocab_shard_stats(hidden, w, T, H, V, v_begin, D, stats, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=96), _lib.GRPO_ERR_SHAPE),
+    (dict(V=500), _lib.GRPO_ERR_SHAPE),
+    (dict(T=-1), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=-8), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=(1 << 31) - 512), _lib.GRPO_ERR_SHAPE),
+    (dict(w=None), _lib.GRPO_ERR_ARG),
+    (dict(hidden=None), _lib.GRPO_ERR_ARG),
+    (dict(stats=None), _lib.GRPO_ERR_ARG),
+    (dict(stats=ctypes.c_void_p(0x100004)), _lib.GRPO_ERR_ALIGN),
+    (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
+])
+def test_fused_shard_stats_rejects_bad_arguments(lib, kw, status):
+    assert call_fused_shard_stats(lib, **kw) == status
+
+
+def test_fused_shard_stats_workspace(lib):
+    T, H, Vs = 65536, 3584, 18992
+    n = lib.fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs)
+    assert n >= 2 * Vs * H + 8 * T * ((Vs + 255) // 256) and n % 256 == 0
+    assert lib.fused_lmhead_vocab_shard_stats_workspace_bytes(-1, H, Vs) == 0
+
+
+def call_fused_shard(lib, *, T=8, H=64, V=512, v_begin=0, V_total=1024, chunk=256, stats=D, n_shards=2, hidden=D,
+                     w=D, dhp=D, dw=D, ws=D, ws_bytes=1 << 40):
+    seg = _lib.Segments()
+    seg.n_traj, seg.group_size, seg.n_steps = 4, 4, 4
+    seg.step_tok_off, seg.traj_step_off = D, D
+    p = _lib.LossParams()
+    p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale = 1, 10.0, 0.2, 0.2, 0.0, 1.0
+    return lib.fused_lmhead_grpo_vocab_shard(hidden, w, T, H, V, v_begin, V_total, chunk, stats, n_shards, D, D, None,
+                                             D, ctypes.byref(seg), ctypes.byref(p), D, dhp, dw, 0, None, ws, ws_bytes,
+                                             None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=96), _lib.GRPO_ERR_SHAPE),
+    (dict(V=500), _lib.GRPO_ERR_SHAPE),
+    (dict(chunk=300), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=-8), _lib.GRPO_ERR_SHAPE),
+    (dict(v_begin=520), _lib.GRPO_ERR_SHAPE),      # v_begin + V_shard > V_total
+    (dict(V_total=1 << 31), _lib.GRPO_ERR_SHAPE),
+    (dict(n_shards=0), _lib.GRPO_ERR_SHAPE),
+    (dict(w=None), _lib.GRPO_ERR_ARG),
+    (dict(dw=None), _lib.GRPO_ERR_ARG),
+    (dict(dhp=None), _lib.GRPO_ERR_ARG),
+    (dict(stats=None), _lib.GRPO_ERR_ARG),
+    (dict(dhp=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),
+    (dict(stats=ctypes.c_void_p(0x100004)), _lib.GRPO_ERR_ALIGN),
+    (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
+])
+def test_fused_shard_rejects_bad_arguments(lib, kw, status):
+    assert call_fused_shard(lib, **kw) == status
 
 
 def test_advantages_ex_rejects_bad_arguments(lib):

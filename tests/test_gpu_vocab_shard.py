@@ -2,7 +2,7 @@
 oracle.
 
 One GPU plays every shard in turn: the logits of a batch are split into column ranges, each range's records are
-computed into one [n_shards, T, 16] tensor (what gathering them across devices would give), and each range's
+computed into one [n_shards, T] record tensor (what gathering them across devices would give), and each range's
 loss pass writes its columns of dlogits.  The concatenated dlogits, the loss and the per-token outputs are held
 to the gates of tests/gpu_parity.py against the oracle's whole-row results; the records against the oracle's
 per-shard statistics (max and action logit exact, the sum relative 5e-6: fp32 partial sums over the shard's
@@ -227,7 +227,7 @@ def test_empty_batch():
     logits = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
     act = torch.empty(0, dtype=torch.int32, device="cuda")
     stats = grpo.grpo_vocab_shard_stats(logits, act, 0)
-    assert stats.shape == (0, 16)
+    assert stats.shape == (0, grpo.VOCAB_STATS_BYTES)
     loss, dl = grpo.grpo_loss_fwd_bwd_vocab_shard(logits, stats[None], 0, 64, act, torch.empty(0, device="cuda"),
                                                   torch.zeros(N, device="cuda"), sto, tso, 4)
     torch.cuda.synchronize()
