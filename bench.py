@@ -219,7 +219,7 @@ def bench_vocab_shard(b: dict, steps: int, n_shards: int = 8, warmup: int = 2) -
             "roofline_rows": roof(alg_rows, rows_ms, "k_shard_rows_vec<bf16, 512, 5>")}
 
 
-def bench_fused(steps: int, warmup: int = 1) -> dict:
+def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0) -> dict:
     """Times fused_lmhead_grpo on the fused workload; the hot region is pass 1 through pass 2."""
     import torch
 
@@ -263,14 +263,87 @@ def bench_fused(steps: int, warmup: int = 1) -> dict:
     hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(steps)) / steps
     alg = 6.0 * T * H * V
     achieved = alg / (hot_ms * 1e-3) / 1e12
+    out = {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
+           "workload": f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], chunks of {cfg.vocab_chunk}, "
+                       f"{cfg.n_groups} groups x G={cfg.G}",
+           "loss": float(loss.item()),
+           "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "hot_ms": hot_ms,
+                        "algorithmic_flop_per_launch": alg,
+                        "executed_frac": (8.0 * T * H * V) / (hot_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}}
+    if shard_steps > 0:
+        del dh, dw, ws
+        torch.cuda.empty_cache()
+        out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps)
+    return out
+
+
+def bench_fused_shard(b: dict, adv, sto, tso, steps: int, n_shards: int = 8, warmup: int = 1) -> dict:
+    """One device's share of the vocabulary-parallel fused LM head on the fused workload: W's columns split n_shards
+    ways, the first shard's statistics call and backward call timed, every shard's records gathered beforehand."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    cfg, st = b["cfg"], b["structure"]
+    T, H, V = st.T, b["H"], b["V"]
+    N = len(st.rewards)
+    Vs = V // n_shards
+    chunk = (Vs + 511) // 512 * 256  # the shard's columns in one pair of chunks
+    dev = b["hidden"].device
+    stats = torch.empty((n_shards, T, grpo.VOCAB_STATS_BYTES), dtype=torch.uint8, device=dev)
+    for g in range(n_shards):
+        grpo.fused_lmhead_vocab_shard_stats(b["hidden"], b["W"][:, g * Vs:(g + 1) * Vs].contiguous(), b["actions"],
+                                            g * Vs, stats=stats[g])
+    w = b["W"][:, :Vs].contiguous()
+    dhp = torch.empty((T, H), dtype=torch.float32, device=dev)
+    dws = torch.empty((H, Vs), dtype=torch.float32, device=dev)
+    ws1 = torch.empty(grpo._lib.load().fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs), dtype=torch.uint8,
+                      device=dev)
+    ws2 = torch.empty(grpo.fused_lmhead_workspace_bytes(T, H, Vs, chunk, N), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    eb = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e in [x for pair in es + eb for x in pair]:
+        e.record(stream)
+    torch.cuda.synchronize()
+
+    def step(i=None):
+        if i is not None:
+            es[i][0].record(stream)
+        grpo.fused_lmhead_vocab_shard_stats(b["hidden"], w, b["actions"], 0, stats=stats[0], workspace=ws1)
+        if i is not None:
+            es[i][1].record(stream)
+            eb[i][0].record(stream)
+        grpo.fused_lmhead_grpo_vocab_shard(b["hidden"], w, stats, 0, V, b["actions"], b["behave"], adv, sto, tso,
+                                           cfg.G, vocab_chunk=chunk, norm=grpo.GRPO_NORM_CONST_K, k=cfg.k,
+                                           dual_clip_c=3.0, dhidden_partial=dhp, dw_shard=dws, workspace=ws2,
+                                           loss_out=loss)
+        if i is not None:
+            eb[i][1].record(stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    stats_ms = sum(a.elapsed_time(c) for a, c in es) / steps
+    bwd_ms = sum(a.elapsed_time(c) for a, c in eb) / steps
+    alg = 6.0 * T * H * Vs
+    achieved = alg / ((stats_ms + bwd_ms) * 1e-3) / 1e12
     return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
-            "workload": f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], chunks of {cfg.vocab_chunk}, "
-                        f"{cfg.n_groups} groups x G={cfg.G}",
-            "loss": float(loss.item()),
+            "workload": f"one device's share of the fused LM head with W's {V} columns split {n_shards} ways: "
+                        f"hidden bf16 [{T}, {H}], W shard bf16 [{H}, {Vs}], chunks of {chunk}; statistics call + "
+                        f"backward call (records of all {n_shards} shards gathered beforehand)",
+            "loss": float(loss.item()), "stats_ms": stats_ms, "backward_ms": bwd_ms,
             "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "hot_ms": hot_ms,
+                         "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
                          "algorithmic_flop_per_launch": alg,
-                         "executed_frac": (8.0 * T * H * V) / (hot_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}}
+                         "executed_frac": (8.0 * T * H * Vs) / ((stats_ms + bwd_ms) * 1e-3) / 1e12
+                         / MFMA_BF16_PEAK_TFLOPS}}
 
 
 def main():
@@ -283,7 +356,8 @@ def main():
         copy_calibration()
         return
     if args.skip_logits:
-        print(json.dumps({"fused_lmhead": bench_fused(max(1, args.fused_steps))}), flush=True)
+        print(json.dumps({"fused_lmhead": bench_fused(max(1, args.fused_steps), shard_steps=args.shard_steps and 3)}),
+              flush=True)
         return
     import numpy as np
     import torch
@@ -366,7 +440,7 @@ def main():
     if args.fused_steps > 0:
         del b
         torch.cuda.empty_cache()
-        out["fused_lmhead"] = bench_fused(args.fused_steps)
+        out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3)
     print(json.dumps(out), flush=True)
 
 
