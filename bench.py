@@ -42,6 +42,9 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_rows_pipe_v152k_traffic.md")
 KERNEL_SOURCES = ["paper_2606_05597_amd/csrc/loss.hip", "paper_2606_05597_amd/csrc/device.h"]
+FUSED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "lmhead_fused_65536x3584x151936_traffic.md")
+FUSED_SOURCES = ["paper_2606_05597_amd/csrc/lmhead.hip", "paper_2606_05597_amd/csrc/gemm.h",
+                 "paper_2606_05597_amd/csrc/device.h"]
 
 
 def kernel_source_hash() -> str:
@@ -50,6 +53,24 @@ def kernel_source_hash() -> str:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def fused_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in FUSED_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_fused_traffic():
+    """HBM bytes per fused call from the committed counter summary, if it is current."""
+    if not os.path.exists(FUSED_TRAFFIC_FILE):
+        return None
+    kv = dict(re.findall(r"^- (\w+): (\S+)", open(FUSED_TRAFFIC_FILE).read(), re.M))
+    if kv.get("kernel_source_sha256") != fused_source_hash():
+        return None
+    return float(kv["traffic_bytes_per_call"])
 
 
 def measured_traffic(T: int):
@@ -268,7 +289,7 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0) -> dict:
                        f"{cfg.n_groups} groups x G={cfg.G}",
            "loss": float(loss.item()),
            "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                        "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None, "hot_ms": hot_ms,
+                        "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": measured_fused_traffic(), "hot_ms": hot_ms,
                         "algorithmic_flop_per_launch": alg,
                         "executed_frac": (8.0 * T * H * V) / (hot_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}}
     if shard_steps > 0:
