@@ -405,6 +405,7 @@ static const RowKernel kPipe[] = {
     k_rows_pipe<22, 9>,  k_rows_pipe<23, 9>,
 };  // from 15 vectors on, 14 in registers (what fits in 128 VGPRs) and the rest in LDS
 constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 14 register vectors and 9 LDS vectors per thread
+constexpr int64_t kPipeMaxT = (int64_t)1 << 30;  // t + gridDim.x stays far below 2^31
 
 struct Launch {
   RowKernel k;
@@ -419,7 +420,7 @@ static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, c
   if (vec_ok) {
     const int64_t nvec = V / epv;
     const int64_t nv = (nvec + 1023) / 1024;
-    if (dt == GRPO_BF16 && nv >= kPipeMinNV && nv <= kPipeMaxNV) {
+    if (dt == GRPO_BF16 && nv >= kPipeMinNV && nv <= kPipeMaxNV && T <= kPipeMaxT) {
       int dev = 0, n_cu = 0;
       if (hipGetDevice(&dev) != hipSuccess ||
           hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
