@@ -30,7 +30,7 @@ from tests.test_gpu_fused import bits, check_dw, setup, small_cfg
 pytestmark = pytest.mark.gpu
 
 
-def run_shards(b, A32, sto, tso, bounds, chunk, norm, c, gs=1.0, dw_init=None, accumulate=False):
+def run_shards(b, A32, sto, tso, bounds, chunk, norm, c, gs=1.0, dw_init=None, accumulate=False, ngt=0.0):
     """Every shard's two calls on one GPU: (losses, summed dhidden partials fp64, concatenated dW fp64, aux of shard
     0, records)."""
     T = b["structure"].T
@@ -46,8 +46,8 @@ def run_shards(b, A32, sto, tso, bounds, chunk, norm, c, gs=1.0, dw_init=None, a
         dw = None if dw_init is None else dw_init[:, b0:bounds[g + 1]].contiguous()
         loss, dhp, dws_g = grpo.fused_lmhead_grpo_vocab_shard(
             b["hidden"], w, stats, b0, V, b["actions"], b["behave"], A32, sto, tso, b["cfg"].G, vocab_chunk=chunk,
-            norm=gpu_norm(norm), k=b["cfg"].k, dual_clip_c=c, grad_scale=gs, dw_shard=dw, accumulate_dw=accumulate,
-            aux=aux)
+            prox_logp=b["prox"], norm=gpu_norm(norm), k=b["cfg"].k, dual_clip_c=c, grad_scale=gs,
+            n_groups_total=ngt, dw_shard=dw, accumulate_dw=accumulate, aux=aux)
         torch.cuda.synchronize()
         losses.append(loss.item())
         dh_sum += dhp.cpu().numpy().astype(np.float64)
@@ -76,19 +76,20 @@ def check_dh_f32(dh, ref_dh, D, W64, what=""):
     assert np.linalg.norm(err) / np.linalg.norm(ref_dh) <= 5e-3
 
 
-def shard_compare(b, bounds, chunk, norm, c, gs=1.0, accumulate=False):
+def shard_compare(b, bounds, chunk, norm, c, gs=1.0, accumulate=False, ngt=0.0):
     A64, A32, seg, sto, tso = setup(b)
     H, V = b["H"], b["V"]
     dw0 = None
     if accumulate:
         dw0 = torch.randn((H, V), device="cuda", generator=torch.Generator("cuda").manual_seed(9)) * 1e-3
-    losses, dh, dW, aux, stats = run_shards(b, A32, sto, tso, bounds, chunk, norm, c, gs, dw0, accumulate)
+    losses, dh, dW, aux, stats = run_shards(b, A32, sto, tso, bounds, chunk, norm, c, gs, dw0, accumulate, ngt)
     assert len(set(losses)) == 1, losses
     hb, Wb = bits(b["hidden"]), bits(b["W"])
     actions = b["actions"].cpu().numpy()
     check_records(stats, hb, Wb, actions, bounds)
-    ref = fused.fused_loss(hb, Wb, actions, b["behave"].cpu().numpy(), None, A64, seg, b["cfg"].G, norm=norm,
-                           k=b["cfg"].k, dual_clip_c=c, grad_scale=gs)
+    prox = None if b["prox"] is None else b["prox"].cpu().numpy()
+    ref = fused.fused_loss(hb, Wb, actions, b["behave"].cpu().numpy(), prox, A64, seg, b["cfg"].G, norm=norm,
+                           k=b["cfg"].k, dual_clip_c=c, grad_scale=gs, n_groups_total=ngt)
     size = np.abs(ref.rows.token_contrib).sum()
     assert abs(losses[0] - ref.loss) <= LOSS_RTOL * size, (losses[0], ref.loss, size)
     assert np.abs(aux.token_logp.cpu().numpy() - ref.rows.token_logp).max() <= 5e-5
@@ -100,8 +101,8 @@ def shard_compare(b, bounds, chunk, norm, c, gs=1.0, accumulate=False):
     check_dw(dW, ref.dW, fused.as_f64(hb), D, "concatenated dW")
     # the single-device fused path on the same batch: the same fp32 logits, so the same loss to rounding
     loss1, _, _ = grpo.fused_lmhead_grpo(b["hidden"], b["W"], b["actions"], b["behave"], A32, sto, tso, b["cfg"].G,
-                                         vocab_chunk=chunk, norm=gpu_norm(norm), k=b["cfg"].k, dual_clip_c=c,
-                                         grad_scale=gs)
+                                         vocab_chunk=chunk, prox_logp=b["prox"], norm=gpu_norm(norm), k=b["cfg"].k,
+                                         dual_clip_c=c, grad_scale=gs, n_groups_total=ngt)
     torch.cuda.synchronize()
     assert abs(losses[0] - loss1.item()) <= 1e-6 * size, (losses[0], loss1.item())
     return losses[0], dh, dW
@@ -118,6 +119,15 @@ def test_fused_shard_small(bounds, c):
 def test_fused_shard_multichunk_accumulate():
     b = make_fused_batch(small_cfg(4, 8, 256, 5000, seed=22, tok_mean=6.0, steps=(2, 9)), "cuda")
     shard_compare(b, [0, 1600, 3200, 5000], 512, oracle.NORM_TRAJ_STEPS, 3.0, gs=0.5, accumulate=True)
+
+
+def test_fused_shard_decoupled_and_global_groups():
+    # a proximal policy distinct from the behaviour one (decoupled ratios), and the normaliser's group count
+    # overridden as a data-parallel shard of a 5x larger batch would pass it
+    b = make_fused_batch(small_cfg(2, 4, 64, 1000, seed=25), "cuda")
+    gen = torch.Generator("cuda").manual_seed(26)
+    b["prox"] = b["behave"] + 0.05 * torch.randn(b["behave"].shape, device="cuda", generator=gen)
+    shard_compare(b, [0, 504, 1000], 256, oracle.NORM_TRAJ_STEPS, 3.0, ngt=10.0)
 
 
 def test_fused_shard_agrees_with_single_device():

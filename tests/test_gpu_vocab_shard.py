@@ -41,7 +41,7 @@ def shard_stats(lg, actions, bounds):
     return stats
 
 
-def run_sharded(b, A32, bounds, *, norm, k, c=0.0, grad_scale=1.0, dlogits=True, aux=True, actions=None):
+def run_sharded(b, A32, bounds, *, norm, k, c=0.0, grad_scale=1.0, dlogits=True, aux=True, actions=None, ngt=0.0):
     """Every shard's two calls on one GPU.  Returns (per-shard losses, dlogits or None, per-shard aux, records)."""
     dev = device_batch(b)
     N = len(b["structure"].rewards)
@@ -56,7 +56,7 @@ def run_sharded(b, A32, bounds, *, norm, k, c=0.0, grad_scale=1.0, dlogits=True,
         loss, _ = grpo.grpo_loss_fwd_bwd_vocab_shard(
             lg[:, b0:b1], stats, b0, b["V"], act, b["behave"], A32, dev["step_tok_off"], dev["traj_step_off"],
             b["cfg"].G, prox_logp=b["prox"], norm=norm, k=k, dual_clip_c=c, grad_scale=grad_scale,
-            dlogits=None if dl is None else dl[:, b0:b1], aux=a)
+            n_groups_total=ngt, dlogits=None if dl is None else dl[:, b0:b1], aux=a)
         losses.append(loss.item())
         auxes.append(a)
     torch.cuda.synchronize()
@@ -177,6 +177,20 @@ def test_v152k_eight_shards_full_size_sampled():
     assert abs(losses[0] - loss1) <= LOSS_RTOL * abs(loss1)
     assert np.abs(tl - aux1.token_logp.cpu().numpy()).max() <= LOGP_ATOL
     assert auxes[0].error_flags.item() == 0
+
+
+def test_global_group_count():
+    # n_groups_total as a data-parallel shard of a larger batch passes it: every w_i, the loss and dlogits scale
+    b = make_batch("tiny", "cuda")
+    cfg = b["cfg"]
+    A64, A32 = _adv(b)
+    oi = oracle_inputs(b, A64)
+    losses, dl, auxes, _ = run_sharded(b, A32, [0, 300, 1024], norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, c=3.0, ngt=17.0)
+    ref = oracle.loss_rows(to_np_logits(b["logits"]), oi["actions"], oi["behave"], None, oi["adv"], oi["seg"], cfg.G,
+                           norm=oracle.NORM_CONST_K, k=cfg.k, dual_clip_c=3.0, n_groups_total=17.0)
+    assert abs(losses[0] - ref.loss) <= LOSS_RTOL * abs(ref.loss)
+    kinks = kink_rows(ref, oi["behave"], None, A64[oi["seg"].tok_traj], 0.2, 0.2, 3.0)
+    check_dlogits(dl_to_f64(dl), ref.dlogits, False, exempt=kinks, what="n_groups_total")
 
 
 def test_forward_only_and_in_place():
