@@ -137,9 +137,49 @@ def cpu_baseline(b: dict, adv64, budget_s: float) -> dict:
         if time.perf_counter() - t0 >= budget_s:
             break
     el = time.perf_counter() - t0
-    return {"value": rows / el, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+    cores = oracle.threads()
+    # the same oracle on one thread, over fewer rows
+    oracle.set_threads(1)
+    r1 = 1024
+    t1 = time.perf_counter()
+    oracle.loss_rows(zl[:r1], actions, behave, None, adv64, seg, cfg.G, norm=oracle.NORM_CONST_K, k=cfg.k,
+                     dual_clip_c=3.0, row_begin=0, row_end=r1, row_offset=0)
+    el1 = time.perf_counter() - t1
+    oracle.set_threads(cores)
+    return {"value": rows / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"first {R} token rows of the same batch (loss + fp64 dlogits), cycled in blocks of "
-                      f"{chunk}; {rows} rows in {el:.1f} s"}
+                      f"{chunk}; {rows} rows in {el:.1f} s",
+            "single_thread": {"value": r1 / el1, "unit": "tokens/s", "cores": 1,
+                              "sample": f"first {r1} token rows, {el1:.1f} s"}}
+
+
+def copy_ceiling(t) -> dict:
+    """A plain device copy of a tensor of the same size (the runtime's copy), read + write bytes per second."""
+    import torch
+    dst = torch.empty_like(t)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    ms = []
+    for _ in range(3):
+        e0.record()
+        dst.copy_(t)
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    del dst
+    nbytes = 2.0 * t.numel() * t.element_size()
+    best = min(ms)
+    return {"GBps": nbytes / (best * 1e-3) / 1e9, "bytes": nbytes, "ms": best, "what": "torch copy_ of the logits"}
+
+
+def device_info() -> dict:
+    import torch
+    p = torch.cuda.get_device_properties(0)
+    out = {"name": p.name, "compute_units": p.multi_processor_count, "hbm_GiB": round(p.total_memory / 2**30, 1)}
+    clk = getattr(p, "clock_rate", None)
+    if clk:
+        out["max_clock_MHz"] = clk / 1000.0
+    return out
 
 
 def bench_logp(b: dict, steps: int, warmup: int = 2) -> dict:
@@ -240,7 +280,37 @@ def bench_vocab_shard(b: dict, steps: int, n_shards: int = 8, warmup: int = 2) -
             "roofline_rows": roof(alg_rows, rows_ms, "k_shard_rows_vec<bf16, 512, 5>")}
 
 
-def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0) -> dict:
+def fused_cpu_baseline(b: dict, rows: int = 64) -> dict:
+    """The fp64 fused oracle (z = h W, the loss rows, dhidden = D W^T, dW += h^T D) on the first rows of the fused
+    batch, timed on the host cores and scaled to tokens/s."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from oracle import fused
+    st, cfg = b["structure"], b["cfg"]
+    hb = b["hidden"][:rows].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    W64 = fused.as_f64(b["W"].contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+    seg = oracle.segments(st.T, st.step_tok_off, st.traj_step_off)
+    A = oracle.advantages(st.rewards, cfg.G).astype(np.float32).astype(np.float64)
+    actions, behave = b["actions"].cpu().numpy(), b["behave"].cpu().numpy()
+    t0 = time.perf_counter()
+    h64 = fused.as_f64(hb)
+    z = h64 @ W64
+    res = oracle.loss_rows(z, actions, behave, None, A, seg, cfg.G, norm=oracle.NORM_CONST_K, k=cfg.k,
+                           dual_clip_c=3.0, row_begin=0, row_end=rows, row_offset=0)
+    D = res.dlogits
+    dh = D @ W64.T
+    dW = h64.T @ D
+    el = time.perf_counter() - t0
+    del z, D, dh, dW, W64
+    return {"value": rows / el, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"first {rows} token rows of the fused batch: the three fp64 products and the loss rows, "
+                      f"{el:.1f} s (numpy float64 matmul on the host's cores; the per-token rate extrapolates "
+                      f"to the whole batch)"}
+
+
+def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = False) -> dict:
     """Times fused_lmhead_grpo on the fused workload; the hot region is pass 1 through pass 2."""
     import torch
 
@@ -296,6 +366,8 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0) -> dict:
         del dh, dw, ws
         torch.cuda.empty_cache()
         out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps)
+    if cpu:
+        out["cpu_baseline"] = fused_cpu_baseline(b)
     return out
 
 
@@ -450,6 +522,11 @@ def main():
                      "algorithmic_bytes_per_launch": alg_bytes},
     }
     del dlogits
+    torch.cuda.empty_cache()
+    out["device"] = device_info()
+    cc = copy_ceiling(b["logits"])
+    out["roofline"]["copy_ceiling_GBps"] = cc["GBps"]
+    out["roofline"]["frac_of_copy_ceiling"] = achieved / cc["GBps"]
     if args.cpu_seconds > 0:
         import oracle
         A = oracle.advantages(st.rewards, cfg.G).astype(np.float32).astype(np.float64)
@@ -461,7 +538,8 @@ def main():
     if args.fused_steps > 0:
         del b
         torch.cuda.empty_cache()
-        out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3)
+        out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3,
+                                          cpu=args.cpu_seconds > 0)
     print(json.dumps(out), flush=True)
 
 

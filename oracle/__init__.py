@@ -65,10 +65,17 @@ def _load():
         lib.oracle_logp_entropy.restype = ctypes.c_int
         lib.oracle_vocab_shard_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, P, I64, I64, P, P, P]
         lib.oracle_vocab_shard_stats.restype = None
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_threads.restype = None
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads for later oracle calls (the results do not depend on the count)."""
+    _load().oracle_set_threads(int(n))
 
 
 def threads() -> int:

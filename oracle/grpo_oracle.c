@@ -354,3 +354,6 @@ void oracle_vocab_shard_stats(const void* logits, int dtype, int64_t V_shard, in
 }
 
 int oracle_threads(void) { return omp_get_max_threads(); }
+
+/* Sets the OpenMP thread count of later calls (results do not depend on it). */
+void oracle_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
