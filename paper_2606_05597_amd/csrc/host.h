@@ -17,7 +17,7 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
 // Workspace of the loss: per-trajectory and per-token scratch.
 struct LossWs {
-  size_t hdr, traj_tok_off, w, traj_loss, traj_rstats, tok_adv, tok_w, contrib, state, tok_ratio, total;
+  size_t hdr, traj_tok_off, w, traj_loss, traj_rstats, tok_adv, tok_w, contrib, state, tok_ratio, records, total;
 };
 
 inline LossWs loss_ws_layout(int64_t T, int32_t n_traj) {
@@ -33,6 +33,7 @@ inline LossWs loss_ws_layout(int64_t T, int32_t n_traj) {
   l.contrib = o;      o = align_up(o + sizeof(double) * (size_t)(T > 0 ? T : 0));
   l.state = o;        o = align_up(o + sizeof(int8_t) * (size_t)(T > 0 ? T : 0));
   l.tok_ratio = o;    o = align_up(o + 2 * sizeof(double) * (size_t)(T > 0 ? T : 0));
+  l.records = o;      o = align_up(o + sizeof(grpo_vocab_stats) * (size_t)(T > 0 ? T : 0));  // two-pass rows
   l.total = o;
   return l;
 }

@@ -15,6 +15,7 @@
 
 #include "device.h"
 #include "host.h"
+#include "launch.h"
 
 namespace grpo {
 
@@ -200,6 +201,16 @@ static void launch_logp(const LogpArgs& a, grpo_dtype dt, hipStream_t s) {
   else if (vec) hipLaunchKernelGGL((k_logp_vec<float, 256, 4>), grid, dim3(256), 0, s, a);
   else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_logp_generic<uint16_t>, grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL(k_logp_generic<float>, grid, dim3(256), 0, s, a);
+}
+
+hipError_t launch_vocab_records(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                                int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats, int32_t* flags,
+                                hipStream_t s) {
+  if (T > 0) {
+    LogpArgs a{logits, ld, V, v_begin, (int)T, actions, nullptr, nullptr, flags, stats};
+    launch_logp(a, dt, s);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace grpo

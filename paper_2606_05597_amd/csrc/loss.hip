@@ -11,6 +11,11 @@
 //                   while row t's dlogits are written: part of each row lives
 //                   in LDS (global_load_lds), the rest in registers.
 //  k_rows_resident  shorter rows: one workgroup per row, several per CU.
+//  two passes       vector rows too long for either (fp32 beyond 77,824
+//                   columns, bf16 beyond 188,416): each row reduced to a
+//                   record (logp.hip), then the record turned into the token
+//                   epilogue and the row's dlogits (vocab.hip); the row is
+//                   read twice.
 //  k_rows_generic   any V, stride or alignment: element loads, three sweeps.
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -431,6 +436,7 @@ static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, c
     for (const Variant& v : kVariants) {
       if ((int64_t)v.nt * v.nv >= nvec) return Launch{dt == GRPO_BF16 ? v.bf16 : v.f32, v.nt, (unsigned)T};
     }
+    return Launch{nullptr, 0, 0};  // two passes
   }
   return Launch{dt == GRPO_BF16 ? k_rows_generic<uint16_t> : k_rows_generic<float>, 256, (unsigned)T};
 }
@@ -472,8 +478,16 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
     const Launch k = pick_row_kernel(dt, T, V, ld, logits, dlogits);
     const bool timed = aux && aux->hot_begin && aux->hot_end;
     if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
-    hipLaunchKernelGGL(k.k, dim3(k.grid), dim3(k.nt), 0, s, a);
-    if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+    if (k.k) {
+      hipLaunchKernelGGL(k.k, dim3(k.grid), dim3(k.nt), 0, s, a);
+      if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+    } else {
+      // the whole vocabulary as one shard: its records, then the merge (trivial), epilogue and dlogits
+      grpo_vocab_stats* rec = reinterpret_cast<grpo_vocab_stats*>(w + L.records);
+      int32_t* flags = &reinterpret_cast<WsHeader*>(w + L.hdr)->flags;
+      if (launch_vocab_records(logits, dt, T, V, ld, 0, actions, rec, flags, s) != hipSuccess) return GRPO_ERR_HIP;
+      if (launch_shard_rows(logits, dlogits, dt, T, V, ld, 0, rec, 1, a.tok, s) != hipSuccess) return GRPO_ERR_HIP;
+    }
     if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   }
   if (launch_reduce(T, seg->n_traj, w, L, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;

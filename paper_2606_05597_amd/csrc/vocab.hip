@@ -119,6 +119,30 @@ __global__ __launch_bounds__(256) void k_shard_rows_generic(const ShardArgs a) {
   }
 }
 
+hipError_t launch_shard_rows(const void* logits, void* dlogits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                             int64_t v_begin, const grpo_vocab_stats* stats, int n_shards, const TokenArgs& tok,
+                             hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  ShardArgs a;
+  a.logits = logits;
+  a.dlogits = dlogits;
+  a.ld = ld;
+  a.V = V;
+  a.v_begin = v_begin;
+  a.T = (int)T;
+  a.n_shards = n_shards;
+  a.stats = stats;
+  a.tok = tok;
+  const int epv = (dt == GRPO_BF16) ? 8 : 4;
+  const bool vec = V % epv == 0 && ld % epv == 0 && aligned(logits, 16) && aligned(dlogits, 16);
+  const dim3 grid((unsigned)T);
+  if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_shard_rows_vec<uint16_t, 512, 5>), grid, dim3(512), 0, s, a);
+  else if (vec) hipLaunchKernelGGL((k_shard_rows_vec<float, 512, 5>), grid, dim3(512), 0, s, a);
+  else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_shard_rows_generic<uint16_t>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_shard_rows_generic<float>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace grpo
 
 using namespace grpo;
@@ -145,26 +169,11 @@ extern "C" int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, 
 
   if (launch_segments(seg, T, ld, actions, adv, p, w, L, aux, s) != hipSuccess) return GRPO_ERR_HIP;
   if (T > 0) {
-    ShardArgs a;
-    a.logits = logits;
-    a.dlogits = dlogits;
-    a.ld = ld;
-    a.V = V_shard;
-    a.v_begin = v_begin;
-    a.T = (int)T;
-    a.n_shards = n_shards;
-    a.stats = stats;
-    a.tok = make_token_args(V_total, actions, behave_logp, prox_logp, adv, p, w, L, aux);
-    const int epv = 16 / (int)esz;
-    const bool vec = V_shard % epv == 0 && ld % epv == 0 && aligned(logits, 16) && aligned(dlogits, 16);
-    const dim3 grid((unsigned)T);
+    const TokenArgs tok = make_token_args(V_total, actions, behave_logp, prox_logp, adv, p, w, L, aux);
     const bool timed = aux && aux->hot_begin && aux->hot_end;
     if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
-    if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_shard_rows_vec<uint16_t, 512, 5>), grid, dim3(512), 0, s, a);
-    else if (vec) hipLaunchKernelGGL((k_shard_rows_vec<float, 512, 5>), grid, dim3(512), 0, s, a);
-    else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_shard_rows_generic<uint16_t>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(k_shard_rows_generic<float>, grid, dim3(256), 0, s, a);
-    if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+    if (launch_shard_rows(logits, dlogits, dt, T, V_shard, ld, v_begin, stats, n_shards, tok, s) != hipSuccess)
+      return GRPO_ERR_HIP;
     if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   }
   if (launch_reduce(T, seg->n_traj, w, L, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;

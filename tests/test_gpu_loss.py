@@ -226,11 +226,13 @@ def _edge_batch(V, dtype="bf16", n_groups=2, G=4, ld=None, seed=5):
 
 @pytest.mark.parametrize("V,dtype", [(7, "bf16"), (7, "f32"), (1000, "bf16"), (4093, "f32"), (33, "bf16"),
                                      (122880, "bf16"), (128256, "bf16"), (151936, "bf16"), (163840, "bf16"),
-                                     (184320, "bf16"), (200000, "bf16")])
+                                     (184320, "bf16"), (200000, "bf16"), (262144, "bf16"), (77824, "f32"),
+                                     (100000, "f32"), (151936, "f32")])
 def test_ragged_vocab_and_kernel_variants(V, dtype):
     # odd V uses the generic row kernel; bf16 rows of 56K to 188K take the pipelined kernel (122,880: one LDS
-    # vector per thread; 128,256: two; 151,936: five; 163,840 and 184,320: nine); 200,000 exceeds it and falls
-    # back to the generic kernel
+    # vector per thread; 128,256: two; 151,936: five; 163,840 and 184,320: nine); fp32 rows up to 77,824 the
+    # register-resident one; longer vector rows (bf16 200,000 and 262,144, fp32 100,000 and 151,936) the two
+    # passes (a record per row, then the epilogue and dlogits)
     b = _edge_batch(V, dtype)
     _full_parity(b, oracle.NORM_TRAJ_STEPS, 3.0)
 
@@ -283,8 +285,9 @@ def test_malformed_offsets_flagged():
     assert (aux.traj_tok_off.cpu() == -1).all()
 
 
-def test_nonfinite_logit_flagged():
-    b = _edge_batch(256, "bf16")
+@pytest.mark.parametrize("V,dtype", [(256, "bf16"), (200000, "bf16")])  # one pass; two passes
+def test_nonfinite_logit_flagged(V, dtype):
+    b = _edge_batch(V, dtype)
     b["logits"][2, 5] = float("nan")
     _, A32 = _adv(b)
     loss, dl, aux = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=4.0)
@@ -292,8 +295,9 @@ def test_nonfinite_logit_flagged():
     assert math.isnan(loss) and math.isnan(aux.token_logp[2].item())
 
 
-def test_forward_only_and_aliasing():
-    b = _edge_batch(4096, "bf16")
+@pytest.mark.parametrize("V,dtype", [(4096, "bf16"), (100000, "f32")])  # one pass; two passes
+def test_forward_only_and_aliasing(V, dtype):
+    b = _edge_batch(V, dtype)
     _, A32 = _adv(b)
     l0, dl0, a0 = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=4.0, c=3.0)
     l1, dl1, a1 = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=4.0, c=3.0, dlogits=None)
