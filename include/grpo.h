@@ -189,7 +189,9 @@ size_t fused_lmhead_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t voc
  * Emits the loss, dhidden = dloss/dh = D W^T and dW = dloss/dW = h^T D, where
  * D = grad_scale * dloss/dz (bf16-rounded per chunk before the two products).
  *   hidden       device bf16 [T, H] row-major       w_lm device bf16 [H, V] row-major
- *   T >= 0, H >= 1 and a multiple of 64, V >= 1 and a multiple of 8,
+ *   0 <= T <= 8,388,352 and 8 <= V <= 8,388,352 (2^23 - 256: the matrix-core products address
+ *   256 of their T- or V-long operand rows with 32-bit offsets), V a multiple of 8, H >= 64 and
+ *   a multiple of 64,
  *   vocab_chunk  a positive multiple of 256 (8192 is the tuned value)
  *   actions, behave_logp, prox_logp, adv, seg, p, loss_out, aux: as above
  *   (aux->gather_idx uses ld = V)
@@ -320,7 +322,8 @@ int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_shard, int6
  * Step 2 of the sharded fused LM head: given every shard's records (gathered by the
  * caller, the same shard order on every device), the loss (the whole rows', the same
  * on every shard), this shard's dW columns and its partial dhidden.
- *   hidden, w_shard, T, H, V_shard, v_begin: as in step 1
+ *   hidden, w_shard, T, H, V_shard, v_begin: as in step 1, and T, V_shard <= 8,388,352 as in
+ *                fused_lmhead_grpo
  *   V_total      the whole vocabulary; vocab_chunk as in fused_lmhead_grpo
  *   stats        device grpo_vocab_stats [n_shards][T], 8-byte aligned; n_shards 1 .. 65536
  *   actions, behave_logp, prox_logp, adv, seg, p, loss_out, aux: as grpo_loss_fwd_bwd

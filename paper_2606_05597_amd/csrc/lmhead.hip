@@ -615,6 +615,10 @@ static LmStatsWs lm_stats_ws_layout(int64_t T, int64_t H, int64_t V) {
   return l;
 }
 
+// The GEMMs address their operands through buffer descriptors with 32-bit byte offsets, 256 rows at a time: the
+// T-long rows of h^T and D^T (dW) and the V-long rows of W (dhidden) must keep 256 rows below 2^32 bytes.
+constexpr int64_t kMaxFusedLen = ((int64_t)1 << 23) - 256;
+
 static int check_fused_shapes(int64_t T, int64_t H, int64_t V) {
   if (T < 0 || T >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
   if (H < 64 || H % 64 != 0 || H >= (1 << 30)) return GRPO_ERR_SHAPE;
@@ -639,6 +643,7 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
   if (st != GRPO_OK) return st;
   if (!w_lm || !dw_lm || (T > 0 && (!hidden || !dhidden))) return GRPO_ERR_ARG;
+  if (T > kMaxFusedLen || V > kMaxFusedLen) return GRPO_ERR_SHAPE;
   if (H < 64 || H % 64 != 0 || H >= (1 << 30)) return GRPO_ERR_SHAPE;
   if (V < 8 || V % 8 != 0 || V >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
   if (vocab_chunk < 256 || vocab_chunk % 256 != 0) return GRPO_ERR_SHAPE;
@@ -733,6 +738,7 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
   if (!w_shard || !dw_shard || (T > 0 && (!hidden || !dhidden_partial || !stats))) return GRPO_ERR_ARG;
   st = check_fused_shapes(T, H, V_shard);
   if (st != GRPO_OK) return st;
+  if (T > kMaxFusedLen || V_shard > kMaxFusedLen) return GRPO_ERR_SHAPE;
   if (vocab_chunk < 256 || vocab_chunk % 256 != 0) return GRPO_ERR_SHAPE;
   if (v_begin < 0 || V_total >= ((int64_t)1 << 31) || v_begin + V_shard > V_total || n_shards < 1 ||
       n_shards > 65536)

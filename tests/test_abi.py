@@ -146,6 +146,8 @@ def call_fused(lib, *, T=8, H=64, V=512, chunk=256, hidden=D, w=D, dh=D, dw=D, w
 
 @pytest.mark.parametrize("kw,status", [
     (dict(H=96), _lib.GRPO_ERR_SHAPE),        # H a multiple of 64
+    (dict(T=(1 << 23) - 255), _lib.GRPO_ERR_SHAPE),  # T- and V-long operand rows addressed with 32-bit offsets
+    (dict(V=(1 << 23) - 248), _lib.GRPO_ERR_SHAPE),
     (dict(V=500), _lib.GRPO_ERR_SHAPE),       # V a multiple of 8
     (dict(chunk=300), _lib.GRPO_ERR_SHAPE),   # chunk a multiple of 256
     (dict(chunk=0), _lib.GRPO_ERR_SHAPE),
@@ -271,6 +273,7 @@ def call_fused_shard(lib, *, T=8, H=64, V=512, v_begin=0, V_total=1024, chunk=25
 @pytest.mark.parametrize("kw,status", [
     (dict(H=96), _lib.GRPO_ERR_SHAPE),
     (dict(V=500), _lib.GRPO_ERR_SHAPE),
+    (dict(T=(1 << 23) - 255), _lib.GRPO_ERR_SHAPE),
     (dict(chunk=300), _lib.GRPO_ERR_SHAPE),
     (dict(v_begin=-8), _lib.GRPO_ERR_SHAPE),
     (dict(v_begin=520), _lib.GRPO_ERR_SHAPE),      # v_begin + V_shard > V_total
