@@ -95,6 +95,7 @@ def parse():
     ap.add_argument("--shard-steps", type=int, default=10,
                     help="timed steps of one device's share of the vocabulary-parallel loss (0 = skip)")
     ap.add_argument("--skip-logits", action="store_true", help="measure only the fused path")
+    ap.add_argument("--token-block", type=int, default=8192, help="token block of the blocked fused schedule")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter calibration)")
     return ap.parse_args()
@@ -310,24 +311,26 @@ def fused_cpu_baseline(b: dict, rows: int = 64) -> dict:
                       f"to the whole batch)"}
 
 
-def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = False) -> dict:
-    """Times fused_lmhead_grpo on the fused workload; the hot region is pass 1 through pass 2."""
+def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int = 0) -> dict:
+    """Times one schedule of the fused LM head on batch b: the vocabulary-chunked fused_lmhead_grpo (token_block 0)
+    or the token-blocked fused_lmhead_grpo_blocked.  The hot region, timed with events the library records on its
+    stream, is the first forward product through the last backward product."""
     import torch
 
     import paper_2606_05597_amd as grpo
-    from synth import make_fused_batch
-
-    dev = torch.device("cuda:0")
-    b = make_fused_batch("fused", dev)
     cfg, st = b["cfg"], b["structure"]
     T, H, V = st.T, b["H"], b["V"]
     N = len(st.rewards)
-    sto = torch.from_numpy(st.step_tok_off).to(dev)
-    tso = torch.from_numpy(st.traj_step_off).to(dev)
-    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    dev = b["hidden"].device
     dh = torch.empty_like(b["hidden"])
     dw = torch.empty((H, V), dtype=torch.float32, device=dev)
-    ws = torch.empty(grpo.fused_lmhead_workspace_bytes(T, H, V, cfg.vocab_chunk, N), dtype=torch.uint8, device=dev)
+    if token_block:
+        need = grpo.fused_lmhead_blocked_workspace_bytes(T, H, V, token_block, N)
+        entry, kw = grpo.fused_lmhead_grpo_blocked, dict(token_block=token_block)
+    else:
+        need = grpo.fused_lmhead_workspace_bytes(T, H, V, cfg.vocab_chunk, N)
+        entry, kw = grpo.fused_lmhead_grpo, dict(vocab_chunk=cfg.vocab_chunk)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
     loss = torch.empty(1, dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream()
     ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
@@ -339,9 +342,8 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
     def step(i=None):
         grpo.grpo_advantages(b["rewards"], cfg.G, out=adv)
         aux = None if i is None else grpo.LossAux(hot_events=(ev0[i].cuda_event, ev1[i].cuda_event))
-        grpo.fused_lmhead_grpo(b["hidden"], b["W"], b["actions"], b["behave"], adv, sto, tso, cfg.G,
-                               vocab_chunk=cfg.vocab_chunk, norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, dual_clip_c=3.0,
-                               dhidden=dh, dw_lm=dw, aux=aux, workspace=ws, loss_out=loss)
+        entry(b["hidden"], b["W"], b["actions"], b["behave"], adv, sto, tso, cfg.G, norm=grpo.GRPO_NORM_CONST_K,
+              k=cfg.k, dual_clip_c=3.0, dhidden=dh, dw_lm=dw, aux=aux, workspace=ws, loss_out=loss, **kw)
 
     for _ in range(warmup):
         step()
@@ -352,19 +354,49 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
     hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(steps)) / steps
+    products = 3 if token_block else 4
     alg = 6.0 * T * H * V
     achieved = alg / (hot_ms * 1e-3) / 1e12
-    out = {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
-           "workload": f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], chunks of {cfg.vocab_chunk}, "
-                       f"{cfg.n_groups} groups x G={cfg.G}",
-           "loss": float(loss.item()),
+    out = {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps, "hot_ms": hot_ms,
+           "loss": float(loss.item()), "workspace_bytes": need,
+           "schedule": (f"token blocks of {token_block} (their fp32 logits kept between the products; 3 products)"
+                        if token_block else
+                        f"vocabulary chunks of {cfg.vocab_chunk} (logits recomputed for the backward; 4 products)"),
            "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                        "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": measured_fused_traffic(), "hot_ms": hot_ms,
+                        "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "hot_ms": hot_ms,
                         "algorithmic_flop_per_launch": alg,
-                        "executed_frac": (8.0 * T * H * V) / (hot_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS}}
+                        "executed_frac": (2.0 * products * T * H * V) / (hot_ms * 1e-3) / 1e12
+                        / MFMA_BF16_PEAK_TFLOPS}}
+    del dh, dw, ws
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = False,
+                token_block: int = 8192) -> dict:
+    """The fused workload in both schedules; the token-blocked one is the line's value, the vocabulary-chunked one
+    is reported beside it."""
+    import torch
+
+    from synth import make_fused_batch
+
+    dev = torch.device("cuda:0")
+    b = make_fused_batch("fused", dev)
+    cfg, st = b["cfg"], b["structure"]
+    T, H, V = st.T, b["H"], b["V"]
+    N = len(st.rewards)
+    sto = torch.from_numpy(st.step_tok_off).to(dev)
+    tso = torch.from_numpy(st.traj_step_off).to(dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    blocked = time_fused(b, adv, sto, tso, steps, warmup, token_block)
+    chunked = time_fused(b, adv, sto, tso, steps, warmup, 0)
+    chunked["roofline"]["traffic"] = measured_fused_traffic()
+    out = dict(blocked)
+    out["workload"] = (f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], {cfg.n_groups} groups x G={cfg.G}; "
+                       f"{blocked['schedule']}")
+    out["roofline"] = dict(blocked["roofline"], traffic=None)
+    out["vocab_chunked"] = chunked
     if shard_steps > 0:
-        del dh, dw, ws
-        torch.cuda.empty_cache()
         out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps)
     if cpu:
         out["cpu_baseline"] = fused_cpu_baseline(b)
@@ -449,7 +481,8 @@ def main():
         copy_calibration()
         return
     if args.skip_logits:
-        print(json.dumps({"fused_lmhead": bench_fused(max(1, args.fused_steps), shard_steps=args.shard_steps and 3)}),
+        print(json.dumps({"fused_lmhead": bench_fused(max(1, args.fused_steps), shard_steps=args.shard_steps and 3,
+                                                          token_block=args.token_block)}),
               flush=True)
         return
     import numpy as np
@@ -539,7 +572,7 @@ def main():
         del b
         torch.cuda.empty_cache()
         out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3,
-                                          cpu=args.cpu_seconds > 0)
+                                          cpu=args.cpu_seconds > 0, token_block=args.token_block)
     print(json.dumps(out), flush=True)
 
 

@@ -209,6 +209,29 @@ int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T, int64_t H
                       float* dw_lm, int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
                       hipStream_t s);
 
+/* Bytes of device workspace fused_lmhead_grpo_blocked needs: besides what fused_lmhead_grpo needs, one block's
+ * fp32 logits and its D and D^T, (4 + 2 + 2) * min(token_block, T rounded up to 256) * (V rounded up to 256)
+ * bytes (11.5 GB in all at T = 65,536, H = 3,584, V = 151,936, token_block = 8192).  0 for invalid sizes. */
+size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t token_block, int32_t n_traj);
+
+/*
+ * The fused LM-head path of fused_lmhead_grpo, scheduled over blocks of tokens instead of vocabulary chunks, and
+ * with the same results up to the order of fp32 sums.  The forward product of a block of `token_block` rows
+ * (z = h W, on the matrix cores, 256-column tiles) is kept in the workspace as fp32 until the block's rows have
+ * their log-sum-exp; D of the block is then formed from the stored logits instead of a second product, so three
+ * products run instead of four.  The logits of the whole batch are never stored: one block at a time.
+ * Per block: dhidden rows = D W^T (the whole vocabulary as K, written once in bf16), dW (+)= h^T D.
+ *   token_block  a positive multiple of 256, at most 8,388,352 (8192 is the tuned value)
+ *   all other arguments as fused_lmhead_grpo
+ *   ws, ws_bytes device workspace of at least fused_lmhead_blocked_workspace_bytes(...)
+ * Errors: as fused_lmhead_grpo (GRPO_ERR_SHAPE for token_block outside the range above).
+ */
+int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V,
+                              int32_t token_block, const int32_t* actions, const float* behave_logp,
+                              const float* prox_logp, const float* adv, const grpo_segments* seg,
+                              const grpo_loss_params* p, double* loss_out, void* dhidden, float* dw_lm,
+                              int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
+
 /*
  * Forward only: the sampled action's log-prob and the policy entropy of each
  * token row, with no loss and no dlogits -- the proximal log-probs recomputed

@@ -19,7 +19,7 @@ from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO
                    GRPO_NORM_TRAJ_STEPS, GrpoError)
 
 __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
-           "fused_lmhead_grpo", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
+           "fused_lmhead_grpo", "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
            "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
            "grpo_status_str", "LossAux", "GrpoError"]
 
@@ -87,6 +87,11 @@ def grpo_loss_workspace_bytes(T: int, n_traj: int) -> int:
 
 def fused_lmhead_workspace_bytes(T: int, H: int, V: int, vocab_chunk: int, n_traj: int) -> int:
     return int(_lib.load().fused_lmhead_workspace_bytes(int(T), int(H), int(V), int(vocab_chunk), int(n_traj)))
+
+
+def fused_lmhead_blocked_workspace_bytes(T: int, H: int, V: int, token_block: int, n_traj: int) -> int:
+    return int(_lib.load().fused_lmhead_blocked_workspace_bytes(int(T), int(H), int(V), int(token_block),
+                                                                int(n_traj)))
 
 
 @dataclass
@@ -214,18 +219,9 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
     return loss_out, dlogits
 
 
-def fused_lmhead_grpo(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.Tensor, behave_logp: torch.Tensor,
-                      adv: torch.Tensor, step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *,
-                      vocab_chunk: int = 8192, prox_logp: torch.Tensor | None = None,
-                      norm: int = GRPO_NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2, eps_high: float = 0.2,
-                      dual_clip_c: float = 0.0, grad_scale: float = 1.0, n_groups_total: float = 0.0,
-                      dhidden: torch.Tensor | None = None, dw_lm: torch.Tensor | None = None,
-                      accumulate_dw: bool = False, aux: LossAux | None = None,
-                      workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None, stream=None):
-    """Loss, dhidden (bf16 [T, H]) and dW (fp32 [H, V]) from hidden [T, H] and W [H, V] (bf16).
-
-    Returns (loss [1] fp64, dhidden, dw_lm).
-    """
+def _fused_call(entry: str, ws_bytes, hidden, w_lm, actions, behave_logp, adv, step_tok_off, traj_step_off,
+                group_size, sched, prox_logp, norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total,
+                dhidden, dw_lm, accumulate_dw, aux, workspace, loss_out, stream):
     _dev(hidden, "hidden")
     _dev(w_lm, "w_lm")
     if hidden.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
@@ -243,19 +239,59 @@ def fused_lmhead_grpo(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.T
         dw_lm = torch.empty((H, V), dtype=torch.float32, device=hidden.device)
     _dev(dhidden, "dhidden")
     _dev(dw_lm, "dw_lm")
-    need = fused_lmhead_workspace_bytes(T, H, V, vocab_chunk, seg.n_traj)
+    need = ws_bytes(T, H, V, sched, seg.n_traj)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
     if loss_out is None:
         loss_out = torch.empty(1, dtype=torch.float64, device=hidden.device)
     ca = aux._c() if aux is not None else None
-    st = _lib.load().fused_lmhead_grpo(
-        _ptr(hidden), _ptr(w_lm), T, H, V, int(vocab_chunk), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
+    st = getattr(_lib.load(), entry)(
+        _ptr(hidden), _ptr(w_lm), T, H, V, int(sched), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
         _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
         _ptr(loss_out), _ptr(dhidden), _ptr(dw_lm), int(bool(accumulate_dw)),
         ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
-    _check(st, "fused_lmhead_grpo")
+    _check(st, entry)
     return loss_out, dhidden, dw_lm
+
+
+def fused_lmhead_grpo(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.Tensor, behave_logp: torch.Tensor,
+                      adv: torch.Tensor, step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *,
+                      vocab_chunk: int = 8192, prox_logp: torch.Tensor | None = None,
+                      norm: int = GRPO_NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2, eps_high: float = 0.2,
+                      dual_clip_c: float = 0.0, grad_scale: float = 1.0, n_groups_total: float = 0.0,
+                      dhidden: torch.Tensor | None = None, dw_lm: torch.Tensor | None = None,
+                      accumulate_dw: bool = False, aux: LossAux | None = None,
+                      workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None, stream=None):
+    """Loss, dhidden (bf16 [T, H]) and dW (fp32 [H, V]) from hidden [T, H] and W [H, V] (bf16), over vocabulary
+    chunks with the logits recomputed for the backward products.
+
+    Returns (loss [1] fp64, dhidden, dw_lm).
+    """
+    return _fused_call("fused_lmhead_grpo", fused_lmhead_workspace_bytes, hidden, w_lm, actions, behave_logp, adv,
+                       step_tok_off, traj_step_off, group_size, vocab_chunk, prox_logp, norm, k, eps_low, eps_high,
+                       dual_clip_c, grad_scale, n_groups_total, dhidden, dw_lm, accumulate_dw, aux, workspace,
+                       loss_out, stream)
+
+
+def fused_lmhead_grpo_blocked(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.Tensor,
+                              behave_logp: torch.Tensor, adv: torch.Tensor, step_tok_off: torch.Tensor,
+                              traj_step_off: torch.Tensor, group_size: int, *, token_block: int = 8192,
+                              prox_logp: torch.Tensor | None = None, norm: int = GRPO_NORM_CONST_K, k: float = 10.0,
+                              eps_low: float = 0.2, eps_high: float = 0.2, dual_clip_c: float = 0.0,
+                              grad_scale: float = 1.0, n_groups_total: float = 0.0,
+                              dhidden: torch.Tensor | None = None, dw_lm: torch.Tensor | None = None,
+                              accumulate_dw: bool = False, aux: LossAux | None = None,
+                              workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None,
+                              stream=None):
+    """As fused_lmhead_grpo, over blocks of `token_block` tokens whose fp32 logits are kept in the workspace
+    between the forward and backward products (three products instead of four).
+
+    Returns (loss [1] fp64, dhidden, dw_lm).
+    """
+    return _fused_call("fused_lmhead_grpo_blocked", fused_lmhead_blocked_workspace_bytes, hidden, w_lm, actions,
+                       behave_logp, adv, step_tok_off, traj_step_off, group_size, token_block, prox_logp, norm, k,
+                       eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total, dhidden, dw_lm, accumulate_dw,
+                       aux, workspace, loss_out, stream)
 
 
 def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | None = None, entropy: bool = True,

@@ -29,6 +29,7 @@ namespace grpo {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 typedef GemmCfg<256, 256, 2, 4> LmCfg;  // BM, BN, waves in M, waves in N
 constexpr int TILE = 256;               // BM = BN
@@ -61,8 +62,11 @@ struct PartialArgs {
   GemmArgs g;    // A = h [T, H], B = W^T [V, H]
   float2* part;  // [T, n_tiles] (max, sum exp over the tile's columns)
   int n_tiles;
+  float* z;      // STORE_Z: the fp32 logits [tiles_of(M) * TILE, ldz], every tile stored whole
+  int64_t ldz;   // a multiple of TILE, at least n_tiles * TILE
 };
 
+template <bool STORE_Z>
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
   int tm, tn;
@@ -72,6 +76,19 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
   gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  if constexpr (STORE_Z) {
+    // rows and columns past M and N hold zeros (their operand rows read as zero); each store instruction writes
+    // two 128-byte row pieces (lanes 0-31 and 32-63)
+    float* zt = p.z + (int64_t)m0 * p.ldz + n0;
+#pragma unroll
+    for (int i = 0; i < LmCfg::IB; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float* zr = zt + (int64_t)gemm_row<LmCfg>(wm, i, r, lane) * p.ldz + gemm_col<LmCfg>(wn, 0, lane);
+#pragma unroll
+        for (int j = 0; j < LmCfg::JB; ++j) __builtin_nontemporal_store(acc[i][j][r], zr + 32 * j);
+      }
+  }
   // A 16-lane row of a wave holds 16 x JB columns of one output row: reduce them with
   // DPP, then the 2 x WGN such groups of each row through LDS.
   constexpr int NG = 2 * LmCfg::WGN;
@@ -143,6 +160,7 @@ struct CombineArgs {
   const uint16_t* WT;  // [V, H]
   RowScale* rs;        // [Tp]; rows >= T get the zero scale
   int T, H, n_tiles;
+  int t0;              // row of blockIdx.x 0; part holds rows from t0 on
 };
 
 // Row t of 256 threads: the row's shift M and S = sum over its tiles of the partials rescaled to M, and the
@@ -194,7 +212,7 @@ __device__ inline void lm_row_stats(const float2* pr, int n_tiles, const uint16_
 
 __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   __shared__ RowStatsSmem sh;
-  const int t = blockIdx.x, tid = threadIdx.x;
+  const int t = a.t0 + (int)blockIdx.x, tid = threadIdx.x;
   if (t >= a.T) {
     if (tid == 0) a.rs[t] = RowScale{-INFINITY, 1.f, 0.f, -1};
     return;
@@ -203,8 +221,8 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   const bool ok = act >= 0 && (int64_t)act < a.tok.V;
   float M;
   double S, za;
-  lm_row_stats(a.part + (int64_t)t * a.n_tiles, a.n_tiles, a.h + (int64_t)t * a.H, a.WT, ok ? act : -1, a.H, sh, M,
-               S, za);
+  lm_row_stats(a.part + (int64_t)(t - a.t0) * a.n_tiles, a.n_tiles, a.h + (int64_t)t * a.H, a.WT, ok ? act : -1, a.H,
+               sh, M, S, za);
   if (tid == 0) {
     const TokenIn in = token_load(a.tok, t);
     a.rs[t] = token_finish(a.tok, t, in, row_lse((double)M, S), za);
@@ -463,6 +481,101 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_dw(const DhDwArgs p) {
   else lm_dh_tile(p.dh, b - p.dw_blocks, (int)gridDim.x - p.dw_blocks, sm);
 }
 
+// The token-blocked schedule's backward launch: the dhidden tiles (K = the whole vocabulary) first, then the dW
+// tiles (K = the block's rows).  A dhidden tile is then the longest unit by far; dispatched first, the long tiles
+// spread over the CUs and the many short dW tiles fill the time the last of them leave.
+struct DhThenDwArgs {
+  DhArgs dh;
+  DwArgs dw;
+  int dh_blocks;  // blocks [0, dh_blocks) take dhidden tiles, the rest dW tiles; a multiple of 8
+};
+
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_then_dw(const DhThenDwArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  const int b = blockIdx.x;
+  if (b < p.dh_blocks) lm_dh_tile(p.dh, b, p.dh_blocks, sm);
+  else lm_dw_tile(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
+}
+
+// ---- token-blocked schedule: a block's stored fp32 logits -> D = g (softmax - onehot), bf16, as D and D^T ----
+struct BlockDArgs {
+  const float* z;      // [rows, ld] the block's logits
+  const RowScale* rs;  // [rows] the block's row scales
+  uint16_t* D;         // [rows, ld]
+  uint16_t* DT;        // [ld, rows]
+  int64_t ld;          // a multiple of 64; columns V..ld get D = 0
+  int V, rows;         // rows: a multiple of 64
+};
+constexpr int kBlockDStrip = 512;  // columns per workgroup: eight 64 x 64 tiles
+
+// 256 threads, 64 rows (blockIdx.x), a strip of up to eight 64-column tiles (blockIdx.y).  Per tile a thread takes two 2 x 4 pieces (rows
+// 2p, 2p + 1 of four columns, p = tid / 16 and p + 16): two 16-byte logit loads each; the D rows go out as 8-byte
+// stores (16 lanes fill a 128-byte line); for D^T every column's row pair is packed into one 32-bit LDS word
+// (stride 33 words per column: the stores are conflict-free and the reads two-way), read back as four words =
+// eight rows, and stored 16 bytes at a time (8 lanes per 128-byte column piece).  Two LDS buffers, one barrier
+// per tile.
+__global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
+  constexpr int kLdw = 33;
+  __shared__ uint32_t tu[2][64 * kLdw];
+  __shared__ RowScale srs[64];
+  const int tid = threadIdx.x;
+  const int r0 = blockIdx.x * 64;
+  const int64_t cs = (int64_t)blockIdx.y * kBlockDStrip;
+  if (tid < 64) srs[tid] = a.rs[r0 + tid];
+  __syncthreads();
+  const int cq = tid & 15, rp = tid >> 4;
+  RowScale rs[4];  // rows 2 rp, 2 rp + 1, 2 rp + 32, 2 rp + 33
+#pragma unroll
+  for (int k = 0; k < 4; ++k) rs[k] = srs[2 * rp + (k & 1) + 32 * (k >> 1)];
+  const int ntiles = (int)min((int64_t)(kBlockDStrip / 64), (a.ld - cs) / 64);
+  for (int it = 0; it < ntiles; ++it) {
+    const int64_t c = cs + it * 64 + 4 * cq;
+    f32x4 x[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int row = 2 * rp + (k & 1) + 32 * (k >> 1);
+      x[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.z + (int64_t)(r0 + row) * a.ld + c));
+    }
+    uint32_t w[4][2];  // packed bf16 pairs: row k, columns (0, 1) and (2, 3)
+    uint16_t d16[4][4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float xv[4] = {x[k][0], x[k][1], x[k][2], x[k][3]};
+      float d[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t v = c + e;
+        d[e] = v >= a.V ? 0.f
+             : (v == rs[k].act) ? rs[k].d_a
+                                : rs[k].sign * __builtin_amdgcn_exp2f(fmaf(xv[e], kLog2e, rs[k].nc));
+      }
+      w[k][0] = pack_bf16(d[0], d[1]);
+      w[k][1] = pack_bf16(d[2], d[3]);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        d16[k][2 * e] = (uint16_t)(w[k][e] & 0xffffu);
+        d16[k][2 * e + 1] = (uint16_t)(w[k][e] >> 16);
+      }
+      const int row = 2 * rp + (k & 1) + 32 * (k >> 1);
+      *reinterpret_cast<u32x2*>(a.D + (int64_t)(r0 + row) * a.ld + c) = u32x2{w[k][0], w[k][1]};
+    }
+    uint32_t* t = tu[it & 1];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        t[(4 * cq + e) * kLdw + rp + 16 * u] = (uint32_t)d16[2 * u][e] | ((uint32_t)d16[2 * u + 1][e] << 16);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int col = (tid >> 3) + 32 * q, rc = tid & 7;
+      const uint32_t* src = t + col * kLdw + 4 * rc;
+      const u32x4 v = {src[0], src[1], src[2], src[3]};
+      *reinterpret_cast<u32x4*>(a.DT + (cs + it * 64 + col) * a.rows + r0 + 8 * rc) = v;
+    }
+  }
+}
+
 // ---- bf16 transpose: dst[c][r] = src[r][c] for r < R, 0 for R <= r < Rp ------------
 __global__ __launch_bounds__(256) void k_transpose_bf16(const uint16_t* __restrict__ src, int64_t lds_, int R,
                                                         int Cc, uint16_t* __restrict__ dst, int64_t ldd, int Rp) {
@@ -547,7 +660,9 @@ static void lm_pass1(const uint16_t* h16, const uint16_t* WT, int64_t T, int64_t
   pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
   pa.part = part;
   pa.n_tiles = n_tiles;
-  hipLaunchKernelGGL(k_lm_partial, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
+  pa.z = nullptr;
+  pa.ldz = 0;
+  hipLaunchKernelGGL(k_lm_partial<false>, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
 }
 
 // Pass 2 over the vocabulary chunks of W [H, V] (a whole LM head or one shard's columns), given every row's
@@ -600,6 +715,32 @@ static void lm_pass2(const Pass2& q, hipStream_t s) {
       hipLaunchKernelGGL(k_lm_dh_dw, dim3((unsigned)ba.dw_blocks + gemm_grid(q.T, q.H).x), dim3(LmCfg::NT), 0, s, ba);
     }
   }
+}
+
+// The token-blocked schedule's workspace: one block of rows at a time keeps its fp32 logits and its D, D^T.
+struct LmBlockWs {
+  LossWs loss;
+  size_t wt, ht, part, rs, z, d, dt, total;
+  int64_t Tp, Tbp, ldz;
+  int n_tiles;
+};
+static LmBlockWs lm_block_ws_layout(int64_t T, int64_t H, int64_t V, int32_t Tb, int32_t n_traj) {
+  LmBlockWs l;
+  l.loss = loss_ws_layout(T, n_traj);
+  l.Tp = (T + TILE - 1) / TILE * TILE;
+  l.Tbp = l.Tp < Tb ? l.Tp : Tb;
+  l.n_tiles = (int)((V + TILE - 1) / TILE);
+  l.ldz = (int64_t)l.n_tiles * TILE;
+  size_t o = l.loss.total;
+  l.wt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(V * H));
+  l.ht = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(H * l.Tp));
+  l.part = o; o = align_up(o + sizeof(float2) * (size_t)(l.Tbp * l.n_tiles));
+  l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
+  l.z = o;    o = align_up(o + sizeof(float) * (size_t)(l.Tbp * l.ldz));
+  l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tbp * l.ldz));
+  l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.ldz * l.Tbp));
+  l.total = o;
+  return l;
 }
 
 // The shard statistics call needs W^T of the shard and the pass-1 partials only.
@@ -686,12 +827,109 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   ca.T = (int)T;
   ca.H = (int)H;
   ca.n_tiles = L.n_tiles;
+  ca.t0 = 0;
   hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)Tp), dim3(256), 0, s, ca);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   lm_pass2(Pass2{h16, W16, WT, hT, rs, D, DT, acc, static_cast<uint16_t*>(dhidden), dw_lm, T, H, V, Tp,
                  vocab_chunk, accumulate_dw},
            s);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
+  if (launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;
+  return GRPO_OK;
+}
+
+extern "C" size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t token_block,
+                                                      int32_t n_traj) {
+  if (T < 0 || H < 1 || V < 1 || token_block < TILE || token_block % TILE != 0 || n_traj < 1) return 0;
+  return lm_block_ws_layout(T, H, V, token_block, n_traj).total;
+}
+
+extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V,
+                                         int32_t token_block, const int32_t* actions, const float* behave_logp,
+                                         const float* prox_logp, const float* adv, const grpo_segments* seg,
+                                         const grpo_loss_params* p, double* loss_out, void* dhidden, float* dw_lm,
+                                         int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
+                                         hipStream_t s) {
+  int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
+  if (st != GRPO_OK) return st;
+  if (!w_lm || !dw_lm || (T > 0 && (!hidden || !dhidden))) return GRPO_ERR_ARG;
+  st = check_fused_shapes(T, H, V);
+  if (st != GRPO_OK) return st;
+  if (T > kMaxFusedLen || V > kMaxFusedLen) return GRPO_ERR_SHAPE;
+  if (token_block < TILE || token_block % TILE != 0 || token_block > kMaxFusedLen) return GRPO_ERR_SHAPE;
+  if (!aligned(hidden, 16) || !aligned(w_lm, 16) || !aligned(dhidden, 16) || !aligned(dw_lm, 16))
+    return GRPO_ERR_ALIGN;
+  const LmBlockWs L = lm_block_ws_layout(T, H, V, token_block, seg->n_traj);
+  if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
+  char* w = static_cast<char*>(ws);
+  const uint16_t* h16 = static_cast<const uint16_t*>(hidden);
+  const uint16_t* W16 = static_cast<const uint16_t*>(w_lm);
+  uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);
+  uint16_t* hT = reinterpret_cast<uint16_t*>(w + L.ht);
+  float2* part = reinterpret_cast<float2*>(w + L.part);
+  RowScale* rs = reinterpret_cast<RowScale*>(w + L.rs);
+  float* z = reinterpret_cast<float*>(w + L.z);
+  uint16_t* D = reinterpret_cast<uint16_t*>(w + L.d);
+  uint16_t* DT = reinterpret_cast<uint16_t*>(w + L.dt);
+  uint16_t* dh16 = static_cast<uint16_t*>(dhidden);
+  const int Tp = (int)L.Tp;
+
+  if (launch_segments(seg, T, V, actions, adv, p, w, L.loss, aux, s) != hipSuccess) return GRPO_ERR_HIP;
+  if (T == 0) {
+    if (!accumulate_dw) hipLaunchKernelGGL(k_fill_f32, dim3(1024), dim3(256), 0, s, dw_lm, H * V, 0.f);
+    if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+    return launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+  }
+  lm_transpose(W16, h16, T, H, V, Tp, WT, hT, s);
+  if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  const bool timed = aux && aux->hot_begin && aux->hot_end;
+  if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
+  const TokenArgs tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
+  for (int64_t t0 = 0; t0 < T; t0 += L.Tbp) {
+    const int rows = (int)(T - t0 < L.Tbp ? T - t0 : L.Tbp);  // the block's tokens
+    const int rows_p = (rows + TILE - 1) / TILE * TILE;
+    // forward product of the block: partials and the stored logits
+    PartialArgs pa;
+    pa.g = GemmArgs{h16 + t0 * H, WT, H, H, rows, (int)V, (int)H};
+    pa.part = part;
+    pa.n_tiles = L.n_tiles;
+    pa.z = z;
+    pa.ldz = L.ldz;
+    hipLaunchKernelGGL(k_lm_partial<true>, gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
+    // the block's rows: lse, action logit, token epilogue, row scale
+    CombineArgs ca;
+    ca.tok = tok;
+    ca.part = part;
+    ca.h = h16;
+    ca.WT = WT;
+    ca.rs = rs;
+    ca.T = (int)T;
+    ca.H = (int)H;
+    ca.n_tiles = L.n_tiles;
+    ca.t0 = (int)t0;
+    hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)rows_p), dim3(256), 0, s, ca);
+    // D and D^T of the block
+    BlockDArgs da{z, rs + t0, D, DT, L.ldz, (int)V, rows_p};
+    hipLaunchKernelGGL(k_lm_block_d, dim3((unsigned)(rows_p / 64), (unsigned)((L.ldz + kBlockDStrip - 1) / kBlockDStrip)),
+                       dim3(256), 0, s, da);
+    // dhidden rows of the block = D W^T (K = V); dW (+)= h^T D (K = the block's rows, zero-padded)
+    DhThenDwArgs ba;
+    ba.dh.g = GemmArgs{D, W16, L.ldz, V, rows, (int)H, (int)V};
+    ba.dh.acc = nullptr;
+    ba.dh.dh = dh16 + t0 * H;
+    ba.dh.first = 1;
+    ba.dh.last = 1;
+    ba.dw.g = GemmArgs{hT + t0, DT, Tp, rows_p, (int)H, (int)V, rows_p};
+    ba.dw.dw = dw_lm;
+    ba.dw.V = V;
+    ba.dw.c0 = 0;
+    ba.dw.accumulate = (t0 > 0 || accumulate_dw) ? 1 : 0;
+    ba.dh_blocks = (int)gemm_grid(rows, H).x;
+    hipLaunchKernelGGL(k_lm_dh_then_dw, dim3((unsigned)ba.dh_blocks + gemm_grid(H, V).x), dim3(LmCfg::NT), 0, s, ba);
+    if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  }
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   if (launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;
   return GRPO_OK;

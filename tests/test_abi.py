@@ -35,6 +35,7 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes",
                                            "grpo_loss_fwd_bwd",
                                            "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_token_logp",
+                                           "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked",
                                            "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
                                            "fused_lmhead_vocab_shard_stats_workspace_bytes",
                                            "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
@@ -68,6 +69,16 @@ def test_workspace_queries(lib):
     assert f >= 2 * V * H + 2 * H * T + 2 * 2 * T * C + 4 * T * H and f % 256 == 0
     # a single chunk needs no dhidden accumulator
     assert lib.fused_lmhead_workspace_bytes(T, H, 4096, 4096, 64) < 2 * 4096 * H + 2 * H * T + 4 * T * 4096 + 4 * T * H
+    # token-blocked: one block's fp32 logits, D and D^T ((4 + 2 + 2) bytes per element of [block, V rounded to 256])
+    Vp = (V + 255) // 256 * 256
+    fb = lib.fused_lmhead_blocked_workspace_bytes(T, H, V, 8192, 64)
+    assert fb >= 2 * V * H + 2 * H * T + 8 * 8192 * Vp and fb % 256 == 0
+    assert fb < 2 * V * H + 2 * H * T + 8 * 8192 * Vp + (64 << 20)
+    # a block larger than the batch is cut to the batch (rounded up to 256 rows)
+    assert lib.fused_lmhead_blocked_workspace_bytes(300, H, V, 8192, 4) == \
+        lib.fused_lmhead_blocked_workspace_bytes(300, H, V, 512, 4)
+    for bad in (0, 300, -256):
+        assert lib.fused_lmhead_blocked_workspace_bytes(T, H, V, bad, 64) == 0
 
 
 D = ctypes.c_void_p(0x100000)  # a dummy, 256-byte aligned device address
@@ -134,14 +145,16 @@ def test_advantages_rejects_bad_arguments(lib):
     assert f(D, 0, 8, 1, 0.0, D, None) == _lib.GRPO_ERR_SHAPE
 
 
-def call_fused(lib, *, T=8, H=64, V=512, chunk=256, hidden=D, w=D, dh=D, dw=D, ws=D, ws_bytes=1 << 40):
+def call_fused(lib, *, blocked=False, T=8, H=64, V=512, chunk=256, hidden=D, w=D, dh=D, dw=D, ws=D,
+               ws_bytes=1 << 40):
     seg = _lib.Segments()
     seg.n_traj, seg.group_size, seg.n_steps = 4, 4, 4
     seg.step_tok_off, seg.traj_step_off = D, D
     p = _lib.LossParams()
     p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale = 1, 10.0, 0.2, 0.2, 0.0, 1.0
-    return lib.fused_lmhead_grpo(hidden, w, T, H, V, chunk, D, D, None, D, ctypes.byref(seg), ctypes.byref(p), D, dh,
-                                 dw, 0, None, ws, ws_bytes, None)
+    f = lib.fused_lmhead_grpo_blocked if blocked else lib.fused_lmhead_grpo
+    return f(hidden, w, T, H, V, chunk, D, D, None, D, ctypes.byref(seg), ctypes.byref(p), D, dh, dw, 0, None, ws,
+             ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -157,8 +170,14 @@ def call_fused(lib, *, T=8, H=64, V=512, chunk=256, hidden=D, w=D, dh=D, dw=D, w
     (dict(dh=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),
     (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
 ])
-def test_fused_rejects_bad_arguments(lib, kw, status):
-    assert call_fused(lib, **kw) == status
+@pytest.mark.parametrize("blocked", [False, True])
+def test_fused_rejects_bad_arguments(lib, kw, status, blocked):
+    # chunk: the vocabulary chunk, or for the token-blocked entry the token block (same rule: a multiple of 256)
+    assert call_fused(lib, blocked=blocked, **kw) == status
+
+
+def test_fused_blocked_rejects_oversized_block(lib):
+    assert call_fused(lib, blocked=True, chunk=1 << 23) == _lib.GRPO_ERR_SHAPE
 
 
 def call_logp(lib, *, logits=D, dt=_lib.GRPO_BF16, T=8, V=64, ld=64, actions=D):

@@ -1,4 +1,6 @@
-"""GPU parity of the fused LM-head path (fused_lmhead_grpo) against the fp64 oracle.
+"""GPU parity of the fused LM-head path against the fp64 oracle, in both schedules: over vocabulary chunks with
+the logits recomputed for the backward products (fused_lmhead_grpo), and over token blocks whose logits are kept
+between the products (fused_lmhead_grpo_blocked).
 
 Gates.  Loss: relative 1e-5.  Token log-probs: absolute 5e-5 (the logits are
 fp32 sums of H bf16 products on the GPU).  dhidden and dW: the GPU rounds each
@@ -49,11 +51,24 @@ def setup(b):
     return A64, A32, seg, sto, tso
 
 
+class Blocked(int):
+    """A schedule argument: the token-blocked entry point with this token_block (a plain int is a vocab_chunk)."""
+
+    def __repr__(self):
+        return f"blocked{int(self)}"
+
+
+def fused_call(b, A32, sto, tso, sched, **kw):
+    args = (b["hidden"], b["W"], b["actions"], b["behave"], A32, sto, tso, b["cfg"].G)
+    if isinstance(sched, Blocked):
+        return grpo.fused_lmhead_grpo_blocked(*args, token_block=int(sched), **kw)
+    return grpo.fused_lmhead_grpo(*args, vocab_chunk=sched, **kw)
+
+
 def run(b, A32, sto, tso, chunk, norm, c, gs=1.0, dw=None, accumulate=False):
     aux = grpo.LossAux.alloc(b["structure"].T, len(b["structure"].rewards), "cuda")
-    loss, dh, dW = grpo.fused_lmhead_grpo(b["hidden"], b["W"], b["actions"], b["behave"], A32, sto, tso, b["cfg"].G,
-                                          vocab_chunk=chunk, norm=gpu_norm(norm), k=b["cfg"].k, dual_clip_c=c,
-                                          grad_scale=gs, dw_lm=dw, accumulate_dw=accumulate, aux=aux)
+    loss, dh, dW = fused_call(b, A32, sto, tso, chunk, norm=gpu_norm(norm), k=b["cfg"].k, dual_clip_c=c,
+                              grad_scale=gs, dw_lm=dw, accumulate_dw=accumulate, aux=aux)
     torch.cuda.synchronize()
     return loss.item(), dh, dW, aux
 
@@ -104,36 +119,60 @@ def full_compare(b, chunk, norm, c, gs=1.0, accumulate=False):
 
 @pytest.mark.parametrize("norm", NORMS)
 @pytest.mark.parametrize("c", [0.0, 3.0])
-def test_fused_small(norm, c):
-    # H = 64, V = 1000, chunks of 256: four chunks, the last 232 wide; T not a multiple of 128
+@pytest.mark.parametrize("sched", [256, Blocked(256)])
+def test_fused_small(norm, c, sched):
+    # H = 64, V = 1000, chunks of 256: four chunks, the last 232 wide; T not a multiple of 128 (one token block)
     b = make_fused_batch(small_cfg(2, 4, 64, 1000, seed=11), "cuda")
     assert b["structure"].T % 128 != 0
-    full_compare(b, 256, norm, c)
+    full_compare(b, sched, norm, c)
 
 
-def test_fused_medium_multichunk_accumulate():
+@pytest.mark.parametrize("sched", [2048, Blocked(256)])
+def test_fused_medium_multichunk_accumulate(sched):
+    # blocked: several blocks of 256 tokens and a ragged last one, dW accumulated over them and onto the input
     b = make_fused_batch(small_cfg(4, 8, 256, 5000, seed=12, tok_mean=6.0, steps=(2, 9)), "cuda")
-    full_compare(b, 2048, oracle.NORM_TRAJ_STEPS, 3.0, gs=0.5, accumulate=True)
+    if isinstance(sched, Blocked):
+        assert b["structure"].T > 3 * 256 and b["structure"].T % 256 != 0
+    full_compare(b, sched, oracle.NORM_TRAJ_STEPS, 3.0, gs=0.5, accumulate=True)
 
 
-def test_fused_single_chunk():
+@pytest.mark.parametrize("sched", [1024, Blocked(512)])
+def test_fused_single_chunk(sched):
     b = make_fused_batch(small_cfg(1, 4, 128, 512, seed=13), "cuda")
-    full_compare(b, 1024, oracle.NORM_CONST_K, 0.0)
+    full_compare(b, sched, oracle.NORM_CONST_K, 0.0)
 
 
-def test_fused_full_hv_reduced_t():
-    # the real H = 3584 and V = 151,936 (18 full chunks of 8192 and a 4480 tail), with ~300 tokens
+@pytest.mark.parametrize("sched", [8192, Blocked(256)])
+def test_fused_full_hv_reduced_t(sched):
+    # the real H = 3584 and V = 151,936 (18 full chunks of 8192 and a 4480 tail), with ~300 tokens (two blocks)
     cfg = Config("fused-hv", 1, 8, 151936, "bf16", 0.0, 0.35, (8, 30), (3, 12), 96.0, (1, 4096), 0.05, 10.0,
                  T_target=320, H=3584, seed=14)
     b = make_fused_batch(cfg, "cuda")
-    full_compare(b, 8192, oracle.NORM_CONST_K, 3.0)
+    full_compare(b, sched, oracle.NORM_CONST_K, 3.0)
 
 
-def test_fused_full_size_sampled():
+def test_fused_schedules_agree():
+    # both schedules form the logits, their tile partials and the rows' epilogue with the same code on the same
+    # inputs: the loss and every per-token output are bit-identical; the backward products differ only in the
+    # order of their fp32 sums
+    b = make_fused_batch(small_cfg(4, 8, 256, 5000, seed=17, tok_mean=6.0, steps=(2, 9)), "cuda")
+    A64, A32, seg, sto, tso = setup(b)
+    l1, dh1, dW1, aux1 = run(b, A32, sto, tso, 1024, oracle.NORM_CONST_K, 3.0)
+    l2, dh2, dW2, aux2 = run(b, A32, sto, tso, Blocked(512), oracle.NORM_CONST_K, 3.0)
+    assert l1 == l2
+    for f in ("token_logp", "traj_loss", "clip_counts", "tok_traj", "error_flags"):
+        assert torch.equal(getattr(aux1, f), getattr(aux2, f)), f
+    dh1, dh2 = dh1.double(), dh2.double()
+    assert ((dh1 - dh2).abs() <= 2.0 ** -7 * dh1.abs() + 1e-3 * dh1.abs().max()).all()
+    assert (dW1.double() - dW2.double()).norm() <= 1e-5 * dW1.double().norm()
+
+
+@pytest.mark.parametrize("sched", [8192, Blocked(8192)])
+def test_fused_full_size_sampled(sched):
     b = make_fused_batch("fused", "cuda")
     A64, A32, seg, sto, tso = setup(b)
     cfg = b["cfg"]
-    loss, dh, dW, aux = run(b, A32, sto, tso, 8192, oracle.NORM_CONST_K, 3.0)
+    loss, dh, dW, aux = run(b, A32, sto, tso, sched, oracle.NORM_CONST_K, 3.0)
     T = b["structure"].T
     hb, Wb = bits(b["hidden"]), bits(b["W"])
     W64 = fused.as_f64(Wb)
@@ -168,25 +207,30 @@ def test_fused_full_size_sampled():
     assert aux.error_flags.item() == 0
 
 
-def test_fused_empty_batch_zeroes_dw():
+@pytest.mark.parametrize("blocked", [False, True])
+def test_fused_empty_batch_zeroes_dw(blocked):
     N, H, V = 4, 64, 256
     sto = torch.zeros(5, dtype=torch.int32, device="cuda")
     tso = torch.arange(0, 5, dtype=torch.int32, device="cuda")
     hidden = torch.empty((0, H), dtype=torch.bfloat16, device="cuda")
     W = torch.randn((H, V), device="cuda").to(torch.bfloat16)
     dw = torch.full((H, V), 7.0, device="cuda")
-    loss, dh, dW = grpo.fused_lmhead_grpo(hidden, W, torch.empty(0, dtype=torch.int32, device="cuda"),
-                                          torch.empty(0, device="cuda"), torch.zeros(N, device="cuda"), sto, tso, 4,
-                                          vocab_chunk=256, dw_lm=dw)
+    args = (hidden, W, torch.empty(0, dtype=torch.int32, device="cuda"), torch.empty(0, device="cuda"),
+            torch.zeros(N, device="cuda"), sto, tso, 4)
+    if blocked:
+        loss, dh, dW = grpo.fused_lmhead_grpo_blocked(*args, token_block=256, dw_lm=dw)
+    else:
+        loss, dh, dW = grpo.fused_lmhead_grpo(*args, vocab_chunk=256, dw_lm=dw)
     torch.cuda.synchronize()
     assert loss.item() == 0.0 and (dW == 0).all()
 
 
-def test_fused_invalid_action_row_zero():
+@pytest.mark.parametrize("sched", [256, Blocked(256)])
+def test_fused_invalid_action_row_zero(sched):
     b = make_fused_batch(small_cfg(2, 4, 64, 1000, seed=15), "cuda")
     b["actions"][2] = 1000
     A64, A32, seg, sto, tso = setup(b)
-    loss, dh, dW, aux = run(b, A32, sto, tso, 256, oracle.NORM_CONST_K, 0.0)
+    loss, dh, dW, aux = run(b, A32, sto, tso, sched, oracle.NORM_CONST_K, 0.0)
     assert aux.error_flags.item() == grpo.GRPO_FLAG_ACTION
     assert (dh[2] == 0).all()
     ref = fused.fused_loss(bits(b["hidden"]), bits(b["W"]), b["actions"].cpu().numpy(), b["behave"].cpu().numpy(),
@@ -200,4 +244,7 @@ def test_fused_rejects_bad_shapes():
     A64, A32, seg, sto, tso = setup(b)
     with pytest.raises(grpo.GrpoError) as e:
         run(b, A32, sto, tso, 300, oracle.NORM_CONST_K, 0.0)  # chunk not a multiple of 256
+    assert e.value.status == grpo._lib.GRPO_ERR_SHAPE
+    with pytest.raises(grpo.GrpoError) as e:
+        run(b, A32, sto, tso, Blocked(300), oracle.NORM_CONST_K, 0.0)  # token block not a multiple of 256
     assert e.value.status == grpo._lib.GRPO_ERR_SHAPE
