@@ -63,14 +63,16 @@ def fused_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_fused_traffic():
-    """HBM bytes per fused call from the committed counter summary, if it is current."""
+def measured_fused_traffic(schedule: str):
+    """HBM bytes per fused call of one schedule ("chunked" or "blocked") from the committed counter summary, if it
+    is current."""
     if not os.path.exists(FUSED_TRAFFIC_FILE):
         return None
     kv = dict(re.findall(r"^- (\w+): (\S+)", open(FUSED_TRAFFIC_FILE).read(), re.M))
-    if kv.get("kernel_source_sha256") != fused_source_hash():
+    key = f"traffic_bytes_per_call_{schedule}"
+    if kv.get("kernel_source_sha256") != fused_source_hash() or key not in kv:
         return None
-    return float(kv["traffic_bytes_per_call"])
+    return float(kv[key])
 
 
 def measured_traffic(T: int):
@@ -390,11 +392,11 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
     adv = torch.empty(N, dtype=torch.float32, device=dev)
     blocked = time_fused(b, adv, sto, tso, steps, warmup, token_block)
     chunked = time_fused(b, adv, sto, tso, steps, warmup, 0)
-    chunked["roofline"]["traffic"] = measured_fused_traffic()
+    chunked["roofline"]["traffic"] = measured_fused_traffic("chunked")
     out = dict(blocked)
     out["workload"] = (f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], {cfg.n_groups} groups x G={cfg.G}; "
                        f"{blocked['schedule']}")
-    out["roofline"] = dict(blocked["roofline"], traffic=None)
+    out["roofline"] = dict(blocked["roofline"], traffic=measured_fused_traffic("blocked"))
     out["vocab_chunked"] = chunked
     if shard_steps > 0:
         out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps)

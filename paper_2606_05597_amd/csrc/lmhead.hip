@@ -77,16 +77,34 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
   gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
   if constexpr (STORE_Z) {
-    // rows and columns past M and N hold zeros (their operand rows read as zero); each store instruction writes
-    // two 128-byte row pieces (lanes 0-31 and 32-63)
-    float* zt = p.z + (int64_t)m0 * p.ldz + n0;
+    // Rows and columns past M and N hold zeros (their operand rows read as zero).  Accumulators 4g..4g+3 of a
+    // lane are four consecutive rows of one column; a 4 x 4 transpose within each quad of lanes (two DPP
+    // exchanges: lanes x ^ 1, then x ^ 2) leaves lane 4a + x with row x of the group and columns 4a..4a+3, so
+    // each lane stores 16 bytes and one store instruction fills eight 128-byte row pieces.
+    const int x = lane & 3;
+    float* zt = p.z + (int64_t)m0 * p.ldz + n0 + wn * LmCfg::WTN + 4 * ((lane & 31) >> 2);
 #pragma unroll
     for (int i = 0; i < LmCfg::IB; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float* zr = zt + (int64_t)gemm_row<LmCfg>(wm, i, r, lane) * p.ldz + gemm_col<LmCfg>(wn, 0, lane);
+      for (int g = 0; g < 4; ++g) {
+        float* zr = zt + (int64_t)(wm * LmCfg::WTM + i * 32 + 8 * g + 4 * (lane >> 5) + x) * p.ldz;
 #pragma unroll
-        for (int j = 0; j < LmCfg::JB; ++j) __builtin_nontemporal_store(acc[i][j][r], zr + 32 * j);
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          float v[4], t[4], o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float q = dpp_f32<0xB1>(v[e ^ 1]);  // lane x ^ 1's accumulator e ^ 1
+            t[e] = ((e ^ x) & 1) ? q : v[e];
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float q = dpp_f32<0x4E>(t[e ^ 2]);  // lane x ^ 2's value e ^ 2
+            o[e] = ((e ^ x) & 2) ? q : t[e];
+          }
+          __builtin_nontemporal_store(f32x4{o[0], o[1], o[2], o[3]}, reinterpret_cast<f32x4*>(zr + 32 * j));
+        }
       }
   }
   // A 16-lane row of a wave holds 16 x JB columns of one output row: reduce them with

@@ -122,3 +122,36 @@ def test_fused_graph_replays():
         torch.cuda.synchronize()
         for x, y in zip(got, (loss, dh, dw)):
             assert torch.equal(x, y), f"replay {rep}"
+
+
+def test_fused_blocked_graph_replays():
+    # token blocks of 256 over ~600 tokens: several blocks, dW accumulated across them inside the graph
+    b = make_fused_batch(small_cfg(4, 8, 128, 2048, seed=32, tok_mean=6.0, steps=(2, 6)), "cuda")
+    st = b["structure"]
+    T, H, V = st.T, b["H"], b["V"]
+    assert T > 2 * 256
+    N = len(st.rewards)
+    sto = torch.from_numpy(st.step_tok_off).cuda()
+    tso = torch.from_numpy(st.traj_step_off).cuda()
+    adv = torch.from_numpy(oracle.advantages(st.rewards, b["cfg"].G).astype(np.float32)).cuda()
+    ws = torch.empty(grpo.fused_lmhead_blocked_workspace_bytes(T, H, V, 256, N), dtype=torch.uint8, device="cuda")
+    loss = torch.empty(1, dtype=torch.float64, device="cuda")
+    dh = torch.empty_like(b["hidden"])
+    dw = torch.empty((H, V), dtype=torch.float32, device="cuda")
+
+    def call():
+        grpo.fused_lmhead_grpo_blocked(b["hidden"], b["W"], b["actions"], b["behave"], adv, sto, tso, b["cfg"].G,
+                                       token_block=256, dual_clip_c=3.0, dhidden=dh, dw_lm=dw, workspace=ws,
+                                       loss_out=loss)
+
+    g = _capture(call)
+    for rep in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        got = (loss.clone(), dh.clone(), dw.clone())
+        dh.zero_()
+        dw.fill_(float("nan"))
+        call()
+        torch.cuda.synchronize()
+        for x, y in zip(got, (loss, dh, dw)):
+            assert torch.equal(x, y), f"replay {rep}"
