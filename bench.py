@@ -85,6 +85,10 @@ def measured_traffic(T: int):
     return float(kv["traffic_bytes_per_launch"])
 
 
+def fused_schedules(args):
+    return FUSED_SCHEDULES if args.fused_schedule == "all" else (args.fused_schedule,)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -98,6 +102,8 @@ def parse():
                     help="timed steps of one device's share of the vocabulary-parallel loss (0 = skip)")
     ap.add_argument("--skip-logits", action="store_true", help="measure only the fused path")
     ap.add_argument("--token-block", type=int, default=8192, help="token block of the blocked fused schedule")
+    ap.add_argument("--fused-schedule", choices=("all",) + FUSED_SCHEDULES, default="all",
+                    help="fused schedules to time (all: the three, two-stream token blocks first)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for counter calibration)")
     return ap.parse_args()
@@ -313,7 +319,8 @@ def fused_cpu_baseline(b: dict, rows: int = 64) -> dict:
                       f"to the whole batch)"}
 
 
-def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int = 0) -> dict:
+def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int = 0,
+               two_streams: bool = False) -> dict:
     """Times one schedule of the fused LM head on batch b: the vocabulary-chunked fused_lmhead_grpo (token_block 0)
     or the token-blocked fused_lmhead_grpo_blocked.  The hot region, timed with events the library records on its
     stream, is the first forward product through the last backward product."""
@@ -329,6 +336,8 @@ def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int
     if token_block:
         need = grpo.fused_lmhead_blocked_workspace_bytes(T, H, V, token_block, N)
         entry, kw = grpo.fused_lmhead_grpo_blocked, dict(token_block=token_block)
+        if two_streams:
+            kw["aux_stream"] = torch.cuda.Stream(device=dev)
     else:
         need = grpo.fused_lmhead_workspace_bytes(T, H, V, cfg.vocab_chunk, N)
         entry, kw = grpo.fused_lmhead_grpo, dict(vocab_chunk=cfg.vocab_chunk)
@@ -374,10 +383,14 @@ def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int
     return out
 
 
-def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = False,
-                token_block: int = 8192) -> dict:
-    """The fused workload in both schedules; the token-blocked one is the line's value, the vocabulary-chunked one
-    is reported beside it."""
+FUSED_SCHEDULES = ("blocked", "blocked1", "chunked")
+
+
+def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = False, token_block: int = 8192,
+                schedules=FUSED_SCHEDULES) -> dict:
+    """The fused workload in the chosen schedules: "blocked" (token blocks, each block's D pass on a second stream
+    beside the next block's forward product), "blocked1" (token blocks on one stream), "chunked" (vocabulary
+    chunks, logits recomputed).  The first one chosen is the line's value; the others are reported beside it."""
     import torch
 
     from synth import make_fused_batch
@@ -390,14 +403,25 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
     sto = torch.from_numpy(st.step_tok_off).to(dev)
     tso = torch.from_numpy(st.traj_step_off).to(dev)
     adv = torch.empty(N, dtype=torch.float32, device=dev)
-    blocked = time_fused(b, adv, sto, tso, steps, warmup, token_block)
-    chunked = time_fused(b, adv, sto, tso, steps, warmup, 0)
-    chunked["roofline"]["traffic"] = measured_fused_traffic("chunked")
-    out = dict(blocked)
+    res = {}
+    for sch in schedules:
+        if sch == "chunked":
+            r = time_fused(b, adv, sto, tso, steps, warmup, 0)
+            r["roofline"]["traffic"] = measured_fused_traffic("chunked")
+        else:
+            r = time_fused(b, adv, sto, tso, steps, warmup, token_block, two_streams=(sch == "blocked"))
+            r["roofline"]["traffic"] = measured_fused_traffic("blocked")
+            if sch == "blocked":
+                r["schedule"] += "; each block's D pass on a second stream beside the next block's forward product"
+        res[sch] = r
+    head = schedules[0]
+    out = dict(res[head])
     out["workload"] = (f"fused: hidden bf16 [{T}, {H}], W bf16 [{H}, {V}], {cfg.n_groups} groups x G={cfg.G}; "
-                       f"{blocked['schedule']}")
-    out["roofline"] = dict(blocked["roofline"], traffic=measured_fused_traffic("blocked"))
-    out["vocab_chunked"] = chunked
+                       f"{out['schedule']}")
+    names = {"blocked": "token_blocked_two_streams", "blocked1": "token_blocked_one_stream",
+             "chunked": "vocab_chunked"}
+    for sch in schedules[1:]:
+        out[names[sch]] = res[sch]
     if shard_steps > 0:
         out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps)
     if cpu:
@@ -484,7 +508,8 @@ def main():
         return
     if args.skip_logits:
         print(json.dumps({"fused_lmhead": bench_fused(max(1, args.fused_steps), shard_steps=args.shard_steps and 3,
-                                                          token_block=args.token_block)}),
+                                                          token_block=args.token_block,
+                                                          schedules=fused_schedules(args))}),
               flush=True)
         return
     import numpy as np
@@ -574,7 +599,8 @@ def main():
         del b
         torch.cuda.empty_cache()
         out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3,
-                                          cpu=args.cpu_seconds > 0, token_block=args.token_block)
+                                          cpu=args.cpu_seconds > 0, token_block=args.token_block,
+                                          schedules=fused_schedules(args))
     print(json.dumps(out), flush=True)
 
 

@@ -209,9 +209,10 @@ int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T, int64_t H
                       float* dw_lm, int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
                       hipStream_t s);
 
-/* Bytes of device workspace fused_lmhead_grpo_blocked needs: besides what fused_lmhead_grpo needs, one block's
- * fp32 logits and its D and D^T, (4 + 2 + 2) * min(token_block, T rounded up to 256) * (V rounded up to 256)
- * bytes (11.5 GB in all at T = 65,536, H = 3,584, V = 151,936, token_block = 8192).  0 for invalid sizes. */
+/* Bytes of device workspace fused_lmhead_grpo_blocked needs: besides W^T, h^T and the per-row scales, the fp32
+ * logits of two blocks (one when a single block covers T) and one block's D and D^T, (4 + 4 + 2 + 2) * B * Vp
+ * bytes with B = min(token_block, T rounded up to 256) and Vp = V rounded up to 256 (16.6 GB in all at
+ * T = 65,536, H = 3,584, V = 151,936, token_block = 8192).  0 for invalid sizes. */
 size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t token_block, int32_t n_traj);
 
 /*
@@ -219,18 +220,26 @@ size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int
  * with the same results up to the order of fp32 sums.  The forward product of a block of `token_block` rows
  * (z = h W, on the matrix cores, 256-column tiles) is kept in the workspace as fp32 until the block's rows have
  * their log-sum-exp; D of the block is then formed from the stored logits instead of a second product, so three
- * products run instead of four.  The logits of the whole batch are never stored: one block at a time.
+ * products run instead of four.  The logits of the whole batch are never stored: at most two blocks at a time.
  * Per block: dhidden rows = D W^T (the whole vocabulary as K, written once in bf16), dW (+)= h^T D.
  *   token_block  a positive multiple of 256, at most 8,388,352 (8192 is the tuned value)
  *   all other arguments as fused_lmhead_grpo
  *   ws, ws_bytes device workspace of at least fused_lmhead_blocked_workspace_bytes(...)
- * Errors: as fused_lmhead_grpo (GRPO_ERR_SHAPE for token_block outside the range above).
+ *   s_aux        NULL (or s): everything runs on s.  Otherwise a second stream of the caller's, on the same
+ *                device: each block's D pass (stored logits -> D, D^T) then runs on s_aux beside the next
+ *                block's forward product on s.  The call orders the two streams with two HIP events it creates
+ *                and releases itself; s_aux's work is joined back into s before the last launch on s, so the
+ *                results are complete in s's order, as with one stream (and the call can be captured from s
+ *                into a HIP graph).  The results are bit-identical either way.
+ * Errors: as fused_lmhead_grpo (GRPO_ERR_SHAPE for token_block outside the range above); GRPO_ERR_HIP if an
+ *   event cannot be created.
  */
 int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V,
                               int32_t token_block, const int32_t* actions, const float* behave_logp,
                               const float* prox_logp, const float* adv, const grpo_segments* seg,
                               const grpo_loss_params* p, double* loss_out, void* dhidden, float* dw_lm,
-                              int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
+                              int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s,
+                              hipStream_t s_aux);
 
 /*
  * Forward only: the sampled action's log-prob and the policy entropy of each

@@ -221,7 +221,7 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
 
 def _fused_call(entry: str, ws_bytes, hidden, w_lm, actions, behave_logp, adv, step_tok_off, traj_step_off,
                 group_size, sched, prox_logp, norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total,
-                dhidden, dw_lm, accumulate_dw, aux, workspace, loss_out, stream):
+                dhidden, dw_lm, accumulate_dw, aux, workspace, loss_out, stream, extra=()):
     _dev(hidden, "hidden")
     _dev(w_lm, "w_lm")
     if hidden.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
@@ -249,7 +249,7 @@ def _fused_call(entry: str, ws_bytes, hidden, w_lm, actions, behave_logp, adv, s
         _ptr(hidden), _ptr(w_lm), T, H, V, int(sched), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
         _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
         _ptr(loss_out), _ptr(dhidden), _ptr(dw_lm), int(bool(accumulate_dw)),
-        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream), *extra)
     _check(st, entry)
     return loss_out, dhidden, dw_lm
 
@@ -282,16 +282,19 @@ def fused_lmhead_grpo_blocked(hidden: torch.Tensor, w_lm: torch.Tensor, actions:
                               dhidden: torch.Tensor | None = None, dw_lm: torch.Tensor | None = None,
                               accumulate_dw: bool = False, aux: LossAux | None = None,
                               workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None,
-                              stream=None):
+                              stream=None, aux_stream=None):
     """As fused_lmhead_grpo, over blocks of `token_block` tokens whose fp32 logits are kept in the workspace
-    between the forward and backward products (three products instead of four).
+    between the forward and backward products (three products instead of four).  With `aux_stream` (a second
+    torch.cuda.Stream on the same device), each block's D pass runs on it beside the next block's forward
+    product; the results are complete in `stream`'s order either way.
 
     Returns (loss [1] fp64, dhidden, dw_lm).
     """
     return _fused_call("fused_lmhead_grpo_blocked", fused_lmhead_blocked_workspace_bytes, hidden, w_lm, actions,
                        behave_logp, adv, step_tok_off, traj_step_off, group_size, token_block, prox_logp, norm, k,
                        eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total, dhidden, dw_lm, accumulate_dw,
-                       aux, workspace, loss_out, stream)
+                       aux, workspace, loss_out, stream,
+                       extra=(None if aux_stream is None else ctypes.c_void_p(aux_stream.cuda_stream),))
 
 
 def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | None = None, entropy: bool = True,

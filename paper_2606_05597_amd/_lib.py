@@ -79,7 +79,7 @@ def load() -> ctypes.CDLL:
         lib.fused_lmhead_grpo.restype = ctypes.c_int
         lib.fused_lmhead_blocked_workspace_bytes.argtypes = [I64, I64, I64, I32, I32]
         lib.fused_lmhead_blocked_workspace_bytes.restype = SZ
-        lib.fused_lmhead_grpo_blocked.argtypes = lib.fused_lmhead_grpo.argtypes
+        lib.fused_lmhead_grpo_blocked.argtypes = lib.fused_lmhead_grpo.argtypes + [P]
         lib.fused_lmhead_grpo_blocked.restype = ctypes.c_int
         lib.grpo_token_logp.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P, P]
         lib.grpo_token_logp.restype = ctypes.c_int

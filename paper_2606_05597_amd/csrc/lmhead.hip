@@ -12,10 +12,20 @@
 //           after every second chunk (and the last), in one launch:
 //             dW[:, c-1..c] = h^T [D_c-1 D_c]
 //             dhidden += [D_c-1 D_c] [W_c-1 W_c]^T   (fp32 accumulator, bf16 at the end)
+// The token-blocked schedule (fused_lmhead_grpo_blocked) takes rows in blocks
+// instead and keeps a block's logits, so the forward product is not recomputed:
+//   per block of B rows:
+//     z = h_block W  -> tile partials and the fp32 logits of the block (HBM)
+//     rows           combine, as above
+//     D pass         stored logits -> D, D^T (bf16), a streaming pass
+//     one launch     dhidden rows = D W^T (K = V, written once), then
+//                    dW (+)= h_block^T D (K = B)
+//   With a second stream, block b's D pass runs beside block b + 1's forward
+//   product (one D-pass workgroup per CU next to the product's workgroup).
 // Every product is one GEMM core (gemm.h) with both operands K-contiguous
 // (C[m, n] = sum_k A[m, k] B[n, k]); W and h are transposed once so that this
-// holds for all four.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16, slabs
-// loaded straight into LDS.
+// holds for all of them.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16,
+// slabs loaded straight into LDS.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -526,70 +536,68 @@ struct BlockDArgs {
 };
 constexpr int kBlockDStrip = 512;  // columns per workgroup: eight 64 x 64 tiles
 
-// 256 threads, 64 rows (blockIdx.x), a strip of up to eight 64-column tiles (blockIdx.y).  Per tile a thread takes two 2 x 4 pieces (rows
-// 2p, 2p + 1 of four columns, p = tid / 16 and p + 16): two 16-byte logit loads each; the D rows go out as 8-byte
-// stores (16 lanes fill a 128-byte line); for D^T every column's row pair is packed into one 32-bit LDS word
-// (stride 33 words per column: the stores are conflict-free and the reads two-way), read back as four words =
-// eight rows, and stored 16 bytes at a time (8 lanes per 128-byte column piece).  Two LDS buffers, one barrier
-// per tile.
+// Work items of 64 rows and a strip of up to eight 64-column tiles, item i = strip * (rows / 64) + row tile; a
+// workgroup of 256 threads takes items blockIdx.x, blockIdx.x + gridDim.x, ... (one each with a full grid; a
+// grid of one workgroup per CU when the pass runs beside a matrix-core launch).  Per tile a thread takes two
+// 2 x 4 pieces (rows 2p, 2p + 1 of four columns, p = tid / 16 and p + 16): two 16-byte logit loads each; the D
+// rows go out as 8-byte stores (16 lanes fill a 128-byte line); for D^T every column's row pair is packed into
+// one 32-bit LDS word (stride 33 words per column), read back as four words = eight rows, and stored 16 bytes
+// at a time (8 lanes per 128-byte column piece).  Two LDS buffers, one barrier per tile.
 __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
   constexpr int kLdw = 33;
   __shared__ uint32_t tu[2][64 * kLdw];
   __shared__ RowScale srs[64];
   const int tid = threadIdx.x;
-  const int r0 = blockIdx.x * 64;
-  const int64_t cs = (int64_t)blockIdx.y * kBlockDStrip;
-  if (tid < 64) srs[tid] = a.rs[r0 + tid];
-  __syncthreads();
-  const int cq = tid & 15, rp = tid >> 4;
-  RowScale rs[4];  // rows 2 rp, 2 rp + 1, 2 rp + 32, 2 rp + 33
-#pragma unroll
-  for (int k = 0; k < 4; ++k) rs[k] = srs[2 * rp + (k & 1) + 32 * (k >> 1)];
-  const int ntiles = (int)min((int64_t)(kBlockDStrip / 64), (a.ld - cs) / 64);
-  for (int it = 0; it < ntiles; ++it) {
-    const int64_t c = cs + it * 64 + 4 * cq;
-    f32x4 x[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int row = 2 * rp + (k & 1) + 32 * (k >> 1);
-      x[k] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(a.z + (int64_t)(r0 + row) * a.ld + c));
-    }
-    uint32_t w[4][2];  // packed bf16 pairs: row k, columns (0, 1) and (2, 3)
-    uint16_t d16[4][4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float xv[4] = {x[k][0], x[k][1], x[k][2], x[k][3]};
-      float d[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t v = c + e;
-        d[e] = v >= a.V ? 0.f
-             : (v == rs[k].act) ? rs[k].d_a
-                                : rs[k].sign * __builtin_amdgcn_exp2f(fmaf(xv[e], kLog2e, rs[k].nc));
-      }
-      w[k][0] = pack_bf16(d[0], d[1]);
-      w[k][1] = pack_bf16(d[2], d[3]);
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        d16[k][2 * e] = (uint16_t)(w[k][e] & 0xffffu);
-        d16[k][2 * e + 1] = (uint16_t)(w[k][e] >> 16);
-      }
-      const int row = 2 * rp + (k & 1) + 32 * (k >> 1);
-      *reinterpret_cast<u32x2*>(a.D + (int64_t)(r0 + row) * a.ld + c) = u32x2{w[k][0], w[k][1]};
-    }
-    uint32_t* t = tu[it & 1];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        t[(4 * cq + e) * kLdw + rp + 16 * u] = (uint32_t)d16[2 * u][e] | ((uint32_t)d16[2 * u + 1][e] << 16);
+  const int n_rt = a.rows / 64;
+  const int n_items = n_rt * (int)((a.ld + kBlockDStrip - 1) / kBlockDStrip);
+  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int r0 = (item % n_rt) * 64;
+    const int64_t cs = (int64_t)(item / n_rt) * kBlockDStrip;
+    __syncthreads();  // the previous item's last reads of tu and srs are done
+    if (tid < 64) srs[tid] = a.rs[r0 + tid];
     __syncthreads();
+    const int cq = tid & 15, rp = tid >> 4;
+    RowScale rs[4];  // rows 2 rp, 2 rp + 1, 2 rp + 32, 2 rp + 33
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int col = (tid >> 3) + 32 * q, rc = tid & 7;
-      const uint32_t* src = t + col * kLdw + 4 * rc;
-      const u32x4 v = {src[0], src[1], src[2], src[3]};
-      *reinterpret_cast<u32x4*>(a.DT + (cs + it * 64 + col) * a.rows + r0 + 8 * rc) = v;
+    for (int k = 0; k < 4; ++k) rs[k] = srs[2 * rp + (k & 1) + 32 * (k >> 1)];
+    const int ntiles = (int)min((int64_t)(kBlockDStrip / 64), (a.ld - cs) / 64);
+    for (int it = 0; it < ntiles; ++it) {
+      const int64_t c = cs + it * 64 + 4 * cq;
+      uint32_t* t = tu[it & 1];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {  // rows 2 rp + 32 u and the next one
+        const int row = 2 * rp + 32 * u;
+        const float* zr = a.z + (int64_t)(r0 + row) * a.ld + c;
+        const f32x4 x0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr));
+        const f32x4 x1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + a.ld));
+        float d0[4], d1[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t v = c + e;
+          const RowScale& s0 = rs[2 * u];
+          const RowScale& s1 = rs[2 * u + 1];
+          d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : s0.sign * __builtin_amdgcn_exp2f(fmaf(x0[e], kLog2e, s0.nc));
+          d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : s1.sign * __builtin_amdgcn_exp2f(fmaf(x1[e], kLog2e, s1.nc));
+        }
+        const uint32_t p00 = pack_bf16(d0[0], d0[1]), p01 = pack_bf16(d0[2], d0[3]);
+        const uint32_t p10 = pack_bf16(d1[0], d1[1]), p11 = pack_bf16(d1[2], d1[3]);
+        *reinterpret_cast<u32x2*>(a.D + (int64_t)(r0 + row) * a.ld + c) = u32x2{p00, p01};
+        *reinterpret_cast<u32x2*>(a.D + (int64_t)(r0 + row + 1) * a.ld + c) = u32x2{p10, p11};
+        // column e's word: row `row` in the low half, row + 1 in the high half
+        uint32_t* tw = t + 4 * cq * kLdw + rp + 16 * u;
+        tw[0 * kLdw] = (p00 & 0xffffu) | (p10 << 16);
+        tw[1 * kLdw] = (p00 >> 16) | (p10 & 0xffff0000u);
+        tw[2 * kLdw] = (p01 & 0xffffu) | (p11 << 16);
+        tw[3 * kLdw] = (p01 >> 16) | (p11 & 0xffff0000u);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int col = (tid >> 3) + 32 * q, rc = tid & 7;
+        const uint32_t* src = t + col * kLdw + 4 * rc;
+        const u32x4 v = {src[0], src[1], src[2], src[3]};
+        *reinterpret_cast<u32x4*>(a.DT + (cs + it * 64 + col) * a.rows + r0 + 8 * rc) = v;
+      }
     }
   }
 }
@@ -735,7 +743,8 @@ static void lm_pass2(const Pass2& q, hipStream_t s) {
   }
 }
 
-// The token-blocked schedule's workspace: one block of rows at a time keeps its fp32 logits and its D, D^T.
+// The token-blocked schedule's workspace: the fp32 logits of two blocks (the next block's forward product runs
+// while the D pass reads the previous block's when a second stream is given), the D and D^T of one block.
 struct LmBlockWs {
   LossWs loss;
   size_t wt, ht, part, rs, z, d, dt, total;
@@ -754,7 +763,7 @@ static LmBlockWs lm_block_ws_layout(int64_t T, int64_t H, int64_t V, int32_t Tb,
   l.ht = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(H * l.Tp));
   l.part = o; o = align_up(o + sizeof(float2) * (size_t)(l.Tbp * l.n_tiles));
   l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
-  l.z = o;    o = align_up(o + sizeof(float) * (size_t)(l.Tbp * l.ldz));
+  l.z = o;    o = align_up(o + sizeof(float) * (size_t)(l.Tbp * l.ldz) * (l.Tp > l.Tbp ? 2 : 1));
   l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tbp * l.ldz));
   l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.ldz * l.Tbp));
   l.total = o;
@@ -868,7 +877,7 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
                                          const float* prox_logp, const float* adv, const grpo_segments* seg,
                                          const grpo_loss_params* p, double* loss_out, void* dhidden, float* dw_lm,
                                          int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
-                                         hipStream_t s) {
+                                         hipStream_t s, hipStream_t s_aux) {
   int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
   if (st != GRPO_OK) return st;
   if (!w_lm || !dw_lm || (T > 0 && (!hidden || !dhidden))) return GRPO_ERR_ARG;
@@ -905,18 +914,20 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   const bool timed = aux && aux->hot_begin && aux->hot_end;
   if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
   const TokenArgs tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
-  for (int64_t t0 = 0; t0 < T; t0 += L.Tbp) {
-    const int rows = (int)(T - t0 < L.Tbp ? T - t0 : L.Tbp);  // the block's tokens
-    const int rows_p = (rows + TILE - 1) / TILE * TILE;
-    // forward product of the block: partials and the stored logits
+  const int n_blocks = (int)((T + L.Tbp - 1) / L.Tbp);
+  auto rows_of = [&](int b) { return (int)(T - (int64_t)b * L.Tbp < L.Tbp ? T - (int64_t)b * L.Tbp : L.Tbp); };
+  auto z_of = [&](int b) { return z + (size_t)(b & 1) * (size_t)(L.Tbp * L.ldz); };
+  // block b's forward product (partials, logits into its buffer) and its rows' combine, on s
+  auto forward = [&](int b) {
+    const int64_t t0 = (int64_t)b * L.Tbp;
+    const int rows = rows_of(b), rows_p = (rows + TILE - 1) / TILE * TILE;
     PartialArgs pa;
     pa.g = GemmArgs{h16 + t0 * H, WT, H, H, rows, (int)V, (int)H};
     pa.part = part;
     pa.n_tiles = L.n_tiles;
-    pa.z = z;
+    pa.z = z_of(b);
     pa.ldz = L.ldz;
     hipLaunchKernelGGL(k_lm_partial<true>, gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
-    // the block's rows: lse, action logit, token epilogue, row scale
     CombineArgs ca;
     ca.tok = tok;
     ca.part = part;
@@ -928,11 +939,18 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     ca.n_tiles = L.n_tiles;
     ca.t0 = (int)t0;
     hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)rows_p), dim3(256), 0, s, ca);
-    // D and D^T of the block
-    BlockDArgs da{z, rs + t0, D, DT, L.ldz, (int)V, rows_p};
-    hipLaunchKernelGGL(k_lm_block_d, dim3((unsigned)(rows_p / 64), (unsigned)((L.ldz + kBlockDStrip - 1) / kBlockDStrip)),
-                       dim3(256), 0, s, da);
-    // dhidden rows of the block = D W^T (K = V); dW (+)= h^T D (K = the block's rows, zero-padded)
+  };
+  // block b's D and D^T from its stored logits; `grid` workgroups (0: one per work item)
+  auto dpass = [&](int b, hipStream_t st, int grid) {
+    const int rows_p = (rows_of(b) + TILE - 1) / TILE * TILE;
+    const BlockDArgs da{z_of(b), rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V, rows_p};
+    const int items = rows_p / 64 * (int)((L.ldz + kBlockDStrip - 1) / kBlockDStrip);
+    hipLaunchKernelGGL(k_lm_block_d, dim3((unsigned)(grid > 0 && grid < items ? grid : items)), dim3(256), 0, st, da);
+  };
+  // block b's dhidden rows = D W^T (K = V) and dW (+)= h^T D (K = the block's rows, zero-padded), on s
+  auto backward = [&](int b) {
+    const int64_t t0 = (int64_t)b * L.Tbp;
+    const int rows = rows_of(b), rows_p = (rows + TILE - 1) / TILE * TILE;
     DhThenDwArgs ba;
     ba.dh.g = GemmArgs{D, W16, L.ldz, V, rows, (int)H, (int)V};
     ba.dh.acc = nullptr;
@@ -943,10 +961,57 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     ba.dw.dw = dw_lm;
     ba.dw.V = V;
     ba.dw.c0 = 0;
-    ba.dw.accumulate = (t0 > 0 || accumulate_dw) ? 1 : 0;
+    ba.dw.accumulate = (b > 0 || accumulate_dw) ? 1 : 0;
     ba.dh_blocks = (int)gemm_grid(rows, H).x;
     hipLaunchKernelGGL(k_lm_dh_then_dw, dim3((unsigned)ba.dh_blocks + gemm_grid(H, V).x), dim3(LmCfg::NT), 0, s, ba);
-    if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+  };
+  const bool two = s_aux && s_aux != s && n_blocks > 1;
+  if (!two) {
+    for (int b = 0; b < n_blocks; ++b) {
+      forward(b);
+      dpass(b, s, 0);
+      backward(b);
+      if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
+    }
+  } else {
+    // The D pass of block b runs on s_aux beside the forward product of block b + 1 on s, as one workgroup per
+    // CU, so that each CU holds one of each: the forward product's workgroup leaves room in LDS and registers
+    // for one D-pass workgroup.  ev_c: block b's rows are combined and the previous backward launch (the last
+    // reader of D, D^T) is done; ev_d: block b's D pass is done.
+    int dev = 0, n_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return GRPO_ERR_HIP;
+    hipEvent_t ev_c = nullptr, ev_d = nullptr;
+    if (hipEventCreateWithFlags(&ev_c, hipEventDisableTiming) != hipSuccess) return GRPO_ERR_HIP;
+    if (hipEventCreateWithFlags(&ev_d, hipEventDisableTiming) != hipSuccess) {
+      hipEventDestroy(ev_c);
+      return GRPO_ERR_HIP;
+    }
+    bool ok = true;
+    forward(0);
+    ok = ok && hipEventRecord(ev_c, s) == hipSuccess && hipStreamWaitEvent(s_aux, ev_c, 0) == hipSuccess;
+    dpass(0, s_aux, n_cu);
+    ok = ok && hipEventRecord(ev_d, s_aux) == hipSuccess;
+    for (int b = 1; ok && b < n_blocks; ++b) {
+      forward(b);
+      ok = ok && hipStreamWaitEvent(s, ev_d, 0) == hipSuccess;
+      backward(b - 1);
+      if (b == n_blocks - 1) break;
+      ok = ok && hipEventRecord(ev_c, s) == hipSuccess && hipStreamWaitEvent(s_aux, ev_c, 0) == hipSuccess;
+      dpass(b, s_aux, n_cu);
+      ok = ok && hipEventRecord(ev_d, s_aux) == hipSuccess && hipGetLastError() == hipSuccess;
+    }
+    // the last block's D pass has no forward product to run beside: the whole grid, on s
+    if (ok) {
+      dpass(n_blocks - 1, s, 0);
+      backward(n_blocks - 1);
+    }
+    ok = ok && hipGetLastError() == hipSuccess;
+    // released by the runtime once the work that uses them has run
+    hipEventDestroy(ev_c);
+    hipEventDestroy(ev_d);
+    if (!ok) return GRPO_ERR_HIP;
   }
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   if (launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;

@@ -69,11 +69,15 @@ def test_workspace_queries(lib):
     assert f >= 2 * V * H + 2 * H * T + 2 * 2 * T * C + 4 * T * H and f % 256 == 0
     # a single chunk needs no dhidden accumulator
     assert lib.fused_lmhead_workspace_bytes(T, H, 4096, 4096, 64) < 2 * 4096 * H + 2 * H * T + 4 * T * 4096 + 4 * T * H
-    # token-blocked: one block's fp32 logits, D and D^T ((4 + 2 + 2) bytes per element of [block, V rounded to 256])
+    # token-blocked: two blocks' fp32 logits, one block's D and D^T ((4 + 4 + 2 + 2) bytes per element of
+    # [block, V rounded to 256])
     Vp = (V + 255) // 256 * 256
     fb = lib.fused_lmhead_blocked_workspace_bytes(T, H, V, 8192, 64)
-    assert fb >= 2 * V * H + 2 * H * T + 8 * 8192 * Vp and fb % 256 == 0
-    assert fb < 2 * V * H + 2 * H * T + 8 * 8192 * Vp + (64 << 20)
+    assert fb >= 2 * V * H + 2 * H * T + 12 * 8192 * Vp and fb % 256 == 0
+    assert fb < 2 * V * H + 2 * H * T + 12 * 8192 * Vp + (64 << 20)
+    # one block covering T needs one logits buffer
+    one = lib.fused_lmhead_blocked_workspace_bytes(8192, H, V, 8192, 64)
+    assert one < 2 * V * H + 2 * H * 8192 + 8 * 8192 * Vp + (64 << 20)
     # a block larger than the batch is cut to the batch (rounded up to 256 rows)
     assert lib.fused_lmhead_blocked_workspace_bytes(300, H, V, 8192, 4) == \
         lib.fused_lmhead_blocked_workspace_bytes(300, H, V, 512, 4)
@@ -152,9 +156,9 @@ def call_fused(lib, *, blocked=False, T=8, H=64, V=512, chunk=256, hidden=D, w=D
     seg.step_tok_off, seg.traj_step_off = D, D
     p = _lib.LossParams()
     p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale = 1, 10.0, 0.2, 0.2, 0.0, 1.0
-    f = lib.fused_lmhead_grpo_blocked if blocked else lib.fused_lmhead_grpo
-    return f(hidden, w, T, H, V, chunk, D, D, None, D, ctypes.byref(seg), ctypes.byref(p), D, dh, dw, 0, None, ws,
-             ws_bytes, None)
+    args = (hidden, w, T, H, V, chunk, D, D, None, D, ctypes.byref(seg), ctypes.byref(p), D, dh, dw, 0, None, ws,
+            ws_bytes, None)
+    return lib.fused_lmhead_grpo_blocked(*args, None) if blocked else lib.fused_lmhead_grpo(*args)
 
 
 @pytest.mark.parametrize("kw,status", [

@@ -167,6 +167,30 @@ def test_fused_schedules_agree():
     assert (dW1.double() - dW2.double()).norm() <= 1e-5 * dW1.double().norm()
 
 
+@pytest.mark.parametrize("tb,cfg_args", [(256, (4, 8, 256, 5000, 18)), (8192, None)])
+def test_fused_blocked_two_streams_bit_identical(tb, cfg_args):
+    # each block's D pass on a second stream beside the next block's forward product: the same kernels on the
+    # same data in a different overlap, so every output is bit-identical to the one-stream call (several blocks
+    # of 256 rows on a small batch; the full fused workload in 8 blocks of 8192)
+    if cfg_args is None:
+        b = make_fused_batch("fused", "cuda")
+    else:
+        b = make_fused_batch(small_cfg(*cfg_args[:4], seed=cfg_args[4], tok_mean=6.0, steps=(2, 9)), "cuda")
+    A64, A32, seg, sto, tso = setup(b)
+    T, N = b["structure"].T, len(b["structure"].rewards)
+    assert T > 2 * tb
+    outs = []
+    for two in (False, True):
+        aux = grpo.LossAux.alloc(T, N, "cuda")
+        side = torch.cuda.Stream() if two else None
+        loss, dh, dW = fused_call(b, A32, sto, tso, Blocked(tb), norm=gpu_norm(oracle.NORM_CONST_K), k=b["cfg"].k,
+                                  dual_clip_c=3.0, aux=aux, aux_stream=side)
+        torch.cuda.synchronize()
+        outs.append((loss, dh, dW, aux.token_logp, aux.traj_loss, aux.clip_counts, aux.error_flags))
+    for x, y in zip(*outs):
+        assert torch.equal(x, y)
+
+
 @pytest.mark.parametrize("sched", [8192, Blocked(8192)])
 def test_fused_full_size_sampled(sched):
     b = make_fused_batch("fused", "cuda")

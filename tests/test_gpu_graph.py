@@ -124,8 +124,10 @@ def test_fused_graph_replays():
             assert torch.equal(x, y), f"replay {rep}"
 
 
-def test_fused_blocked_graph_replays():
-    # token blocks of 256 over ~600 tokens: several blocks, dW accumulated across them inside the graph
+@pytest.mark.parametrize("two_streams", [False, True])
+def test_fused_blocked_graph_replays(two_streams):
+    # token blocks of 256 over ~600 tokens: several blocks, dW accumulated across them inside the graph; with a
+    # second stream the capture forks onto it and joins back through the call's events
     b = make_fused_batch(small_cfg(4, 8, 128, 2048, seed=32, tok_mean=6.0, steps=(2, 6)), "cuda")
     st = b["structure"]
     T, H, V = st.T, b["H"], b["V"]
@@ -138,11 +140,12 @@ def test_fused_blocked_graph_replays():
     loss = torch.empty(1, dtype=torch.float64, device="cuda")
     dh = torch.empty_like(b["hidden"])
     dw = torch.empty((H, V), dtype=torch.float32, device="cuda")
+    side = torch.cuda.Stream() if two_streams else None
 
     def call():
         grpo.fused_lmhead_grpo_blocked(b["hidden"], b["W"], b["actions"], b["behave"], adv, sto, tso, b["cfg"].G,
                                        token_block=256, dual_clip_c=3.0, dhidden=dh, dw_lm=dw, workspace=ws,
-                                       loss_out=loss)
+                                       loss_out=loss, aux_stream=side)
 
     g = _capture(call)
     for rep in range(3):
