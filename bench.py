@@ -423,15 +423,19 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
     for sch in schedules[1:]:
         out[names[sch]] = res[sch]
     if shard_steps > 0:
-        out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps)
+        out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps, keep=True)
+        out["vocab_shard"]["recompute"] = bench_fused_shard(b, adv, sto, tso, shard_steps, keep=False)
     if cpu:
         out["cpu_baseline"] = fused_cpu_baseline(b)
     return out
 
 
-def bench_fused_shard(b: dict, adv, sto, tso, steps: int, n_shards: int = 8, warmup: int = 1) -> dict:
+def bench_fused_shard(b: dict, adv, sto, tso, steps: int, n_shards: int = 8, warmup: int = 1,
+                      keep: bool = True) -> dict:
     """One device's share of the vocabulary-parallel fused LM head on the fused workload: W's columns split n_shards
-    ways, the first shard's statistics call and backward call timed, every shard's records gathered beforehand."""
+    ways, the first shard's statistics call and backward call timed, every shard's records gathered beforehand.
+    keep: the statistics call keeps the shard's logits and the backward call uses them (three products in the two
+    calls); otherwise the backward call forms them again (four)."""
     import torch
 
     import paper_2606_05597_amd as grpo
@@ -450,6 +454,9 @@ def bench_fused_shard(b: dict, adv, sto, tso, steps: int, n_shards: int = 8, war
     dws = torch.empty((H, Vs), dtype=torch.float32, device=dev)
     ws1 = torch.empty(grpo._lib.load().fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs), dtype=torch.uint8,
                       device=dev)
+    kept = grpo.vocab_shard_logits_buffer(T, Vs, dev) if keep else None
+    if keep:
+        chunk = (Vs + 255) // 256 * 256  # the whole shard as one chunk
     ws2 = torch.empty(grpo.fused_lmhead_workspace_bytes(T, H, Vs, chunk, N), dtype=torch.uint8, device=dev)
     loss = torch.empty(1, dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream()
@@ -462,14 +469,15 @@ def bench_fused_shard(b: dict, adv, sto, tso, steps: int, n_shards: int = 8, war
     def step(i=None):
         if i is not None:
             es[i][0].record(stream)
-        grpo.fused_lmhead_vocab_shard_stats(b["hidden"], w, b["actions"], 0, stats=stats[0], workspace=ws1)
+        grpo.fused_lmhead_vocab_shard_stats(b["hidden"], w, b["actions"], 0, stats=stats[0], workspace=ws1,
+                                            logits_out=kept)
         if i is not None:
             es[i][1].record(stream)
             eb[i][0].record(stream)
         grpo.fused_lmhead_grpo_vocab_shard(b["hidden"], w, stats, 0, V, b["actions"], b["behave"], adv, sto, tso,
                                            cfg.G, vocab_chunk=chunk, norm=grpo.GRPO_NORM_CONST_K, k=cfg.k,
                                            dual_clip_c=3.0, dhidden_partial=dhp, dw_shard=dws, workspace=ws2,
-                                           loss_out=loss)
+                                           loss_out=loss, logits_in=kept)
         if i is not None:
             eb[i][1].record(stream)
 
@@ -485,15 +493,18 @@ def bench_fused_shard(b: dict, adv, sto, tso, steps: int, n_shards: int = 8, war
     bwd_ms = sum(a.elapsed_time(c) for a, c in eb) / steps
     alg = 6.0 * T * H * Vs
     achieved = alg / ((stats_ms + bwd_ms) * 1e-3) / 1e12
+    how = ("the statistics call keeps the shard's fp32 logits, the backward call forms D from them"
+           if keep else f"the backward call forms the logits again in chunks of {chunk}")
+    products = 3 if keep else 4
     return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
             "workload": f"one device's share of the fused LM head with W's {V} columns split {n_shards} ways: "
-                        f"hidden bf16 [{T}, {H}], W shard bf16 [{H}, {Vs}], chunks of {chunk}; statistics call + "
-                        f"backward call (records of all {n_shards} shards gathered beforehand)",
+                        f"hidden bf16 [{T}, {H}], W shard bf16 [{H}, {Vs}]; statistics call + backward call "
+                        f"(records of all {n_shards} shards gathered beforehand); {how}",
             "loss": float(loss.item()), "stats_ms": stats_ms, "backward_ms": bwd_ms,
             "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
                          "algorithmic_flop_per_launch": alg,
-                         "executed_frac": (8.0 * T * H * Vs) / ((stats_ms + bwd_ms) * 1e-3) / 1e12
+                         "executed_frac": (2.0 * products * T * H * Vs) / ((stats_ms + bwd_ms) * 1e-3) / 1e12
                          / MFMA_BF16_PEAK_TFLOPS}}
 
 

@@ -336,19 +336,27 @@ size_t fused_lmhead_vocab_shard_stats_workspace_bytes(int64_t T, int64_t H, int6
  * Step 1 of the sharded fused LM head: the device holding W's columns
  * [v_begin, v_begin + V_shard) reduces every row of z = h W_shard to its
  * grpo_vocab_stats record (m and s from the matrix-core logits; z_a = h_t .
- * W[:, a_t] in fp64, rounded to fp32, when a_t is one of the shard's columns).
+ * W[:, a_t] in fp64 when a_t is one of the shard's columns).
  *   hidden       device bf16 [T, H] row-major       w_shard device bf16 [H, V_shard] row-major
  *   T >= 0, H >= 64 and a multiple of 64, V_shard >= 8 and a multiple of 8,
  *   v_begin >= 0, v_begin + V_shard < 2^31
  *   actions      device int32 [T]  global token ids
  *   stats        device grpo_vocab_stats [T] (written)
+ *   logits_out   NULL, or device fp32 [Tp, Vsp] (Tp = T and Vsp = V_shard rounded up to 256, row stride Vsp;
+ *                fused_lmhead_vocab_shard_logits_bytes(T, V_shard) bytes, caller-owned): written with the
+ *                shard's logits z = h W_shard as the matrix cores formed them (zeros past T and V_shard), for
+ *                step 2 to use instead of forming them again
  *   ws, ws_bytes device workspace of at least fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, V_shard)
- * hidden and w_shard must be 16-byte aligned, stats 8-byte aligned.
+ * hidden, w_shard and logits_out must be 16-byte aligned, stats 8-byte aligned.
  * Errors: GRPO_ERR_ARG, GRPO_ERR_SHAPE, GRPO_ERR_ALIGN, GRPO_ERR_WORKSPACE, GRPO_ERR_HIP.
  */
 int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_shard, int64_t T, int64_t H, int64_t V_shard,
-                                   int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats, void* ws,
-                                   size_t ws_bytes, hipStream_t s);
+                                   int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats,
+                                   float* logits_out, void* ws, size_t ws_bytes, hipStream_t s);
+
+/* Bytes of the logits buffer of fused_lmhead_vocab_shard_stats and fused_lmhead_grpo_vocab_shard:
+ * 4 * (T rounded up to 256) * (V_shard rounded up to 256); 0 for T < 0 or V_shard < 1. */
+size_t fused_lmhead_vocab_shard_logits_bytes(int64_t T, int64_t V_shard);
 
 /*
  * Step 2 of the sharded fused LM head: given every shard's records (gathered by the
@@ -364,19 +372,25 @@ int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_shard, int6
  *                devices) and rounds as it needs
  *   dw_shard     device fp32 [H, V_shard]: this shard's dW columns, written or
  *                accumulated into (accumulate_dw != 0)
+ *   logits_in    NULL: the shard's logits are formed again on the matrix cores, chunk by chunk (four
+ *                products in the two steps).  Otherwise the buffer step 1 filled through logits_out
+ *                (unchanged since): D is formed from it and only the two backward products run (three
+ *                in the two steps); vocab_chunk is then not used, the shard is one chunk of Vsp columns
  *   ws, ws_bytes device workspace of at least fused_lmhead_workspace_bytes(T, H, V_shard,
- *                vocab_chunk, n_traj)
+ *                vocab_chunk, n_traj), with vocab_chunk = Vsp when logits_in is given
  * D = grad_scale * dloss/dz is rounded to bf16 per chunk before the two products, as in
- * fused_lmhead_grpo.  Errors: as fused_lmhead_grpo, plus GRPO_ERR_SHAPE for v_begin < 0,
- * v_begin + V_shard > V_total, V_total >= 2^31 or n_shards outside 1..65536, and GRPO_ERR_ARG
- * for stats or dhidden_partial NULL with T > 0.
+ * fused_lmhead_grpo; both ways give bit-identical loss, per-token outputs and D.  Errors: as
+ * fused_lmhead_grpo, plus GRPO_ERR_SHAPE for v_begin < 0, v_begin + V_shard > V_total,
+ * V_total >= 2^31 or n_shards outside 1..65536, GRPO_ERR_ARG for stats or dhidden_partial NULL
+ * with T > 0, and GRPO_ERR_ALIGN for logits_in not 16-byte aligned.
  */
 int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_shard, int64_t T, int64_t H, int64_t V_shard,
                                   int64_t v_begin, int64_t V_total, int32_t vocab_chunk, const grpo_vocab_stats* stats,
                                   int32_t n_shards, const int32_t* actions, const float* behave_logp,
                                   const float* prox_logp, const float* adv, const grpo_segments* seg,
                                   const grpo_loss_params* p, double* loss_out, float* dhidden_partial, float* dw_shard,
-                                  int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
+                                  int32_t accumulate_dw, grpo_aux* aux, const float* logits_in, void* ws,
+                                  size_t ws_bytes, hipStream_t s);
 
 /* A static, human-readable name for a grpo_status value. */
 const char* grpo_status_str(int status);

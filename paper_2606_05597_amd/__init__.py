@@ -21,6 +21,7 @@ from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO
 __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
            "fused_lmhead_grpo", "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
            "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
+           "vocab_shard_logits_buffer",
            "grpo_status_str", "LossAux", "GrpoError"]
 
 
@@ -419,11 +420,26 @@ def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor,
     return loss_out, dlogits
 
 
+def vocab_shard_logits_buffer(T: int, V_shard: int, device) -> torch.Tensor:
+    """An fp32 buffer for the shard's logits kept between the two steps of the sharded fused LM head."""
+    n = int(_lib.load().fused_lmhead_vocab_shard_logits_bytes(int(T), int(V_shard))) // 4
+    return torch.empty(max(n, 1), dtype=torch.float32, device=device)
+
+
+def _check_logits_buffer(buf: torch.Tensor, T: int, V_shard: int):
+    _dev(buf, "logits buffer")
+    need = int(_lib.load().fused_lmhead_vocab_shard_logits_bytes(int(T), int(V_shard)))
+    if buf.dtype != torch.float32 or not buf.is_contiguous() or buf.numel() * 4 < need:
+        raise ValueError(f"the logits buffer must be contiguous float32 of at least {need} bytes")
+
+
 def fused_lmhead_vocab_shard_stats(hidden: torch.Tensor, w_shard: torch.Tensor, actions: torch.Tensor, v_begin: int,
                                    *, stats: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                                   stream=None):
+                                   logits_out: torch.Tensor | None = None, stream=None):
     """Step 1 of the vocabulary-sharded fused LM head: each row of h W_shard (W's columns [v_begin, v_begin +
-    V_shard)) reduced to its record.  Returns uint8 [T, 24] records (read them with ``vocab_stats_fields``)."""
+    V_shard)) reduced to its record.  Returns uint8 [T, 24] records (read them with ``vocab_stats_fields``).
+    ``logits_out`` (fp32, ``fused_lmhead_vocab_shard_logits_bytes(T, V_shard) / 4`` elements, see
+    ``vocab_shard_logits_buffer``) also receives the shard's logits for step 2."""
     _dev(hidden, "hidden")
     _dev(w_shard, "w_shard")
     if hidden.dtype != torch.bfloat16 or w_shard.dtype != torch.bfloat16:
@@ -442,8 +458,11 @@ def fused_lmhead_vocab_shard_stats(hidden: torch.Tensor, w_shard: torch.Tensor, 
     need = lib.fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    if logits_out is not None:
+        _check_logits_buffer(logits_out, T, Vs)
     st = lib.fused_lmhead_vocab_shard_stats(_ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), _ptr(actions),
-                                            _ptr(stats), _ptr(workspace), workspace.numel(), _stream(stream))
+                                            _ptr(stats), _ptr(logits_out), _ptr(workspace), workspace.numel(),
+                                            _stream(stream))
     _check(st, "fused_lmhead_vocab_shard_stats")
     return stats
 
@@ -457,10 +476,12 @@ def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, s
                                   n_groups_total: float = 0.0, dhidden_partial: torch.Tensor | None = None,
                                   dw_shard: torch.Tensor | None = None, accumulate_dw: bool = False,
                                   aux: LossAux | None = None, workspace: torch.Tensor | None = None,
-                                  loss_out: torch.Tensor | None = None, stream=None):
+                                  loss_out: torch.Tensor | None = None, logits_in: torch.Tensor | None = None,
+                                  stream=None):
     """Step 2 of the vocabulary-sharded fused LM head: the loss (fp64 [1]), this shard's partial dhidden (fp32
     [T, H], to be summed over the shards) and its dW columns (fp32 [H, V_shard]), from every shard's records
-    ``stats_all`` (uint8 [n_shards, T, 24], in shard order).  Returns (loss, dhidden_partial, dw_shard)."""
+    ``stats_all`` (uint8 [n_shards, T, 24], in shard order).  With ``logits_in`` (the buffer step 1 filled), D
+    comes from the kept logits instead of a recomputed product.  Returns (loss, dhidden_partial, dw_shard)."""
     _dev(hidden, "hidden")
     _dev(w_shard, "w_shard")
     if hidden.dtype != torch.bfloat16 or w_shard.dtype != torch.bfloat16:
@@ -483,6 +504,9 @@ def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, s
     _dev(dw_shard, "dw_shard")
     if dhidden_partial.dtype != torch.float32 or dw_shard.dtype != torch.float32:
         raise TypeError("dhidden_partial and dw_shard must be float32")
+    if logits_in is not None:
+        _check_logits_buffer(logits_in, T, Vs)
+        vocab_chunk = (Vs + 255) // 256 * 256  # the whole shard as one chunk
     need = fused_lmhead_workspace_bytes(T, H, Vs, vocab_chunk, seg.n_traj)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
@@ -494,6 +518,7 @@ def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, s
         int(stats_all.shape[0]), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
         _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
         _ptr(loss_out), _ptr(dhidden_partial), _ptr(dw_shard), int(bool(accumulate_dw)),
-        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
+        ctypes.byref(ca) if ca is not None else None, _ptr(logits_in), _ptr(workspace), workspace.numel(),
+        _stream(stream))
     _check(st, "fused_lmhead_grpo_vocab_shard")
     return loss_out, dhidden_partial, dw_shard

@@ -91,11 +91,13 @@ def load() -> ctypes.CDLL:
         lib.grpo_loss_fwd_bwd_vocab_shard.restype = ctypes.c_int
         lib.fused_lmhead_vocab_shard_stats_workspace_bytes.argtypes = [I64, I64, I64]
         lib.fused_lmhead_vocab_shard_stats_workspace_bytes.restype = SZ
-        lib.fused_lmhead_vocab_shard_stats.argtypes = [P, P, I64, I64, I64, I64, P, P, P, SZ, P]
+        lib.fused_lmhead_vocab_shard_stats.argtypes = [P, P, I64, I64, I64, I64, P, P, P, P, SZ, P]
         lib.fused_lmhead_vocab_shard_stats.restype = ctypes.c_int
         lib.fused_lmhead_grpo_vocab_shard.argtypes = [P, P, I64, I64, I64, I64, I64, I32, P, I32, P, P, P, P,
                                                       ctypes.POINTER(Segments), ctypes.POINTER(LossParams), P, P, P,
-                                                      I32, ctypes.POINTER(Aux), P, SZ, P]
+                                                      I32, ctypes.POINTER(Aux), P, P, SZ, P]
+        lib.fused_lmhead_vocab_shard_logits_bytes.argtypes = [I64, I64]
+        lib.fused_lmhead_vocab_shard_logits_bytes.restype = SZ
         lib.fused_lmhead_grpo_vocab_shard.restype = ctypes.c_int
         lib.grpo_status_str.argtypes = [ctypes.c_int]
         lib.grpo_status_str.restype = ctypes.c_char_p

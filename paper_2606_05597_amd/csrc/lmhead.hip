@@ -670,11 +670,12 @@ static dim3 gemm_grid(int64_t M, int64_t N) {
   return dim3((unsigned)((tiles + 7) / 8 * 8));
 }
 
-// W^T [V, H] from W [H, V], and (when hT is set) h^T [H, Tp] with zero columns T..Tp.
+// W^T [V, H] from W [H, V] (when WT is set), and h^T [H, Tp] with zero columns T..Tp (when hT is set).
 static void lm_transpose(const uint16_t* W16, const uint16_t* h16, int64_t T, int64_t H, int64_t V, int Tp,
                          uint16_t* WT, uint16_t* hT, hipStream_t s) {
-  hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((V + 63) / 64), (unsigned)((H + 63) / 64)), dim3(256), 0, s,
-                     W16, V, (int)H, (int)V, WT, H, (int)H);
+  if (WT)
+    hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((V + 63) / 64), (unsigned)((H + 63) / 64)), dim3(256), 0,
+                       s, W16, V, (int)H, (int)V, WT, H, (int)H);
   if (hT)
     hipLaunchKernelGGL(k_transpose_bf16, dim3((unsigned)((H + 63) / 64), (unsigned)((Tp + 63) / 64)), dim3(256), 0,
                        s, h16, H, (int)T, (int)H, hT, (int64_t)Tp, Tp);
@@ -1023,14 +1024,21 @@ extern "C" size_t fused_lmhead_vocab_shard_stats_workspace_bytes(int64_t T, int6
   return lm_stats_ws_layout(T, H, V_shard).total;
 }
 
+extern "C" size_t fused_lmhead_vocab_shard_logits_bytes(int64_t T, int64_t V_shard) {
+  if (T < 0 || V_shard < 1) return 0;
+  return sizeof(float) * (size_t)((T + TILE - 1) / TILE * TILE) * (size_t)((V_shard + TILE - 1) / TILE * TILE);
+}
+
 extern "C" int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_shard, int64_t T, int64_t H,
                                               int64_t V_shard, int64_t v_begin, const int32_t* actions,
-                                              grpo_vocab_stats* stats, void* ws, size_t ws_bytes, hipStream_t s) {
+                                              grpo_vocab_stats* stats, float* logits_out, void* ws,
+                                              size_t ws_bytes, hipStream_t s) {
   int st = check_fused_shapes(T, H, V_shard);
   if (st != GRPO_OK) return st;
   if (v_begin < 0 || v_begin + V_shard >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
   if (!w_shard || (T > 0 && (!hidden || !actions || !stats))) return GRPO_ERR_ARG;
-  if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(stats, 8)) return GRPO_ERR_ALIGN;
+  if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(stats, 8) || !aligned(logits_out, 16))
+    return GRPO_ERR_ALIGN;
   const LmStatsWs L = lm_stats_ws_layout(T, H, V_shard);
   if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
@@ -1041,7 +1049,17 @@ extern "C" int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_
   float2* part = reinterpret_cast<float2*>(w + L.part);
   const int n_tiles = (int)((V_shard + TILE - 1) / TILE);
   lm_transpose(static_cast<const uint16_t*>(w_shard), h16, T, H, V_shard, 0, WT, nullptr, s);
-  lm_pass1(h16, WT, T, H, V_shard, part, n_tiles, s);
+  if (logits_out) {  // the shard's fp32 logits kept for the backward call
+    PartialArgs pa;
+    pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V_shard, (int)H};
+    pa.part = part;
+    pa.n_tiles = n_tiles;
+    pa.z = logits_out;
+    pa.ldz = (int64_t)n_tiles * TILE;
+    hipLaunchKernelGGL(k_lm_partial<true>, gemm_grid(T, V_shard), dim3(LmCfg::NT), 0, s, pa);
+  } else {
+    lm_pass1(h16, WT, T, H, V_shard, part, n_tiles, s);
+  }
   RecordArgs ra{part, h16, WT, actions, stats, v_begin, V_shard, (int)T, (int)H, n_tiles};
   hipLaunchKernelGGL(k_lm_record, dim3((unsigned)T), dim3(256), 0, s, ra);
   return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
@@ -1053,19 +1071,23 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
                                              const float* behave_logp, const float* prox_logp, const float* adv,
                                              const grpo_segments* seg, const grpo_loss_params* p, double* loss_out,
                                              float* dhidden_partial, float* dw_shard, int32_t accumulate_dw,
-                                             grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s) {
+                                             grpo_aux* aux, const float* logits_in, void* ws, size_t ws_bytes,
+                                             hipStream_t s) {
   int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
   if (st != GRPO_OK) return st;
   if (!w_shard || !dw_shard || (T > 0 && (!hidden || !dhidden_partial || !stats))) return GRPO_ERR_ARG;
   st = check_fused_shapes(T, H, V_shard);
   if (st != GRPO_OK) return st;
   if (T > kMaxFusedLen || V_shard > kMaxFusedLen) return GRPO_ERR_SHAPE;
+  // with the statistics call's logits, the shard is one chunk of V_shard rounded up to the tile
+  const int64_t Vsp = (V_shard + TILE - 1) / TILE * TILE;
+  if (logits_in) vocab_chunk = (int32_t)Vsp;
   if (vocab_chunk < 256 || vocab_chunk % 256 != 0) return GRPO_ERR_SHAPE;
   if (v_begin < 0 || V_total >= ((int64_t)1 << 31) || v_begin + V_shard > V_total || n_shards < 1 ||
       n_shards > 65536)
     return GRPO_ERR_SHAPE;
   if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(dhidden_partial, 16) || !aligned(dw_shard, 16) ||
-      !aligned(stats, 8))
+      !aligned(stats, 8) || !aligned(logits_in, 16))
     return GRPO_ERR_ALIGN;
   const LmWs L = lm_ws_layout(T, H, V_shard, vocab_chunk, seg->n_traj);
   if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
@@ -1086,7 +1108,7 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
     return launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
   }
-  lm_transpose(W16, h16, T, H, V_shard, Tp, WT, hT, s);
+  lm_transpose(W16, h16, T, H, V_shard, Tp, logits_in ? nullptr : WT, hT, s);  // no W^T: nothing recomputed
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   const bool timed = aux && aux->hot_begin && aux->hot_end;
   if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
@@ -1101,9 +1123,30 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
   sa.n_shards = n_shards;
   hipLaunchKernelGGL(k_lm_shard_scale, dim3((unsigned)((Tp + 255) / 256)), dim3(256), 0, s, sa);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
-  lm_pass2(Pass2{h16, W16, WT, hT, rs, D, DT, dhidden_partial, nullptr, dw_shard, T, H, V_shard, Tp, vocab_chunk,
-                 accumulate_dw},
-           s);
+  if (logits_in) {
+    // D, D^T of the whole shard from its stored logits, then dW (K = Tp) and the fp32 partial dhidden (K = V_shard)
+    // in one launch, the long dW tiles first
+    const BlockDArgs da{logits_in, rs, D, DT, Vsp, (int)V_shard, Tp};
+    hipLaunchKernelGGL(k_lm_block_d, dim3((unsigned)(Tp / 64 * ((Vsp + kBlockDStrip - 1) / kBlockDStrip))), dim3(256),
+                       0, s, da);
+    DhDwArgs ba;
+    ba.dh.g = GemmArgs{D, W16, Vsp, V_shard, (int)T, (int)H, (int)V_shard};
+    ba.dh.acc = dhidden_partial;
+    ba.dh.dh = nullptr;
+    ba.dh.first = 1;
+    ba.dh.last = 0;
+    ba.dw.g = GemmArgs{hT, DT, Tp, Tp, (int)H, (int)V_shard, Tp};
+    ba.dw.dw = dw_shard;
+    ba.dw.V = V_shard;
+    ba.dw.c0 = 0;
+    ba.dw.accumulate = accumulate_dw;
+    ba.dw_blocks = (int)gemm_grid(H, V_shard).x;
+    hipLaunchKernelGGL(k_lm_dh_dw, dim3((unsigned)ba.dw_blocks + gemm_grid(T, H).x), dim3(LmCfg::NT), 0, s, ba);
+  } else {
+    lm_pass2(Pass2{h16, W16, WT, hT, rs, D, DT, dhidden_partial, nullptr, dw_shard, T, H, V_shard, Tp, vocab_chunk,
+                   accumulate_dw},
+             s);
+  }
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;
   if (launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;

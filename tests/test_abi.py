@@ -39,6 +39,7 @@ def test_header_declares_the_boundary():
                                            "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
                                            "fused_lmhead_vocab_shard_stats_workspace_bytes",
                                            "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
+                                           "fused_lmhead_vocab_shard_logits_bytes",
                                            "grpo_status_str"])
 
 
@@ -254,8 +255,9 @@ def test_shard_loss_rejects_bad_arguments(lib, kw, status):
     assert call_shard_loss(lib, **kw) == status
 
 
-def call_fused_shard_stats(lib, *, T=8, H=64, V=512, v_begin=0, hidden=D, w=D, stats=D, ws=D, ws_bytes=1 << 30):
-    return lib.fused_lmhead_vocab_shard_stats(hidden, w, T, H, V, v_begin, D, stats, ws, ws_bytes, None)
+def call_fused_shard_stats(lib, *, T=8, H=64, V=512, v_begin=0, hidden=D, w=D, stats=D, logits=None, ws=D,
+                           ws_bytes=1 << 30):
+    return lib.fused_lmhead_vocab_shard_stats(hidden, w, T, H, V, v_begin, D, stats, logits, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -268,6 +270,7 @@ def call_fused_shard_stats(lib, *, T=8, H=64, V=512, v_begin=0, hidden=D, w=D, s
     (dict(hidden=None), _lib.GRPO_ERR_ARG),
     (dict(stats=None), _lib.GRPO_ERR_ARG),
     (dict(stats=ctypes.c_void_p(0x100004)), _lib.GRPO_ERR_ALIGN),
+    (dict(logits=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),  # the kept logits are 16-byte aligned
     (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
 ])
 def test_fused_shard_stats_rejects_bad_arguments(lib, kw, status):
@@ -279,18 +282,22 @@ def test_fused_shard_stats_workspace(lib):
     n = lib.fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs)
     assert n >= 2 * Vs * H + 8 * T * ((Vs + 255) // 256) and n % 256 == 0
     assert lib.fused_lmhead_vocab_shard_stats_workspace_bytes(-1, H, Vs) == 0
+    # the kept logits: fp32, T and V_shard rounded up to the 256 tile
+    assert lib.fused_lmhead_vocab_shard_logits_bytes(T, Vs) == 4 * T * 19200
+    assert lib.fused_lmhead_vocab_shard_logits_bytes(300, 8) == 4 * 512 * 256
+    assert lib.fused_lmhead_vocab_shard_logits_bytes(-1, Vs) == 0 and lib.fused_lmhead_vocab_shard_logits_bytes(T, 0) == 0
 
 
 def call_fused_shard(lib, *, T=8, H=64, V=512, v_begin=0, V_total=1024, chunk=256, stats=D, n_shards=2, hidden=D,
-                     w=D, dhp=D, dw=D, ws=D, ws_bytes=1 << 40):
+                     w=D, dhp=D, dw=D, logits=None, ws=D, ws_bytes=1 << 40):
     seg = _lib.Segments()
     seg.n_traj, seg.group_size, seg.n_steps = 4, 4, 4
     seg.step_tok_off, seg.traj_step_off = D, D
     p = _lib.LossParams()
     p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale = 1, 10.0, 0.2, 0.2, 0.0, 1.0
     return lib.fused_lmhead_grpo_vocab_shard(hidden, w, T, H, V, v_begin, V_total, chunk, stats, n_shards, D, D, None,
-                                             D, ctypes.byref(seg), ctypes.byref(p), D, dhp, dw, 0, None, ws, ws_bytes,
-                                             None)
+                                             D, ctypes.byref(seg), ctypes.byref(p), D, dhp, dw, 0, None, logits, ws,
+                                             ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -308,10 +315,19 @@ def call_fused_shard(lib, *, T=8, H=64, V=512, v_begin=0, V_total=1024, chunk=25
     (dict(stats=None), _lib.GRPO_ERR_ARG),
     (dict(dhp=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),
     (dict(stats=ctypes.c_void_p(0x100004)), _lib.GRPO_ERR_ALIGN),
+    (dict(logits=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),
     (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
 ])
 def test_fused_shard_rejects_bad_arguments(lib, kw, status):
     assert call_fused_shard(lib, **kw) == status
+
+
+def test_fused_shard_kept_logits_ignores_chunk(lib):
+    # with the statistics call's logits the shard is one chunk: a chunk that is not a multiple of 256 passes the
+    # shape checks, and the workspace needed is the whole-shard chunk's (T = 8, H = 64, V_shard = 512, 4 trajectories)
+    assert call_fused_shard(lib, chunk=300) == _lib.GRPO_ERR_SHAPE
+    need = lib.fused_lmhead_workspace_bytes(8, 64, 512, 512, 4)
+    assert call_fused_shard(lib, chunk=300, logits=D, ws_bytes=need - 1) == _lib.GRPO_ERR_WORKSPACE
 
 
 def test_advantages_ex_rejects_bad_arguments(lib):

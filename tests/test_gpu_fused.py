@@ -65,10 +65,11 @@ def fused_call(b, A32, sto, tso, sched, **kw):
     return grpo.fused_lmhead_grpo(*args, vocab_chunk=sched, **kw)
 
 
-def run(b, A32, sto, tso, chunk, norm, c, gs=1.0, dw=None, accumulate=False):
+def run(b, A32, sto, tso, chunk, norm, c, gs=1.0, dw=None, accumulate=False, prox=None, ngt=0.0):
     aux = grpo.LossAux.alloc(b["structure"].T, len(b["structure"].rewards), "cuda")
     loss, dh, dW = fused_call(b, A32, sto, tso, chunk, norm=gpu_norm(norm), k=b["cfg"].k, dual_clip_c=c,
-                              grad_scale=gs, dw_lm=dw, accumulate_dw=accumulate, aux=aux)
+                              grad_scale=gs, dw_lm=dw, accumulate_dw=accumulate, aux=aux, prox_logp=prox,
+                              n_groups_total=ngt)
     torch.cuda.synchronize()
     return loss.item(), dh, dW, aux
 
@@ -89,17 +90,19 @@ def check_dw(dw_gpu, ref_dw, h64, D, what=""):
     assert rel <= 5e-3, f"{what}: dW relative Frobenius {rel}"
 
 
-def full_compare(b, chunk, norm, c, gs=1.0, accumulate=False):
+def full_compare(b, chunk, norm, c, gs=1.0, accumulate=False, prox=None, ngt=0.0):
     A64, A32, seg, sto, tso = setup(b)
     H, V = b["H"], b["V"]
     dw0 = None
     if accumulate:
         dw0 = torch.randn((H, V), device="cuda", generator=torch.Generator("cuda").manual_seed(9)) * 1e-3
     dw_in = None if dw0 is None else dw0.clone()
-    loss, dh, dW, aux = run(b, A32, sto, tso, chunk, norm, c, gs, dw=dw_in, accumulate=accumulate)
+    loss, dh, dW, aux = run(b, A32, sto, tso, chunk, norm, c, gs, dw=dw_in, accumulate=accumulate, prox=prox,
+                            ngt=ngt)
     hb, Wb = bits(b["hidden"]), bits(b["W"])
-    ref = fused.fused_loss(hb, Wb, b["actions"].cpu().numpy(), b["behave"].cpu().numpy(), None, A64, seg,
-                           b["cfg"].G, norm=norm, k=b["cfg"].k, dual_clip_c=c, grad_scale=gs)
+    ref = fused.fused_loss(hb, Wb, b["actions"].cpu().numpy(), b["behave"].cpu().numpy(),
+                           None if prox is None else prox.cpu().numpy(), A64, seg, b["cfg"].G, norm=norm,
+                           k=b["cfg"].k, dual_clip_c=c, grad_scale=gs, n_groups_total=ngt)
     assert abs(loss - ref.loss) <= LOSS_RTOL * abs(ref.loss), (loss, ref.loss)
     assert np.abs(aux.token_logp.cpu().numpy() - ref.rows.token_logp).max() <= 5e-5
     np.testing.assert_allclose(aux.traj_loss.cpu().numpy(), ref.rows.traj_loss, rtol=LOSS_RTOL,
@@ -140,6 +143,18 @@ def test_fused_medium_multichunk_accumulate(sched):
 def test_fused_single_chunk(sched):
     b = make_fused_batch(small_cfg(1, 4, 128, 512, seed=13), "cuda")
     full_compare(b, sched, oracle.NORM_CONST_K, 0.0)
+
+
+@pytest.mark.parametrize("sched", [256, Blocked(256)])
+def test_fused_decoupled_and_global_groups(sched):
+    # a proximal policy distinct from the behaviour one (decoupled ratios: the clip acts on pi/pi_prox, the
+    # weight is pi_prox/pi_behave), and the normaliser's group count overridden as a data-parallel shard of a
+    # 3x larger batch would pass it; several token blocks of 256
+    b = make_fused_batch(small_cfg(4, 8, 128, 1000, seed=19, tok_mean=6.0, steps=(2, 6)), "cuda")
+    gen = torch.Generator("cuda").manual_seed(20)
+    prox = b["behave"] + 0.05 * torch.randn(b["behave"].shape, device="cuda", generator=gen)
+    assert b["structure"].T > 2 * 256
+    full_compare(b, sched, oracle.NORM_TRAJ_STEPS, 3.0, prox=prox, ngt=12.0)
 
 
 @pytest.mark.parametrize("sched", [8192, Blocked(256)])
