@@ -534,7 +534,15 @@ struct BlockDArgs {
   int64_t ld;          // a multiple of 64; columns V..ld get D = 0
   int V, rows;         // rows: a multiple of 64
 };
-constexpr int kBlockDStrip = 512;  // columns per workgroup: eight 64 x 64 tiles
+constexpr int kBlockDStrip = 512;  // columns per work item: eight 64 x 64 tiles
+constexpr int64_t kBlockDMaxGrid = 1 << 20;  // workgroups per launch at most; they loop over the rest
+
+// Workgroups for n work items: all of them up to the cap, or `grid` (> 0) when fewer.
+static unsigned block_d_grid(int64_t rows, int64_t ld, int grid) {
+  int64_t items = rows / 64 * ((ld + kBlockDStrip - 1) / kBlockDStrip);
+  if (items > kBlockDMaxGrid) items = kBlockDMaxGrid;
+  return (unsigned)(grid > 0 && grid < items ? grid : items);
+}
 
 // Work items of 64 rows and a strip of up to eight 64-column tiles, item i = strip * (rows / 64) + row tile; a
 // workgroup of 256 threads takes items blockIdx.x, blockIdx.x + gridDim.x, ... (one each with a full grid; a
@@ -548,11 +556,11 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
   __shared__ uint32_t tu[2][64 * kLdw];
   __shared__ RowScale srs[64];
   const int tid = threadIdx.x;
-  const int n_rt = a.rows / 64;
-  const int n_items = n_rt * (int)((a.ld + kBlockDStrip - 1) / kBlockDStrip);
-  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
-    const int r0 = (item % n_rt) * 64;
-    const int64_t cs = (int64_t)(item / n_rt) * kBlockDStrip;
+  const int64_t n_rt = a.rows / 64;
+  const int64_t n_items = n_rt * ((a.ld + kBlockDStrip - 1) / kBlockDStrip);
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int r0 = (int)(item % n_rt) * 64;
+    const int64_t cs = (item / n_rt) * kBlockDStrip;
     __syncthreads();  // the previous item's last reads of tu and srs are done
     if (tid < 64) srs[tid] = a.rs[r0 + tid];
     __syncthreads();
@@ -945,8 +953,7 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   auto dpass = [&](int b, hipStream_t st, int grid) {
     const int rows_p = (rows_of(b) + TILE - 1) / TILE * TILE;
     const BlockDArgs da{z_of(b), rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V, rows_p};
-    const int items = rows_p / 64 * (int)((L.ldz + kBlockDStrip - 1) / kBlockDStrip);
-    hipLaunchKernelGGL(k_lm_block_d, dim3((unsigned)(grid > 0 && grid < items ? grid : items)), dim3(256), 0, st, da);
+    hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(rows_p, L.ldz, grid)), dim3(256), 0, st, da);
   };
   // block b's dhidden rows = D W^T (K = V) and dW (+)= h^T D (K = the block's rows, zero-padded), on s
   auto backward = [&](int b) {
@@ -1127,8 +1134,7 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
     // D, D^T of the whole shard from its stored logits, then dW (K = Tp) and the fp32 partial dhidden (K = V_shard)
     // in one launch, the long dW tiles first
     const BlockDArgs da{logits_in, rs, D, DT, Vsp, (int)V_shard, Tp};
-    hipLaunchKernelGGL(k_lm_block_d, dim3((unsigned)(Tp / 64 * ((Vsp + kBlockDStrip - 1) / kBlockDStrip))), dim3(256),
-                       0, s, da);
+    hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(Tp, Vsp, 0)), dim3(256), 0, s, da);
     DhDwArgs ba;
     ba.dh.g = GemmArgs{D, W16, Vsp, V_shard, (int)T, (int)H, (int)V_shard};
     ba.dh.acc = dhidden_partial;
