@@ -21,7 +21,7 @@ from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO
 __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
            "fused_lmhead_grpo", "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
            "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
-           "vocab_shard_logits_buffer",
+           "vocab_shard_logits_buffer", "GrpoLoss", "FusedLmHeadGrpoLoss",
            "grpo_status_str", "LossAux", "GrpoError"]
 
 
@@ -522,3 +522,6 @@ def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, s
         _stream(stream))
     _check(st, "fused_lmhead_grpo_vocab_shard")
     return loss_out, dhidden_partial, dw_shard
+
+
+from .autograd import FusedLmHeadGrpoLoss, GrpoLoss  # noqa: E402  (needs the entry points above)
