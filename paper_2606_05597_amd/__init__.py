@@ -21,7 +21,7 @@ from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO
 __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
            "fused_lmhead_grpo", "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
            "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
-           "vocab_shard_logits_buffer", "GrpoLoss", "FusedLmHeadGrpoLoss",
+           "vocab_shard_logits_buffer", "GrpoLoss", "FusedLmHeadGrpoLoss", "loss",
            "grpo_status_str", "LossAux", "GrpoError"]
 
 
@@ -84,6 +84,17 @@ def grpo_advantages_ex(rewards: torch.Tensor, group_size: int, mode: int = GRPO_
 
 def grpo_loss_workspace_bytes(T: int, n_traj: int) -> int:
     return int(_lib.load().grpo_loss_workspace_bytes(int(T), int(n_traj)))
+
+
+def loss(logits: torch.Tensor, actions: torch.Tensor, old_logp: torch.Tensor, rewards: torch.Tensor,
+         step_tok_off: torch.Tensor, traj_step_off: torch.Tensor, group_size: int, *, ddof: int = 1,
+         std_eps: float = 0.0, stream=None, **opts):
+    """The loss and dlogits from rewards: the group-relative advantages of Sec. 3.2 (``grpo_advantages``), then
+    ``grpo_loss_fwd_bwd`` with ``old_logp`` as the behaviour log-probs, on the same stream.  ``opts``: the keyword
+    options of ``grpo_loss_fwd_bwd``.  Returns (loss [1] fp64, dlogits)."""
+    adv = grpo_advantages(rewards, group_size, ddof=ddof, std_eps=std_eps, stream=stream)
+    return grpo_loss_fwd_bwd(logits, actions, old_logp, adv, step_tok_off, traj_step_off, group_size,
+                             stream=stream, **opts)
 
 
 def fused_lmhead_workspace_bytes(T: int, H: int, V: int, vocab_chunk: int, n_traj: int) -> int:

@@ -72,3 +72,17 @@ def test_fused_autograd_matches_entry_point(opts):
     assert loss.item() == want_loss.item()
     assert torch.equal(h.grad, want_dh)
     assert w.grad.dtype == torch.bfloat16 and torch.equal(w.grad, want_dw.to(torch.bfloat16))
+
+
+def test_loss_from_rewards_equals_the_two_calls():
+    # grpo.loss: advantages from the rewards, then the loss, in one call; bit-identical to making the two calls
+    b = make_batch("v32k", "cuda")
+    st, cfg = b["structure"], b["cfg"]
+    sto, tso = _seg(st)
+    l1, d1 = grpo.loss(b["logits"], b["actions"], b["behave"], b["rewards"], sto, tso, cfg.G, k=cfg.k,
+                       dual_clip_c=3.0)
+    adv = grpo.grpo_advantages(b["rewards"], cfg.G)
+    l2, d2 = grpo.grpo_loss_fwd_bwd(b["logits"], b["actions"], b["behave"], adv, sto, tso, cfg.G, k=cfg.k,
+                                    dual_clip_c=3.0)
+    torch.cuda.synchronize()
+    assert torch.equal(l1, l2) and torch.equal(d1, d2)
