@@ -231,8 +231,8 @@ size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int
  *                and releases itself; s_aux's work is joined back into s before the last launch on s, so the
  *                results are complete in s's order, as with one stream (and the call can be captured from s
  *                into a HIP graph).  The results are bit-identical either way.
- * Errors: as fused_lmhead_grpo (GRPO_ERR_SHAPE for token_block outside the range above); GRPO_ERR_HIP if an
- *   event cannot be created.
+ * Errors: as fused_lmhead_grpo (GRPO_ERR_SHAPE for token_block outside the range above); GRPO_ERR_ARG if s_aux
+ *   is on another device than s; GRPO_ERR_HIP if an event cannot be created.
  */
 int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V,
                               int32_t token_block, const int32_t* actions, const float* behave_logp,

@@ -302,6 +302,8 @@ def fused_lmhead_grpo_blocked(hidden: torch.Tensor, w_lm: torch.Tensor, actions:
 
     Returns (loss [1] fp64, dhidden, dw_lm).
     """
+    if aux_stream is not None and aux_stream.device != hidden.device:
+        raise ValueError("aux_stream must be on hidden's device")
     return _fused_call("fused_lmhead_grpo_blocked", fused_lmhead_blocked_workspace_bytes, hidden, w_lm, actions,
                        behave_logp, adv, step_tok_off, traj_step_off, group_size, token_block, prox_logp, norm, k,
                        eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total, dhidden, dw_lm, accumulate_dw,

@@ -899,6 +899,12 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   const LmBlockWs L = lm_block_ws_layout(T, H, V, token_block, seg->n_traj);
   if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
+  if (s_aux && s_aux != s) {  // the second stream must be on the first one's device
+    hipDevice_t dev_s = 0, dev_aux = 0;
+    if (hipStreamGetDevice(s, &dev_s) != hipSuccess || hipStreamGetDevice(s_aux, &dev_aux) != hipSuccess)
+      return GRPO_ERR_HIP;
+    if (dev_s != dev_aux) return GRPO_ERR_ARG;
+  }
   char* w = static_cast<char*>(ws);
   const uint16_t* h16 = static_cast<const uint16_t*>(hidden);
   const uint16_t* W16 = static_cast<const uint16_t*>(w_lm);
