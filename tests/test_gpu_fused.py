@@ -182,28 +182,49 @@ def test_fused_schedules_agree():
     assert (dW1.double() - dW2.double()).norm() <= 1e-5 * dW1.double().norm()
 
 
-@pytest.mark.parametrize("tb,cfg_args", [(256, (4, 8, 256, 5000, 18)), (8192, None)])
-def test_fused_blocked_two_streams_bit_identical(tb, cfg_args):
+@pytest.mark.parametrize("tb,cfg_args,extras", [(256, (4, 8, 256, 5000, 18), False),
+                                                (256, (4, 8, 256, 5000, 28), True),
+                                                (8192, None, False)])
+def test_fused_blocked_two_streams_bit_identical(tb, cfg_args, extras):
     # each block's D pass on a second stream beside the next block's forward product: the same kernels on the
     # same data in a different overlap, so every output is bit-identical to the one-stream call (several blocks
-    # of 256 rows on a small batch; the full fused workload in 8 blocks of 8192)
+    # of 256 rows on a small batch; the full fused workload in 8 blocks of 8192).  extras: dW accumulated onto an
+    # input, a proximal policy distinct from the behaviour one, a gradient scale and a global group count.
     if cfg_args is None:
         b = make_fused_batch("fused", "cuda")
     else:
         b = make_fused_batch(small_cfg(*cfg_args[:4], seed=cfg_args[4], tok_mean=6.0, steps=(2, 9)), "cuda")
     A64, A32, seg, sto, tso = setup(b)
     T, N = b["structure"].T, len(b["structure"].rewards)
+    H, V = b["H"], b["V"]
     assert T > 2 * tb
+    kw = {}
+    dw0 = None
+    if extras:
+        gen = torch.Generator("cuda").manual_seed(29)
+        kw = dict(prox_logp=b["behave"] + 0.05 * torch.randn(b["behave"].shape, device="cuda", generator=gen),
+                  grad_scale=0.25, n_groups_total=12.0, accumulate_dw=True)
+        dw0 = torch.randn((H, V), device="cuda", generator=gen) * 1e-3
     outs = []
     for two in (False, True):
         aux = grpo.LossAux.alloc(T, N, "cuda")
         side = torch.cuda.Stream() if two else None
+        dw = None if dw0 is None else dw0.clone()
         loss, dh, dW = fused_call(b, A32, sto, tso, Blocked(tb), norm=gpu_norm(oracle.NORM_CONST_K), k=b["cfg"].k,
-                                  dual_clip_c=3.0, aux=aux, aux_stream=side)
+                                  dual_clip_c=3.0, aux=aux, aux_stream=side, dw_lm=dw, **kw)
         torch.cuda.synchronize()
         outs.append((loss, dh, dW, aux.token_logp, aux.traj_loss, aux.clip_counts, aux.error_flags))
     for x, y in zip(*outs):
         assert torch.equal(x, y)
+    if extras:  # and against the oracle
+        ref = fused.fused_loss(bits(b["hidden"]), bits(b["W"]), b["actions"].cpu().numpy(), b["behave"].cpu().numpy(),
+                               kw["prox_logp"].cpu().numpy(), A64, seg, b["cfg"].G, norm=oracle.NORM_CONST_K,
+                               k=b["cfg"].k, dual_clip_c=3.0, grad_scale=0.25, n_groups_total=12.0)
+        assert abs(outs[1][0].item() - ref.loss) <= LOSS_RTOL * abs(ref.loss)
+        dW = outs[1][2].cpu().numpy().astype(np.float64) - dw0.cpu().numpy().astype(np.float64)
+        check_dw(dW, ref.dW, fused.as_f64(bits(b["hidden"])), ref.rows.dlogits, "two-stream dW")
+        check_dh(outs[1][1].float().cpu().numpy().astype(np.float64), ref.dhidden, ref.rows.dlogits,
+                 fused.as_f64(bits(b["W"])), "two-stream dhidden")
 
 
 @pytest.mark.parametrize("sched", [8192, Blocked(8192)])
