@@ -383,6 +383,39 @@ def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int
     return out
 
 
+def bench_fused_logp(b: dict, steps: int, warmup: int = 1) -> dict:
+    """Forward only from hidden states (fused_lmhead_token_logp): the action log-probs and entropies of the fused
+    workload, z = h W formed once on the matrix cores and never stored; the whole call timed with HIP events."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    st = b["structure"]
+    T, H, V = st.T, b["H"], b["V"]
+    dev = b["hidden"].device
+    ws = torch.empty(grpo._lib.load().fused_lmhead_token_logp_workspace_bytes(T, H, V), dtype=torch.uint8,
+                     device=dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for _ in range(warmup):
+        grpo.fused_lmhead_token_logp(b["hidden"], b["W"], b["actions"], workspace=ws)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        ev[i][0].record()
+        grpo.fused_lmhead_token_logp(b["hidden"], b["W"], b["actions"], workspace=ws)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(c) for a, c in ev) / steps
+    alg = 2.0 * T * H * V
+    achieved = alg / (ms * 1e-3) / 1e12
+    del ws
+    torch.cuda.empty_cache()
+    return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
+            "workload": f"forward only from hidden states: log-prob and entropy per token, hidden bf16 [{T}, {H}], "
+                        f"W bf16 [{H}, {V}]",
+            "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                         "algorithmic_flop_per_launch": alg}}
+
+
 FUSED_SCHEDULES = ("blocked", "blocked1", "chunked")
 
 
@@ -422,6 +455,7 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
              "chunked": "vocab_chunked"}
     for sch in schedules[1:]:
         out[names[sch]] = res[sch]
+    out["forward_only"] = bench_fused_logp(b, max(1, steps))
     if shard_steps > 0:
         out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps, keep=True)
         out["vocab_shard"]["recompute"] = bench_fused_shard(b, adv, sto, tso, shard_steps, keep=False)

@@ -264,6 +264,30 @@ int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, int64_t T, i
 int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const int32_t* actions,
                     float* token_logp, float* token_entropy, int32_t* error_flags, hipStream_t s);
 
+/* Bytes of device workspace fused_lmhead_token_logp needs (W^T and the per-(row, 256-column tile) partials:
+ * 2 V H + 12 T ceil(V / 256) bytes, rounded up); 0 for invalid sizes. */
+size_t fused_lmhead_token_logp_workspace_bytes(int64_t T, int64_t H, int64_t V);
+
+/*
+ * Forward only from the final hidden states: grpo_token_logp's outputs (the action's log-prob and the policy
+ * entropy per token, for the proximal log-probs recomputed before an update, Table 5, and the entropy of Sec. 5)
+ * with z = h W formed on the matrix cores in 256-column tiles and never stored.
+ *   hidden, w_lm, T, H, V: as fused_lmhead_grpo
+ *   actions      device int32 [T]
+ *   token_logp   device fp32 [T] or NULL   l_t (0 where a_t is outside [0, V))
+ *   token_entropy device fp32 [T] or NULL  H_t; NULL skips its partial sums in the product's epilogue
+ *   error_flags  device int32 [1] or NULL: overwritten with GRPO_FLAG_ACTION when some a_t is outside [0, V),
+ *                GRPO_FLAG_NONFINITE when a row's log-sum-exp is not finite
+ *   ws, ws_bytes device workspace of at least fused_lmhead_token_logp_workspace_bytes(T, H, V)
+ * Per row: the tile partials (max, sum e^(z - m), sum e^(z - m)(z - m)) merged in fp64; the action logit
+ * h_t . W[:, a_t] as an fp64 dot product of the bf16 inputs.
+ * Errors: GRPO_ERR_ARG, GRPO_ERR_SHAPE (as fused_lmhead_grpo), GRPO_ERR_ALIGN (hidden, w_lm not 16-byte aligned,
+ *   outputs not 4-byte aligned), GRPO_ERR_WORKSPACE, GRPO_ERR_HIP.
+ */
+int fused_lmhead_token_logp(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V,
+                            const int32_t* actions, float* token_logp, float* token_entropy, int32_t* error_flags,
+                            void* ws, size_t ws_bytes, hipStream_t s);
+
 /*
  * The vocabulary split over devices (tensor-parallel LM head; the extension of
  * the loss of Eq. 1 to a sharded vocabulary): the calls one device makes for the

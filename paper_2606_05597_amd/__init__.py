@@ -22,6 +22,7 @@ __all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes",
            "fused_lmhead_grpo", "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
            "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
            "vocab_shard_logits_buffer", "GrpoLoss", "FusedLmHeadGrpoLoss", "loss",
+           "fused_lmhead_token_logp",
            "grpo_status_str", "LossAux", "GrpoError"]
 
 
@@ -342,6 +343,35 @@ def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | Non
 
 
 VOCAB_STATS_BYTES = 24  # one grpo_vocab_stats record: fp64 m, s, z_a
+
+
+def fused_lmhead_token_logp(hidden: torch.Tensor, w_lm: torch.Tensor, actions: torch.Tensor, *,
+                            entropy: bool = True, error_flags: torch.Tensor | None = None,
+                            workspace: torch.Tensor | None = None, stream=None):
+    """Forward only from hidden states: the action's log-prob (fp32 [T]) and, if ``entropy``, the policy entropy
+    (fp32 [T]) of softmax(h W) per token, without storing the logits.  Returns (token_logp, token_entropy or
+    None)."""
+    _dev(hidden, "hidden")
+    _dev(w_lm, "w_lm")
+    if hidden.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
+        raise TypeError("hidden and w_lm must be bfloat16")
+    T, H = hidden.shape
+    H2, V = w_lm.shape
+    if H2 != H:
+        raise ValueError("hidden and w_lm disagree on H")
+    _dev(actions, "actions")
+    if actions.dtype != torch.int32:
+        raise TypeError("actions must be int32")
+    lib = _lib.load()
+    need = int(lib.fused_lmhead_token_logp_workspace_bytes(T, H, V))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    logp = torch.empty(T, dtype=torch.float32, device=hidden.device)
+    ent = torch.empty(T, dtype=torch.float32, device=hidden.device) if entropy else None
+    st = lib.fused_lmhead_token_logp(_ptr(hidden), _ptr(w_lm), T, H, V, _ptr(actions), _ptr(logp), _ptr(ent),
+                                     _ptr(error_flags), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "fused_lmhead_token_logp")
+    return logp, ent
 
 
 def vocab_stats_fields(stats: torch.Tensor):

@@ -81,6 +81,10 @@ def load() -> ctypes.CDLL:
         lib.fused_lmhead_blocked_workspace_bytes.restype = SZ
         lib.fused_lmhead_grpo_blocked.argtypes = lib.fused_lmhead_grpo.argtypes + [P]
         lib.fused_lmhead_grpo_blocked.restype = ctypes.c_int
+        lib.fused_lmhead_token_logp_workspace_bytes.argtypes = [I64, I64, I64]
+        lib.fused_lmhead_token_logp_workspace_bytes.restype = SZ
+        lib.fused_lmhead_token_logp.argtypes = [P, P, I64, I64, I64, P, P, P, P, P, SZ, P]
+        lib.fused_lmhead_token_logp.restype = ctypes.c_int
         lib.grpo_token_logp.argtypes = [P, ctypes.c_int, I64, I64, I64, P, P, P, P, P]
         lib.grpo_token_logp.restype = ctypes.c_int
         lib.grpo_vocab_shard_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, I64, P, P, P, P]

@@ -74,7 +74,14 @@ struct PartialArgs {
   int n_tiles;
   float* z;      // STORE_Z: the fp32 logits [tiles_of(M) * TILE, ldz], every tile stored whole
   int64_t ldz;   // a multiple of TILE, at least n_tiles * TILE
+  float* part_t; // entropy partials [T, n_tiles]: sum over the tile of e^(z - m) (z - m), m the tile's max
 };
+
+// The forward product's epilogue: per (row, 256-column tile) the max m and sum exp(z - m) into part, and with ENT
+// also sum exp(z - m) (z - m) into part_t (the entropy's second moment).  Columns past N are left out.
+template <bool ENT>
+__device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x16 (&acc)[LmCfg::IB][LmCfg::JB],
+                                                    int m0, int n0, int tn, GemmSmem& sm);
 
 template <bool STORE_Z>
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
@@ -117,11 +124,30 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
         }
       }
   }
+  lm_partial_epilogue<false>(p, acc, m0, n0, tn, sm);
+}
+
+// The forward-only fused product: tile partials with the entropy moment, no logits stored.
+__global__ __launch_bounds__(LmCfg::NT) void k_lm_partial_ent(const PartialArgs p) {
+  __shared__ __attribute__((aligned(16))) GemmSmem sm;
+  int tm, tn;
+  if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  g_f32x16 acc[LmCfg::IB][LmCfg::JB];
+  gemm_mainloop<LmCfg>(p.g, tm * TILE, tn * TILE, acc, sm.s);
+  lm_partial_epilogue<true>(p, acc, tm * TILE, tn * TILE, tn, sm);
+}
+
+template <bool ENT>
+__device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x16 (&acc)[LmCfg::IB][LmCfg::JB],
+                                                    int m0, int n0, int tn, GemmSmem& sm) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   // A 16-lane row of a wave holds 16 x JB columns of one output row: reduce them with
   // DPP, then the 2 x WGN such groups of each row through LDS.
   constexpr int NG = 2 * LmCfg::WGN;
   float* sh_m = reinterpret_cast<float*>(sm.s);  // [NG][TILE]
   float* sh_s = sh_m + NG * TILE;                 // [NG][TILE]
+  float* sh_t = sh_s + NG * TILE;                 // [NG][TILE], ENT only
   const int grp = wn * 2 + ((lane >> 4) & 1);
   const int c = n0 + gemm_col<LmCfg>(wn, 0, lane);
   const bool full = n0 + TILE <= p.g.N;
@@ -129,7 +155,7 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   for (int i = 0; i < LmCfg::IB; ++i) {
 #pragma unroll
     for (int r0 = 0; r0 < 16; r0 += 4) {  // four rows at a time: independent DPP chains interleave
-      float v[4][LmCfg::JB], m[4], e[4];
+      float v[4][LmCfg::JB], m[4], e[4], tt[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         m[u] = -INFINITY;
@@ -148,13 +174,24 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
       for (int u = 0; u < 4; ++u) {
         const float nm = (m[u] == -INFINITY) ? 0.f : -m[u] * kLog2e;
         e[u] = 0.f;
+        tt[u] = 0.f;
 #pragma unroll
-        for (int j = 0; j < LmCfg::JB; ++j) e[u] += __builtin_amdgcn_exp2f(fmaf(v[u][j], kLog2e, nm));
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          const float x = __builtin_amdgcn_exp2f(fmaf(v[u][j], kLog2e, nm));
+          e[u] += x;
+          if constexpr (ENT) tt[u] += (v[u][j] == -INFINITY) ? 0.f : x * (v[u][j] - m[u]);
+        }
       }
       GRPO_DPP_STEP(add_f32, e, 0xB1)
       GRPO_DPP_STEP(add_f32, e, 0x4E)
       GRPO_DPP_STEP(add_f32, e, 0x141)
       GRPO_DPP_STEP(add_f32, e, 0x140)
+      if constexpr (ENT) {
+        GRPO_DPP_STEP(add_f32, tt, 0xB1)
+        GRPO_DPP_STEP(add_f32, tt, 0x4E)
+        GRPO_DPP_STEP(add_f32, tt, 0x141)
+        GRPO_DPP_STEP(add_f32, tt, 0x140)
+      }
 #undef GRPO_DPP_STEP
       if ((lane & 15) == 0) {
 #pragma unroll
@@ -162,6 +199,7 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
           const int row = gemm_row<LmCfg>(wm, i, r0 + u, lane);
           sh_m[grp * TILE + row] = m[u];
           sh_s[grp * TILE + row] = e[u];
+          if constexpr (ENT) sh_t[grp * TILE + row] = tt[u];
         }
       }
     }
@@ -171,12 +209,18 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
     float M = -INFINITY;
 #pragma unroll
     for (int q = 0; q < NG; ++q) M = fmaxf(M, sh_m[q * TILE + tid]);
-    float S = 0.f;
+    float S = 0.f, Tm = 0.f;
     if (M != -INFINITY)
 #pragma unroll
-      for (int q = 0; q < NG; ++q)
-        S += sh_s[q * TILE + tid] * __builtin_amdgcn_exp2f((sh_m[q * TILE + tid] - M) * kLog2e);
+      for (int q = 0; q < NG; ++q) {
+        const float mq = sh_m[q * TILE + tid];
+        const float g = __builtin_amdgcn_exp2f((mq - M) * kLog2e);
+        S += sh_s[q * TILE + tid] * g;
+        // a group with no column in range has m = -inf and nothing to add
+        if constexpr (ENT) Tm += (mq == -INFINITY) ? 0.f : g * (sh_t[q * TILE + tid] + sh_s[q * TILE + tid] * (mq - M));
+      }
     p.part[(int64_t)(m0 + tid) * p.n_tiles + tn] = make_float2(M, S);
+    if constexpr (ENT) p.part_t[(int64_t)(m0 + tid) * p.n_tiles + tn] = Tm;
   }
 }
 
@@ -283,6 +327,61 @@ __global__ __launch_bounds__(256) void k_lm_record(const RecordArgs a) {
     r.s = S;
     r.z_a = own ? za : -INFINITY;
     a.stats[t] = r;
+  }
+}
+
+// ---- forward only: the action's log-prob and the entropy per row, one workgroup per row -------------------
+struct LmLogpArgs {
+  const float2* part;     // [T, n_tiles]
+  const float* part_t;    // [T, n_tiles] or null (no entropy)
+  const uint16_t* h;      // [T, H]
+  const uint16_t* WT;     // [V, H]
+  const int32_t* actions;
+  float* logp;            // [T] or null
+  float* entropy;         // [T] or null
+  int32_t* flags;         // or null
+  int64_t V;
+  int T, H, n_tiles;
+};
+
+__global__ void k_lm_clear_flags(int32_t* f) { *f = 0; }
+
+__global__ __launch_bounds__(256) void k_lm_logp(const LmLogpArgs a) {
+  __shared__ RowStatsSmem sh;
+  __shared__ double sh_t[4];
+  const int t = blockIdx.x, tid = threadIdx.x;
+  const int act = a.actions[t];
+  const bool ok = act >= 0 && (int64_t)act < a.V;
+  float M;
+  double S, za;
+  const float2* pr = a.part + (int64_t)t * a.n_tiles;
+  lm_row_stats(pr, a.n_tiles, a.h + (int64_t)t * a.H, a.WT, ok ? act : -1, a.H, sh, M, S, za);
+  double Tm = 0.0;
+  if (a.entropy) {
+    // the row's second moment about M: sum over tiles of e^(m_j - M) (T_j + S_j (m_j - M))
+    const float* pt = a.part_t + (int64_t)t * a.n_tiles;
+    double x = 0.0;
+    if (M != -INFINITY)
+      for (int j = tid; j < a.n_tiles; j += 256) {
+        const float2 q = pr[j];
+        if (q.x != -INFINITY) {
+          const double d = (double)q.x - (double)M;
+          x += exp(d) * ((double)pt[j] + (double)q.y * d);
+        }
+      }
+    x = wave_sum(x);
+    if ((tid & 63) == 0) sh_t[tid >> 6] = x;
+    __syncthreads();
+    Tm = sh_t[0] + sh_t[1] + sh_t[2] + sh_t[3];
+  }
+  if (tid == 0) {
+    const double lse = (double)M + log(S);
+    if (a.logp) a.logp[t] = ok ? (float)(za - lse) : 0.f;
+    if (a.entropy) a.entropy[t] = (float)(log(S) - Tm / S);
+    if (a.flags) {
+      if (!ok) atomicOr(a.flags, GRPO_FLAG_ACTION);
+      if (!isfinite(lse)) atomicOr(a.flags, GRPO_FLAG_NONFINITE);
+    }
   }
 }
 
@@ -697,6 +796,7 @@ static void lm_pass1(const uint16_t* h16, const uint16_t* WT, int64_t T, int64_t
   pa.n_tiles = n_tiles;
   pa.z = nullptr;
   pa.ldz = 0;
+  pa.part_t = nullptr;
   hipLaunchKernelGGL(k_lm_partial<false>, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
 }
 
@@ -942,6 +1042,7 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     pa.n_tiles = L.n_tiles;
     pa.z = z_of(b);
     pa.ldz = L.ldz;
+    pa.part_t = nullptr;
     hipLaunchKernelGGL(k_lm_partial<true>, gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
     CombineArgs ca;
     ca.tok = tok;
@@ -1032,6 +1133,65 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   return GRPO_OK;
 }
 
+// The forward-only call's workspace: W^T and the tile partials (with the entropy moment).
+struct LmLogpWs {
+  size_t wt, part, part_t, total;
+};
+static LmLogpWs lm_logp_ws_layout(int64_t T, int64_t H, int64_t V) {
+  LmLogpWs l;
+  const int64_t n_tiles = (V + TILE - 1) / TILE;
+  size_t o = 0;
+  l.wt = o;     o = align_up(o + sizeof(uint16_t) * (size_t)(V * H));
+  l.part = o;   o = align_up(o + sizeof(float2) * (size_t)(T * n_tiles));
+  l.part_t = o; o = align_up(o + sizeof(float) * (size_t)(T * n_tiles));
+  l.total = o;
+  return l;
+}
+
+extern "C" size_t fused_lmhead_token_logp_workspace_bytes(int64_t T, int64_t H, int64_t V) {
+  if (T < 0 || H < 1 || V < 1) return 0;
+  return lm_logp_ws_layout(T, H, V).total;
+}
+
+extern "C" int fused_lmhead_token_logp(const void* hidden, const void* w_lm, int64_t T, int64_t H, int64_t V,
+                                       const int32_t* actions, float* token_logp, float* token_entropy,
+                                       int32_t* error_flags, void* ws, size_t ws_bytes, hipStream_t s) {
+  int st = check_fused_shapes(T, H, V);
+  if (st != GRPO_OK) return st;
+  if (T > kMaxFusedLen || V > kMaxFusedLen) return GRPO_ERR_SHAPE;
+  if (!w_lm || (T > 0 && (!hidden || !actions))) return GRPO_ERR_ARG;
+  if (!aligned(hidden, 16) || !aligned(w_lm, 16) || !aligned(token_logp, 4) || !aligned(token_entropy, 4))
+    return GRPO_ERR_ALIGN;
+  const LmLogpWs L = lm_logp_ws_layout(T, H, V);
+  if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
+  if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
+  if (error_flags) hipLaunchKernelGGL(k_lm_clear_flags, dim3(1), dim3(1), 0, s, error_flags);
+  if (T == 0) return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+  char* w = static_cast<char*>(ws);
+  const uint16_t* h16 = static_cast<const uint16_t*>(hidden);
+  uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);
+  float2* part = reinterpret_cast<float2*>(w + L.part);
+  float* part_t = reinterpret_cast<float*>(w + L.part_t);
+  const int n_tiles = (int)((V + TILE - 1) / TILE);
+  lm_transpose(static_cast<const uint16_t*>(w_lm), h16, T, H, V, 0, WT, nullptr, s);
+  if (token_entropy) {
+    PartialArgs pa;
+    pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
+    pa.part = part;
+    pa.n_tiles = n_tiles;
+    pa.z = nullptr;
+    pa.ldz = 0;
+    pa.part_t = part_t;
+    hipLaunchKernelGGL(k_lm_partial_ent, gemm_grid(T, V), dim3(LmCfg::NT), 0, s, pa);
+  } else {
+    lm_pass1(h16, WT, T, H, V, part, n_tiles, s);
+  }
+  const LmLogpArgs la{part, token_entropy ? part_t : nullptr, h16, WT, actions, token_logp, token_entropy,
+                      error_flags, V, (int)T, (int)H, n_tiles};
+  hipLaunchKernelGGL(k_lm_logp, dim3((unsigned)T), dim3(256), 0, s, la);
+  return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
+}
+
 extern "C" size_t fused_lmhead_vocab_shard_stats_workspace_bytes(int64_t T, int64_t H, int64_t V_shard) {
   if (T < 0 || H < 1 || V_shard < 1) return 0;
   return lm_stats_ws_layout(T, H, V_shard).total;
@@ -1069,6 +1229,7 @@ extern "C" int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_
     pa.n_tiles = n_tiles;
     pa.z = logits_out;
     pa.ldz = (int64_t)n_tiles * TILE;
+    pa.part_t = nullptr;
     hipLaunchKernelGGL(k_lm_partial<true>, gemm_grid(T, V_shard), dim3(LmCfg::NT), 0, s, pa);
   } else {
     lm_pass1(h16, WT, T, H, V_shard, part, n_tiles, s);

@@ -40,6 +40,7 @@ def test_header_declares_the_boundary():
                                            "fused_lmhead_vocab_shard_stats_workspace_bytes",
                                            "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
                                            "fused_lmhead_vocab_shard_logits_bytes",
+                                           "fused_lmhead_token_logp_workspace_bytes", "fused_lmhead_token_logp",
                                            "grpo_status_str"])
 
 
@@ -339,3 +340,30 @@ def test_advantages_ex_rejects_bad_arguments(lib):
     assert f(D, 8, 8, 1, 3, 0.0, D, None, None, None) == _lib.GRPO_ERR_ARG      # ddof checked under the filter too
     assert f(D, 12, 8, 1, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_SHAPE
     assert f(D, 0, 1, 1, 1, 0.0, D, None, None, None) == _lib.GRPO_ERR_SHAPE
+
+
+def call_fused_logp(lib, *, T=8, H=64, V=512, hidden=D, w=D, actions=D, logp=D, ent=D, ws=D, ws_bytes=1 << 30):
+    return lib.fused_lmhead_token_logp(hidden, w, T, H, V, actions, logp, ent, None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H=96), _lib.GRPO_ERR_SHAPE),
+    (dict(V=500), _lib.GRPO_ERR_SHAPE),
+    (dict(T=-1), _lib.GRPO_ERR_SHAPE),
+    (dict(T=(1 << 23) - 255), _lib.GRPO_ERR_SHAPE),
+    (dict(w=None), _lib.GRPO_ERR_ARG),
+    (dict(hidden=None), _lib.GRPO_ERR_ARG),
+    (dict(actions=None), _lib.GRPO_ERR_ARG),
+    (dict(hidden=ctypes.c_void_p(0x100008)), _lib.GRPO_ERR_ALIGN),
+    (dict(logp=ctypes.c_void_p(0x100002)), _lib.GRPO_ERR_ALIGN),
+    (dict(ws_bytes=16), _lib.GRPO_ERR_WORKSPACE),
+])
+def test_fused_logp_rejects_bad_arguments(lib, kw, status):
+    assert call_fused_logp(lib, **kw) == status
+
+
+def test_fused_logp_workspace(lib):
+    T, H, V = 65536, 3584, 151936
+    n = lib.fused_lmhead_token_logp_workspace_bytes(T, H, V)
+    assert n >= 2 * V * H + 12 * T * 594 and n % 256 == 0
+    assert lib.fused_lmhead_token_logp_workspace_bytes(-1, H, V) == 0
