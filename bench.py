@@ -47,20 +47,25 @@ FUSED_SOURCES = ["paper_2606_05597_amd/csrc/lmhead.hip", "paper_2606_05597_amd/c
                  "paper_2606_05597_amd/csrc/device.h"]
 
 
-def kernel_source_hash() -> str:
+def _code_hash(paths) -> str:
+    """A hash of the sources' code: comments and whitespace removed, so that a measurement stays current across
+    edits of the comments alone."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+    for p in paths:
+        with open(os.path.join(ROOT, p)) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
     return h.hexdigest()[:16]
+
+
+def kernel_source_hash() -> str:
+    return _code_hash(KERNEL_SOURCES)
 
 
 def fused_source_hash() -> str:
-    h = hashlib.sha256()
-    for p in FUSED_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
+    return _code_hash(FUSED_SOURCES)
 
 
 def measured_fused_traffic(schedule: str):

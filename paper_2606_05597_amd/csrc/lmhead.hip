@@ -22,6 +22,10 @@
 //                    dW (+)= h_block^T D (K = B)
 //   With a second stream, block b's D pass runs beside block b + 1's forward
 //   product (one D-pass workgroup per CU next to the product's workgroup).
+// Also here: a vocabulary shard's two calls (its per-token records from pass 1 on
+// its columns; then, given every shard's records, pass 2 on its columns, with the
+// logits formed again or kept from the first call), and the forward-only call
+// (log-prob and entropy from tile partials that carry a third, entropy moment).
 // Every product is one GEMM core (gemm.h) with both operands K-contiguous
 // (C[m, n] = sum_k A[m, k] B[n, k]); W and h are transposed once so that this
 // holds for all of them.  256 x 256 tiles, 8 waves, v_mfma_f32_32x32x16_bf16,
