@@ -103,6 +103,30 @@ def test_dual_clip_forced():
     assert ((ref.token_state >> 1) & 1).sum() > 0 and aux.clip_counts[1].item() > 0
 
 
+@pytest.mark.parametrize("eps_low,eps_high", [(0.2, 0.28), (0.0, 0.0), (0.99, 10.0)])
+def test_clip_ranges(eps_low, eps_high):
+    # an asymmetric range (a wider upper bound), a zero-width one (every ratio but 1 clipped) and one too wide to
+    # clip anything ([0.01, 11]: eps_low must stay below 1), with decoupled ratios and the dual clip on
+    b = make_batch("tiny", "cuda", with_prox=True)
+    A64, A32 = _adv(b)
+    oi = oracle_inputs(b, A64)
+    ref = oracle.loss_rows(to_np_logits(b["logits"]), oi["actions"], oi["behave"], oi["prox"], oi["adv"], oi["seg"],
+                           b["cfg"].G, norm=oracle.NORM_CONST_K, k=b["cfg"].k, eps_low=eps_low, eps_high=eps_high,
+                           dual_clip_c=3.0)
+    loss, dl, aux = run_gpu(b, A32, norm=gpu_norm(oracle.NORM_CONST_K), k=b["cfg"].k, eps_low=eps_low,
+                            eps_high=eps_high, c=3.0)
+    assert abs(loss - ref.loss) <= LOSS_RTOL * abs(ref.loss), (loss, ref.loss)
+    assert np.abs(aux.token_logp.cpu().numpy() - ref.token_logp).max() <= LOGP_ATOL
+    kinks = kink_rows(ref, oi["behave"], oi["prox"], A64[oi["seg"].tok_traj], eps_low, eps_high, 3.0)
+    assert len(kinks) <= 2
+    check_dlogits(dl_to_f64(dl[:, :b["V"]]), ref.dlogits, False, exempt=kinks, what=f"dlogits eps {eps_low}/{eps_high}")
+    clipped = (ref.token_state & 1).sum()
+    if eps_low == 0.0:
+        assert clipped > 0.4 * len(oi["actions"])  # the clipped branch is taken wherever it is the smaller
+    if eps_low == 0.99:
+        assert clipped == 0 and aux.clip_counts[0].item() == 0
+
+
 # ---------------------------------------------------------------- 32k vocabulary (bf16), full batch
 
 @pytest.mark.parametrize("norm", NORMS)
