@@ -1097,8 +1097,9 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     // CU, so that each CU holds one of each: the forward product's workgroup leaves room in LDS and registers
     // for one D-pass workgroup.  ev_c: block b's rows are combined and the previous backward launch (the last
     // reader of D, D^T) is done; ev_d: block b's D pass is done.
-    int dev = 0, n_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
+    int n_cu = 0;  // of the streams' device, which need not be the current one
+    hipDevice_t dev = 0;
+    if (hipStreamGetDevice(s, &dev) != hipSuccess ||
         hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return GRPO_ERR_HIP;
     hipEvent_t ev_c = nullptr, ev_d = nullptr;
