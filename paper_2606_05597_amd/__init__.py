@@ -38,6 +38,31 @@ def _dev(t, name):
     return t
 
 
+def _workspace(workspace, need, device):
+    """The caller's workspace (a contiguous tensor of any dtype on the inputs' device; its size in bytes is what the
+    library is told) or a new one of ``need`` bytes."""
+    if workspace is None:
+        return torch.empty(max(int(need), 1), dtype=torch.uint8, device=device)
+    _dev(workspace, "workspace")
+    if workspace.device != torch.device(device):
+        raise ValueError("workspace must be on the inputs' device")
+    return workspace
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def _loss_out(loss_out, device):
+    """The caller's fp64 loss scalar on the inputs' device, or a new one."""
+    if loss_out is None:
+        return torch.empty(1, dtype=torch.float64, device=device)
+    _dev(loss_out, "loss_out")
+    if loss_out.dtype != torch.float64 or loss_out.numel() < 1 or loss_out.device != torch.device(device):
+        raise ValueError("loss_out must be a float64 GPU tensor of at least one element on the inputs' device")
+    return loss_out
+
+
 def _stream(stream):
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
@@ -136,12 +161,18 @@ class LossAux:
         }
         return LossAux(**{k: mk[k]() for k in which})
 
-    def _c(self):
+    def _c(self, T: int, n_traj: int):
         a = _lib.Aux()
-        for name in ("token_logp", "tok_traj", "traj_tok_off", "gather_idx", "traj_loss", "clip_counts",
-                     "ratio_stats", "error_flags"):
+        want = {"token_logp": (torch.float32, T), "tok_traj": (torch.int32, T), "traj_tok_off": (torch.int32, n_traj + 1),
+                "gather_idx": (torch.int64, T), "traj_loss": (torch.float64, n_traj), "clip_counts": (torch.int64, 2),
+                "ratio_stats": (torch.float64, 8), "error_flags": (torch.int32, 1)}
+        for name, (dt, n) in want.items():
             t = getattr(self, name)
-            setattr(a, name, None if t is None else _dev(t, name).data_ptr())
+            if t is not None:
+                _dev(t, name)
+                if t.dtype != dt or t.numel() < n:
+                    raise ValueError(f"aux.{name} must be {dt} with at least {n} elements")
+            setattr(a, name, None if t is None else t.data_ptr())
         if self.hot_events is not None:
             a.hot_begin, a.hot_end = self.hot_events
         return a
@@ -218,16 +249,14 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
                                 or dlogits.dtype != logits.dtype):
         raise ValueError("dlogits must match logits in shape, stride and dtype")
     need = grpo_loss_workspace_bytes(T, seg.n_traj)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=logits.device)
-    if loss_out is None:
-        loss_out = torch.empty(1, dtype=torch.float64, device=logits.device)
-    ca = aux._c() if aux is not None else None
+    workspace = _workspace(workspace, need, logits.device)
+    loss_out = _loss_out(loss_out, logits.device)
+    ca = aux._c(T, seg.n_traj) if aux is not None else None
     st = _lib.load().grpo_loss_fwd_bwd(
         _ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
         _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
         _ptr(loss_out), _ptr(dlogits), ctypes.byref(ca) if ca is not None else None, _ptr(workspace),
-        workspace.numel(), _stream(stream))
+        _nbytes(workspace), _stream(stream))
     _check(st, "grpo_loss_fwd_bwd")
     return loss_out, dlogits
 
@@ -253,16 +282,14 @@ def _fused_call(entry: str, ws_bytes, hidden, w_lm, actions, behave_logp, adv, s
     _dev(dhidden, "dhidden")
     _dev(dw_lm, "dw_lm")
     need = ws_bytes(T, H, V, sched, seg.n_traj)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
-    if loss_out is None:
-        loss_out = torch.empty(1, dtype=torch.float64, device=hidden.device)
-    ca = aux._c() if aux is not None else None
+    workspace = _workspace(workspace, need, hidden.device)
+    loss_out = _loss_out(loss_out, hidden.device)
+    ca = aux._c(T, seg.n_traj) if aux is not None else None
     st = getattr(_lib.load(), entry)(
         _ptr(hidden), _ptr(w_lm), T, H, V, int(sched), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
         _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
         _ptr(loss_out), _ptr(dhidden), _ptr(dw_lm), int(bool(accumulate_dw)),
-        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream), *extra)
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace), _stream(stream), *extra)
     _check(st, entry)
     return loss_out, dhidden, dw_lm
 
@@ -362,14 +389,15 @@ def fused_lmhead_token_logp(hidden: torch.Tensor, w_lm: torch.Tensor, actions: t
     _dev(actions, "actions")
     if actions.dtype != torch.int32:
         raise TypeError("actions must be int32")
+    if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
+        raise ValueError("error_flags must be an int32 GPU tensor")
     lib = _lib.load()
     need = int(lib.fused_lmhead_token_logp_workspace_bytes(T, H, V))
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    workspace = _workspace(workspace, need, hidden.device)
     logp = torch.empty(T, dtype=torch.float32, device=hidden.device)
     ent = torch.empty(T, dtype=torch.float32, device=hidden.device) if entropy else None
     st = lib.fused_lmhead_token_logp(_ptr(hidden), _ptr(w_lm), T, H, V, _ptr(actions), _ptr(logp), _ptr(ent),
-                                     _ptr(error_flags), _ptr(workspace), workspace.numel(), _stream(stream))
+                                     _ptr(error_flags), _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "fused_lmhead_token_logp")
     return logp, ent
 
@@ -449,16 +477,14 @@ def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor,
                                 or dlogits.dtype != logits.dtype):
         raise ValueError("dlogits must match logits in shape, stride and dtype")
     need = grpo_loss_workspace_bytes(T, seg.n_traj)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=logits.device)
-    if loss_out is None:
-        loss_out = torch.empty(1, dtype=torch.float64, device=logits.device)
-    ca = aux._c() if aux is not None else None
+    workspace = _workspace(workspace, need, logits.device)
+    loss_out = _loss_out(loss_out, logits.device)
+    ca = aux._c(T, seg.n_traj) if aux is not None else None
     st = _lib.load().grpo_loss_fwd_bwd_vocab_shard(
         _ptr(logits), dt, T, Vv, ld, int(v_begin), int(V_total), _ptr(stats_all), int(n_shards), _ptr(actions),
         _ptr(_f32(behave_logp, "behave_logp")), _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")),
         ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dlogits),
-        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), workspace.numel(), _stream(stream))
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "grpo_loss_fwd_bwd_vocab_shard")
     return loss_out, dlogits
 
@@ -499,12 +525,11 @@ def fused_lmhead_vocab_shard_stats(hidden: torch.Tensor, w_shard: torch.Tensor, 
         raise ValueError(f"stats must be uint8 [T, {VOCAB_STATS_BYTES}]")
     lib = _lib.load()
     need = lib.fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
+    workspace = _workspace(workspace, need, hidden.device)
     if logits_out is not None:
         _check_logits_buffer(logits_out, T, Vs)
     st = lib.fused_lmhead_vocab_shard_stats(_ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), _ptr(actions),
-                                            _ptr(stats), _ptr(logits_out), _ptr(workspace), workspace.numel(),
+                                            _ptr(stats), _ptr(logits_out), _ptr(workspace), _nbytes(workspace),
                                             _stream(stream))
     _check(st, "fused_lmhead_vocab_shard_stats")
     return stats
@@ -551,17 +576,15 @@ def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, s
         _check_logits_buffer(logits_in, T, Vs)
         vocab_chunk = (Vs + 255) // 256 * 256  # the whole shard as one chunk
     need = fused_lmhead_workspace_bytes(T, H, Vs, vocab_chunk, seg.n_traj)
-    if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=hidden.device)
-    if loss_out is None:
-        loss_out = torch.empty(1, dtype=torch.float64, device=hidden.device)
-    ca = aux._c() if aux is not None else None
+    workspace = _workspace(workspace, need, hidden.device)
+    loss_out = _loss_out(loss_out, hidden.device)
+    ca = aux._c(T, seg.n_traj) if aux is not None else None
     st = _lib.load().fused_lmhead_grpo_vocab_shard(
         _ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), int(V_total), int(vocab_chunk), _ptr(stats_all),
         int(stats_all.shape[0]), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
         _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
         _ptr(loss_out), _ptr(dhidden_partial), _ptr(dw_shard), int(bool(accumulate_dw)),
-        ctypes.byref(ca) if ca is not None else None, _ptr(logits_in), _ptr(workspace), workspace.numel(),
+        ctypes.byref(ca) if ca is not None else None, _ptr(logits_in), _ptr(workspace), _nbytes(workspace),
         _stream(stream))
     _check(st, "fused_lmhead_grpo_vocab_shard")
     return loss_out, dhidden_partial, dw_shard
