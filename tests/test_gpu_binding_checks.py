@@ -63,3 +63,28 @@ def test_fused_logp_error_flags_checked():
     grpo.fused_lmhead_token_logp(h, w, a, error_flags=flags)
     torch.cuda.synchronize()
     assert flags.item() == 0
+
+
+def test_fused_caller_buffers_checked():
+    from tests.test_gpu_fused_edges import edge_batch
+    e = edge_batch(300, 64, 520, seed=5)
+    A = oracle.advantages(e["rewards"], e["G"])
+    args = (e["hidden"], e["W"], torch.from_numpy(e["actions"]).cuda(), torch.from_numpy(e["behave"]).cuda(),
+            torch.from_numpy(A.astype(np.float32)).cuda(), torch.from_numpy(e["sto"]).cuda(),
+            torch.from_numpy(e["tso"]).cuda(), e["G"])
+    need = grpo.fused_lmhead_blocked_workspace_bytes(300, 64, 520, 256, len(e["rewards"]))
+    with pytest.raises(ValueError, match="workspace"):
+        grpo.fused_lmhead_grpo_blocked(*args, token_block=256, workspace=torch.empty(need, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="loss_out"):
+        grpo.fused_lmhead_grpo_blocked(*args, token_block=256,
+                                       loss_out=torch.empty(1, dtype=torch.float64, device="cpu"))
+    aux = grpo.LossAux.alloc(300, len(e["rewards"]), "cuda")
+    aux.gather_idx = torch.empty(300, dtype=torch.int32, device="cuda")
+    with pytest.raises(ValueError, match="gather_idx"):
+        grpo.fused_lmhead_grpo_blocked(*args, token_block=256, aux=aux)
+    # the same call with valid buffers of the caller's
+    ws = torch.empty((need + 7) // 8, dtype=torch.float64, device="cuda")
+    loss, dh, dw = grpo.fused_lmhead_grpo_blocked(*args, token_block=256, workspace=ws)
+    ref, dh_ref, dw_ref = grpo.fused_lmhead_grpo_blocked(*args, token_block=256)
+    torch.cuda.synchronize()
+    assert loss.item() == ref.item() and torch.equal(dh, dh_ref) and torch.equal(dw, dw_ref)
