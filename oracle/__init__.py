@@ -55,6 +55,9 @@ def _load():
         lib.oracle_loss_rows.argtypes = [P, ctypes.c_int, I64, I64, P, P, P, P, P, P, I32, I32, D,
                                          ctypes.c_int, D, D, D, D, D, I64, I64, P, P, P, P, P]
         lib.oracle_loss_rows.restype = ctypes.c_int
+        lib.oracle_loss_from_logp.argtypes = [P, I64, P, P, P, P, P, P, I32, I32, D, ctypes.c_int, D, D, D, D, D,
+                                              I64, I64, P, P, P]
+        lib.oracle_loss_from_logp.restype = ctypes.c_int
         lib.oracle_reduce.argtypes = [P, P, I64, I32, P]
         lib.oracle_reduce.restype = D
         lib.oracle_advantages_success_filter.argtypes = [P, I32, P]
@@ -65,6 +68,8 @@ def _load():
         lib.oracle_logp_entropy.restype = ctypes.c_int
         lib.oracle_vocab_shard_stats.argtypes = [P, ctypes.c_int, I64, I64, I64, P, I64, I64, P, P, P]
         lib.oracle_vocab_shard_stats.restype = None
+        lib.oracle_ratio_stats.argtypes = [I64, P, P, P, P, D, D, P]
+        lib.oracle_ratio_stats.restype = None
         lib.oracle_set_threads.argtypes = [ctypes.c_int]
         lib.oracle_set_threads.restype = None
         lib.oracle_threads.argtypes = []
@@ -156,6 +161,20 @@ class LossResult:
     dlogits: np.ndarray | None  # [rows, V] fp64
     flags: int
 
+    @property
+    def abs_terms(self) -> float:
+        """sum_t |w_i s_t| over the rows computed: the magnitude of the terms the loss sums."""
+        return float(np.abs(self.token_contrib).sum())
+
+    @property
+    def kappa(self) -> float:
+        """Cancellation ratio of the loss sum, sum_t |w_i s_t| / |sum_t w_i s_t| (>= 1; inf for a zero loss).
+
+        Group-relative advantages sum to zero over each group (Sec. 3.2), so the per-token terms of Eq. 1 carry
+        both signs and largely cancel: an absolute error e in the terms moves the loss by up to kappa * e
+        relative to its own size."""
+        return cancellation_ratio(self.token_contrib)
+
 
 def _logits_dtype(logits: np.ndarray) -> int:
     if logits.dtype == np.float32:
@@ -214,6 +233,72 @@ def loss_rows(logits: np.ndarray, actions, behave_logp, prox_logp, adv, seg: Seg
     tt = np.ascontiguousarray(seg.tok_traj[row_begin:row_end])
     total = lib.oracle_reduce(_ptr(contrib), _ptr(tt), n_rows, n_traj, _ptr(traj))
     return LossResult(float(total), traj, logp, contrib, g, st, dl, int(f))
+
+
+def cancellation_ratio(terms) -> float:
+    """sum |x| / |sum x| of the terms of a sum, in fp64 (inf when the sum is 0)."""
+    x = np.asarray(terms, dtype=np.float64)
+    total = abs(float(np.sum(x)))
+    mag = float(np.abs(x).sum())
+    return float("inf") if total == 0.0 else mag / total
+
+
+def valid_tokens(actions, V: int, seg: Segments) -> np.ndarray:
+    """Tokens that enter the loss: the action lies in [0, V) and the offsets are well formed (int32 0/1)."""
+    a = np.asarray(actions, dtype=np.int64)
+    ok = (a >= 0) & (a < V)
+    if seg.flags & ERR_OFFSETS:
+        ok[:] = False
+    return ok.astype(np.int32)
+
+
+def ratio_stats(token_logp, behave_logp, prox_logp, valid, eps_low: float = 0.2, eps_high: float = 0.2) -> np.ndarray:
+    """Importance-ratio statistics over the valid tokens (see grpo_oracle.c): [sum r, min r, max r, sum rho,
+    min rho, max rho, tokens with r outside [1 - eps_low, 1 + eps_high], tokens counted], r = pi/pi_prox and
+    rho = pi/pi_behave (Sec. 3.2), fp64."""
+    lib = _load()
+    l = _c(token_logp, np.float64)
+    b = _c(behave_logp, np.float32)
+    p = _c(prox_logp, np.float32)
+    v = _c(valid, np.int32)
+    n = len(l)
+    assert len(b) >= n and len(v) >= n and (p is None or len(p) >= n)
+    out = np.empty(8, np.float64)
+    lib.oracle_ratio_stats(n, _ptr(l), _ptr(b), _ptr(p), _ptr(v), float(eps_low), float(eps_high), _ptr(out))
+    return out
+
+
+def loss_from_logp(token_logp, actions, behave_logp, prox_logp, adv, seg: Segments, group_size: int, *, V: int,
+                   norm: int = NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2, eps_high: float = 0.2,
+                   dual_clip_c: float = 0.0, grad_scale: float = 1.0, n_groups_total: float = 0.0,
+                   row_begin: int = 0, row_end: int | None = None) -> LossResult:
+    """Eq. 1 for token rows [row_begin, row_end) from their new log-probs ``token_logp`` (indexed by
+    t - row_begin, as loss_rows returns them), without the logits: the same per-token terms loss_rows forms after
+    its log-softmax, for another normaliser or other parameters.  dlogits is None."""
+    lib = _load()
+    T = len(seg.tok_traj)
+    n_traj = len(seg.traj_steps)
+    if row_end is None:
+        row_end = T
+    n_rows = row_end - row_begin
+    l = _c(token_logp, np.float64)
+    assert len(l) == n_rows
+    a = _c(actions, np.int32)
+    b = _c(behave_logp, np.float32)
+    p = _c(prox_logp, np.float32)
+    A = _c(adv, np.float64)
+    n_groups = float(n_groups_total) if n_groups_total else n_traj / group_size
+    contrib = np.empty(n_rows, np.float64)
+    g = np.empty(n_rows, np.float64)
+    st = np.empty(n_rows, np.int32)
+    f = lib.oracle_loss_from_logp(_ptr(l), int(V), _ptr(a), _ptr(b), _ptr(p), _ptr(A), _ptr(seg.tok_traj),
+                                  _ptr(seg.traj_steps), seg.flags, group_size, n_groups, norm, float(k),
+                                  float(eps_low), float(eps_high), float(dual_clip_c), float(grad_scale), row_begin,
+                                  row_end, _ptr(contrib), _ptr(g), _ptr(st))
+    traj = np.zeros(n_traj, np.float64)
+    tt = np.ascontiguousarray(seg.tok_traj[row_begin:row_end])
+    total = lib.oracle_reduce(_ptr(contrib), _ptr(tt), n_rows, n_traj, _ptr(traj))
+    return LossResult(float(total), traj, l.copy(), contrib, g, st, None, int(f))
 
 
 class LogpEntropy:

@@ -198,6 +198,25 @@ static double token_surrogate(double l, double b, double p, double A, double eps
   return s;
 }
 
+/* The quantities of Eq. 1 for one token once its new log-prob l is known:
+ * the trajectory weight w_i = 1/(n_groups * G * (|tau_i| or k)), the term s_t,
+ * the token's share of the loss -w_i s_t and its coefficient
+ * g_t = grad_scale * w_i * ds_t/dl_t.  Returns ORACLE_ERR_NONFINITE when an
+ * input is not finite (the values then propagate), else 0. */
+static int token_terms(double l, float behave, float prox, double A, int32_t steps, int32_t group_size,
+                       double n_groups, int norm, double k, double eps_lo, double eps_hi, double c,
+                       double grad_scale, double* contrib, double* g, int* state) {
+  double b = (double)behave;
+  double p = (double)prox;
+  double denom = (norm == ORACLE_NORM_CONST_K) ? k : (double)steps;
+  double w = 1.0 / (n_groups * (double)group_size * denom);
+  double dsdl;
+  double s = token_surrogate(l, b, p, A, eps_lo, eps_hi, c, &dsdl, state);
+  *contrib = -w * s;
+  *g = grad_scale * w * dsdl;
+  return (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) ? ORACLE_ERR_NONFINITE : 0;
+}
+
 /* ---- the loss and dlogits for a range of token rows --------------------- */
 
 /* For rows t in [row_begin, row_end) of logits (row t starts at element
@@ -245,18 +264,12 @@ int oracle_loss_rows(const void* logits, int dtype, int64_t V, int64_t ld, const
     int64_t base = t * ld;
     double lse = row_logsumexp(logits, dtype, base, V);
     double l = load_elem(logits, dtype, base + a) - lse;
-    double b = (double)behave[t];
-    double p = prox ? (double)prox[t] : b;
-    double A = adv[i];
-    double denom = (norm == ORACLE_NORM_CONST_K) ? k : (double)traj_steps[i];
-    double w = 1.0 / (n_groups * (double)group_size * denom);
-    double dsdl;
+    double contrib, g;
     int st;
-    double s = token_surrogate(l, b, p, A, eps_lo, eps_hi, c, &dsdl, &st);
-    double g = grad_scale * w * dsdl;
-    if (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) flags |= ORACLE_ERR_NONFINITE;
+    flags |= token_terms(l, behave[t], prox ? prox[t] : behave[t], adv[i], traj_steps[i], group_size, n_groups,
+                         norm, k, eps_lo, eps_hi, c, grad_scale, &contrib, &g, &st);
     if (token_logp) token_logp[q] = l;
-    if (token_contrib) token_contrib[q] = -w * s;
+    if (token_contrib) token_contrib[q] = contrib;
     if (token_g) token_g[q] = g;
     if (token_state) token_state[q] = st;
     if (drow) {
@@ -265,6 +278,40 @@ int oracle_loss_rows(const void* logits, int dtype, int64_t V, int64_t ld, const
         drow[v] = g * (pv - (v == a ? 1.0 : 0.0));
       }
     }
+  }
+  return flags;
+}
+
+/* Eq. 1 for token rows [row_begin, row_end) given their new log-probs
+ * logp[t - row_begin] (as an earlier oracle_loss_rows call on the same rows
+ * returned them), for another normaliser or other loss parameters without
+ * forming the log-softmax again.  Rows are handled exactly as in
+ * oracle_loss_rows: a token whose action is outside [0, V), or every token
+ * when seg_flags has ORACLE_ERR_OFFSETS, contributes 0 (NaN for bad offsets)
+ * with g = 0 and state 0.  Outputs are indexed by t - row_begin; returns the
+ * OR of the error flags seen. */
+int oracle_loss_from_logp(const double* logp, int64_t V, const int32_t* actions, const float* behave,
+                          const float* prox, const double* adv, const int32_t* tok_traj,
+                          const int32_t* traj_steps, int32_t seg_flags, int32_t group_size, double n_groups,
+                          int norm, double k, double eps_lo, double eps_hi, double c, double grad_scale,
+                          int64_t row_begin, int64_t row_end, double* token_contrib, double* token_g,
+                          int32_t* token_state) {
+  int flags = seg_flags & ORACLE_ERR_OFFSETS;
+  for (int64_t t = row_begin; t < row_end; ++t) {
+    int64_t q = t - row_begin;
+    int64_t a = actions[t];
+    if ((seg_flags & ORACLE_ERR_OFFSETS) || a < 0 || a >= V) {
+      if (!(seg_flags & ORACLE_ERR_OFFSETS)) flags |= ORACLE_ERR_ACTION;
+      token_contrib[q] = (seg_flags & ORACLE_ERR_OFFSETS) ? NAN : 0.0;
+      token_g[q] = 0.0;
+      token_state[q] = 0;
+      continue;
+    }
+    int32_t i = tok_traj[t];
+    int st;
+    flags |= token_terms(logp[q], behave[t], prox ? prox[t] : behave[t], adv[i], traj_steps[i], group_size,
+                         n_groups, norm, k, eps_lo, eps_hi, c, grad_scale, &token_contrib[q], &token_g[q], &st);
+    token_state[q] = st;
   }
   return flags;
 }
@@ -283,7 +330,51 @@ double oracle_reduce(const double* token_contrib, const int32_t* tok_traj, int64
   return total;
 }
 
-/* Threads the row loop runs on (for reporting the oracle's timing). */
+/* ---- importance-ratio statistics ----------------------------------------- */
+
+/* Diagnostics of the ratios that enter Eq. 1, over the tokens that enter the
+ * loss (valid[t] != 0: an action inside the vocabulary, well-formed offsets):
+ * r = pi/pi_prox = exp(l - p) (the clipped ratio) and rho = pi/pi_behave =
+ * exp(l - b) (the importance weight), where l is the token's new log-prob,
+ * b its behaviour log-prob and p its proximal log-prob (p = b when prox is
+ * NULL, the coupled ratio).  The paper reports how often the eps clip engages
+ * and how the coupled ratio compares with the decoupled one (Sec. 4.3,
+ * Sec. 5); these are those quantities' building blocks:
+ *   out[0..2] = sum, min, max of r       out[3..5] = sum, min, max of rho
+ *   out[6]    = tokens with r outside [1 - eps_lo, 1 + eps_hi] (inclusive range)
+ *   out[7]    = tokens counted.
+ * With no token counted the sums are 0, the minima +inf and the maxima -inf.
+ * Sums run in token order in fp64. */
+void oracle_ratio_stats(int64_t n, const double* logp, const float* behave, const float* prox,
+                        const int32_t* valid, double eps_lo, double eps_hi, double* out) {
+  double sr = 0.0, rmin = INFINITY, rmax = -INFINITY;
+  double sp = 0.0, pmin = INFINITY, pmax = -INFINITY;
+  double outside = 0.0, count = 0.0;
+  for (int64_t t = 0; t < n; ++t) {
+    if (!valid[t]) continue;
+    double b = (double)behave[t];
+    double p = prox ? (double)prox[t] : b;
+    double r = exp(logp[t] - p);
+    double rho = exp(logp[t] - b);
+    sr += r;
+    if (r < rmin) rmin = r;
+    if (r > rmax) rmax = r;
+    sp += rho;
+    if (rho < pmin) pmin = rho;
+    if (rho > pmax) pmax = rho;
+    if (r < 1.0 - eps_lo || r > 1.0 + eps_hi) outside += 1.0;
+    count += 1.0;
+  }
+  out[0] = sr;
+  out[1] = rmin;
+  out[2] = rmax;
+  out[3] = sp;
+  out[4] = pmin;
+  out[5] = pmax;
+  out[6] = outside;
+  out[7] = count;
+}
+
 /* ---- forward only: the action's log-prob and the policy entropy ---------- */
 
 /* Per token row t in [row_begin, row_end): l_t = z[a_t] - lse(z) (the
@@ -353,6 +444,7 @@ void oracle_vocab_shard_stats(const void* logits, int dtype, int64_t V_shard, in
   }
 }
 
+/* Threads the row loop runs on (for reporting the oracle's timing). */
 int oracle_threads(void) { return omp_get_max_threads(); }
 
 /* Sets the OpenMP thread count of later calls (results do not depend on it). */
