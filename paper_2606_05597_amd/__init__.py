@@ -30,22 +30,84 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _dev(t, name):
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be a GPU tensor (no CPU path)")
-    if not t.is_contiguous():
-        raise ValueError(f"{name} must be contiguous")
+# Argument checks run in two stages, so that each is seen whatever the other would say: first every tensor's dtype
+# and size (_meta), then where the tensors live (_placed: GPU, the inputs' device, contiguous).  Nothing reaches the
+# library before both pass, so the library is never handed a host pointer or a buffer it would overrun.
+
+def _meta(t, name, dtype, n=None, shape=None, optional=False):
+    """dtype and size of a caller tensor: dtype (None = any), at least n elements, or exactly this shape."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if n is not None and t.numel() < n:
+        raise ValueError(f"{name} must hold at least {n} elements, got {t.numel()}")
     return t
 
 
+def _placed(device, strided=(), **tensors):
+    """Every tensor given is on the GPU, on `device`, and contiguous (those named in `strided` only need a unit
+    column stride, checked with their shape)."""
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor (no CPU path)")
+        if t.device != device:
+            raise ValueError(f"{name} must be on {device} (the inputs' device), got {t.device}")
+        if name not in strided and not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+
+def _logits2d(logits, name="logits"):
+    """dtype code, rows and row stride of a [T, ld] logits tensor with unit column stride."""
+    _meta(logits, name, None)
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError(f"{name} must be [T, ld] with unit column stride")
+    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
+    if dt is None:
+        raise TypeError(f"{name} must be bfloat16 or float32")
+    T = logits.shape[0]
+    ld = logits.stride(0) if T > 0 else logits.shape[1]
+    return dt, T, ld
+
+
+def _hidden_w(hidden, w, w_name):
+    """(T, H, V) of bf16 hidden [T, H] and weight [H, V]."""
+    _meta(hidden, "hidden", torch.bfloat16)
+    _meta(w, w_name, torch.bfloat16)
+    if hidden.dim() != 2 or w.dim() != 2:
+        raise ValueError(f"hidden and {w_name} must be 2-D")
+    T, H = hidden.shape
+    H2, V = w.shape
+    if H2 != H:
+        raise ValueError(f"hidden and {w_name} disagree on H")
+    return T, H, V
+
+
+def _dlogits_arg(dlogits, logits):
+    if dlogits is True:
+        return torch.empty_like(logits)
+    if dlogits is False or dlogits is None:
+        return None
+    _meta(dlogits, "dlogits", logits.dtype)
+    if dlogits.shape != logits.shape or dlogits.stride() != logits.stride():
+        raise ValueError("dlogits must match logits in shape, stride and dtype")
+    return dlogits
+
+
 def _workspace(workspace, need, device):
-    """The caller's workspace (a contiguous tensor of any dtype on the inputs' device; its size in bytes is what the
-    library is told) or a new one of ``need`` bytes."""
+    """The caller's workspace (a contiguous GPU tensor of any dtype on the inputs' device; its size in bytes is what
+    the library is told, and the library refuses one that is too small) or a new one of ``need`` bytes."""
     if workspace is None:
         return torch.empty(max(int(need), 1), dtype=torch.uint8, device=device)
-    _dev(workspace, "workspace")
-    if workspace.device != torch.device(device):
-        raise ValueError("workspace must be on the inputs' device")
+    _placed(device, workspace=workspace)
     return workspace
 
 
@@ -57,9 +119,8 @@ def _loss_out(loss_out, device):
     """The caller's fp64 loss scalar on the inputs' device, or a new one."""
     if loss_out is None:
         return torch.empty(1, dtype=torch.float64, device=device)
-    _dev(loss_out, "loss_out")
-    if loss_out.dtype != torch.float64 or loss_out.numel() < 1 or loss_out.device != torch.device(device):
-        raise ValueError("loss_out must be a float64 GPU tensor of at least one element on the inputs' device")
+    _meta(loss_out, "loss_out", torch.float64, n=1)
+    _placed(device, loss_out=loss_out)
     return loss_out
 
 
@@ -73,6 +134,10 @@ def _check(status, what):
         raise GrpoError(status, what)
 
 
+def _n_traj(traj_step_off):
+    return max(traj_step_off.numel() - 1, 0)
+
+
 def grpo_status_str(status: int) -> str:
     return _lib.status_str(status)
 
@@ -80,10 +145,10 @@ def grpo_status_str(status: int) -> str:
 def grpo_advantages(rewards: torch.Tensor, group_size: int, ddof: int = 1, std_eps: float = 0.0,
                     out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Group-relative advantages A_i (fp32 [N]) from rewards (fp32 [N])."""
-    _dev(rewards, "rewards")
-    if rewards.dtype != torch.float32:
-        raise TypeError("rewards must be float32")
-    out = torch.empty_like(rewards) if out is None else _dev(out, "out")
+    _meta(rewards, "rewards", torch.float32)
+    _meta(out, "out", torch.float32, n=rewards.numel(), optional=True)
+    _placed(rewards.device, rewards=rewards, out=out)
+    out = torch.empty_like(rewards) if out is None else out
     st = _lib.load().grpo_advantages(_ptr(rewards), rewards.numel(), int(group_size), int(ddof), float(std_eps),
                                      _ptr(out), _stream(stream))
     _check(st, "grpo_advantages")
@@ -94,10 +159,10 @@ def grpo_advantages_ex(rewards: torch.Tensor, group_size: int, mode: int = GRPO_
                        std_eps: float = 0.0, out: torch.Tensor | None = None, mixed: bool = True, stream=None):
     """Advantages under ``mode`` (group-normalised, or the RAFT++ success filter) and, with ``mixed``, DAPO's
     mixed-group mask (int32 [N / G]) and count (int32 [1]).  Returns (adv, group_mixed or None, n_mixed or None)."""
-    _dev(rewards, "rewards")
-    if rewards.dtype != torch.float32:
-        raise TypeError("rewards must be float32")
-    out = torch.empty_like(rewards) if out is None else _dev(out, "out")
+    _meta(rewards, "rewards", torch.float32)
+    _meta(out, "out", torch.float32, n=rewards.numel(), optional=True)
+    _placed(rewards.device, rewards=rewards, out=out)
+    out = torch.empty_like(rewards) if out is None else out
     gm = nm = None
     if mixed:
         gm = torch.empty(max(rewards.numel() // max(int(group_size), 1), 1), dtype=torch.int32, device=rewards.device)
@@ -161,17 +226,23 @@ class LossAux:
         }
         return LossAux(**{k: mk[k]() for k in which})
 
-    def _c(self, T: int, n_traj: int):
+    _WANT = {"token_logp": torch.float32, "tok_traj": torch.int32, "traj_tok_off": torch.int32,
+             "gather_idx": torch.int64, "traj_loss": torch.float64, "clip_counts": torch.int64,
+             "ratio_stats": torch.float64, "error_flags": torch.int32}
+
+    def _meta(self, T: int, n_traj: int):
+        """dtype and size of every output given (checked with the other arguments' before any device check)."""
+        n = {"token_logp": T, "tok_traj": T, "traj_tok_off": n_traj + 1, "gather_idx": T, "traj_loss": n_traj,
+             "clip_counts": 2, "ratio_stats": 8, "error_flags": 1}
+        for name, dt in self._WANT.items():
+            _meta(getattr(self, name), f"aux.{name}", dt, n=n[name], optional=True)
+
+    def _c(self, T: int, n_traj: int, device):
         a = _lib.Aux()
-        want = {"token_logp": (torch.float32, T), "tok_traj": (torch.int32, T), "traj_tok_off": (torch.int32, n_traj + 1),
-                "gather_idx": (torch.int64, T), "traj_loss": (torch.float64, n_traj), "clip_counts": (torch.int64, 2),
-                "ratio_stats": (torch.float64, 8), "error_flags": (torch.int32, 1)}
-        for name, (dt, n) in want.items():
-            t = getattr(self, name)
-            if t is not None:
-                _dev(t, name)
-                if t.dtype != dt or t.numel() < n:
-                    raise ValueError(f"aux.{name} must be {dt} with at least {n} elements")
+        self._meta(T, n_traj)
+        got = {name: getattr(self, name) for name in self._WANT}
+        _placed(device, **{f"aux.{name}": t for name, t in got.items()})
+        for name, t in got.items():
             setattr(a, name, None if t is None else t.data_ptr())
         if self.hot_events is not None:
             a.hot_begin, a.hot_end = self.hot_events
@@ -179,17 +250,31 @@ class LossAux:
 
 
 def _segments(step_tok_off, traj_step_off, group_size):
-    _dev(step_tok_off, "step_tok_off")
-    _dev(traj_step_off, "traj_step_off")
-    if step_tok_off.dtype != torch.int32 or traj_step_off.dtype != torch.int32:
-        raise TypeError("offsets must be int32")
+    """The CSR offsets (int32) as a grpo_segments struct (their device is checked with the other tensors)."""
+    _meta(step_tok_off, "step_tok_off", torch.int32, n=1)
+    _meta(traj_step_off, "traj_step_off", torch.int32, n=1)
     seg = _lib.Segments()
-    seg.n_traj = traj_step_off.numel() - 1
+    seg.n_traj = _n_traj(traj_step_off)
     seg.group_size = int(group_size)
     seg.n_steps = step_tok_off.numel() - 1
     seg.step_tok_off = step_tok_off.data_ptr()
     seg.traj_step_off = traj_step_off.data_ptr()
     return seg
+
+
+def _outputs_meta(T, n_traj, aux, loss_out):
+    """dtypes and sizes of a loss call's optional outputs."""
+    if aux is not None:
+        aux._meta(T, n_traj)
+    _meta(loss_out, "loss_out", torch.float64, n=1, optional=True)
+
+
+def _token_inputs(T, n_traj, actions, behave_logp, prox_logp, adv):
+    """dtypes and sizes of the per-token and per-trajectory inputs of a loss call."""
+    _meta(actions, "actions", torch.int32, n=T)
+    _meta(behave_logp, "behave_logp", torch.float32, n=T)
+    _meta(prox_logp, "prox_logp", torch.float32, n=T, optional=True)
+    _meta(adv, "adv", torch.float32, n=n_traj)
 
 
 def _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total):
@@ -202,15 +287,6 @@ def _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
     p.grad_scale = float(grad_scale)
     p.n_groups_total = float(n_groups_total)
     return p
-
-
-def _f32(t, name):
-    if t is None:
-        return None
-    _dev(t, name)
-    if t.dtype != torch.float32:
-        raise TypeError(f"{name} must be float32")
-    return t
 
 
 def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: torch.Tensor, adv: torch.Tensor,
@@ -226,37 +302,26 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
     forward only; a tensor is written in place (it may be ``logits`` itself).
     Returns (loss [1] fp64, dlogits or None).
     """
-    if logits.dim() != 2 or logits.stride(1) != 1:
-        raise ValueError("logits must be [T, ld] with unit column stride")
-    if not logits.is_cuda:
-        raise ValueError("logits must be a GPU tensor (no CPU path)")
-    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
-    if dt is None:
-        raise TypeError("logits must be bfloat16 or float32")
-    T = logits.shape[0]
-    ld = logits.stride(0) if T > 0 else logits.shape[1]
+    dt, T, ld = _logits2d(logits)
     Vv = logits.shape[1] if V is None else int(V)
-    _dev(actions, "actions")
-    if actions.dtype != torch.int32:
-        raise TypeError("actions must be int32")
     seg = _segments(step_tok_off, traj_step_off, group_size)
+    _token_inputs(T, seg.n_traj, actions, behave_logp, prox_logp, adv)
     par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
-    if dlogits is True:
-        dlogits = torch.empty_like(logits)
-    elif dlogits is False:
-        dlogits = None
-    if dlogits is not None and (dlogits.shape != logits.shape or dlogits.stride() != logits.stride()
-                                or dlogits.dtype != logits.dtype):
-        raise ValueError("dlogits must match logits in shape, stride and dtype")
+    dlogits = _dlogits_arg(dlogits, logits) if dlogits is not True else True
+    _outputs_meta(T, seg.n_traj, aux, loss_out)
+    dev = logits.device
+    _placed(dev, strided=("logits", "dlogits"), logits=logits, dlogits=None if dlogits is True else dlogits,
+            actions=actions, behave_logp=behave_logp, prox_logp=prox_logp, adv=adv, step_tok_off=step_tok_off,
+            traj_step_off=traj_step_off)
+    ca = aux._c(T, seg.n_traj, dev) if aux is not None else None
     need = grpo_loss_workspace_bytes(T, seg.n_traj)
-    workspace = _workspace(workspace, need, logits.device)
-    loss_out = _loss_out(loss_out, logits.device)
-    ca = aux._c(T, seg.n_traj) if aux is not None else None
+    workspace = _workspace(workspace, need, dev)
+    loss_out = _loss_out(loss_out, dev)
+    dlogits = _dlogits_arg(dlogits, logits)
     st = _lib.load().grpo_loss_fwd_bwd(
-        _ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
-        _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
-        _ptr(loss_out), _ptr(dlogits), ctypes.byref(ca) if ca is not None else None, _ptr(workspace),
-        _nbytes(workspace), _stream(stream))
+        _ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(behave_logp), _ptr(prox_logp), _ptr(adv),
+        ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dlogits),
+        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "grpo_loss_fwd_bwd")
     return loss_out, dlogits
 
@@ -264,31 +329,27 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
 def _fused_call(entry: str, ws_bytes, hidden, w_lm, actions, behave_logp, adv, step_tok_off, traj_step_off,
                 group_size, sched, prox_logp, norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total,
                 dhidden, dw_lm, accumulate_dw, aux, workspace, loss_out, stream, extra=()):
-    _dev(hidden, "hidden")
-    _dev(w_lm, "w_lm")
-    if hidden.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
-        raise TypeError("hidden and w_lm must be bfloat16")
-    T, H = hidden.shape
-    H2, V = w_lm.shape
-    if H2 != H:
-        raise ValueError("hidden and w_lm disagree on H")
-    _dev(actions, "actions")
+    T, H, V = _hidden_w(hidden, w_lm, "w_lm")
     seg = _segments(step_tok_off, traj_step_off, group_size)
+    _token_inputs(T, seg.n_traj, actions, behave_logp, prox_logp, adv)
     par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
+    _meta(dhidden, "dhidden", torch.bfloat16, shape=(T, H), optional=True)
+    _meta(dw_lm, "dw_lm", torch.float32, n=H * V, optional=True)
+    _outputs_meta(T, seg.n_traj, aux, loss_out)
+    dev = hidden.device
+    _placed(dev, hidden=hidden, w_lm=w_lm, actions=actions, behave_logp=behave_logp, prox_logp=prox_logp, adv=adv,
+            step_tok_off=step_tok_off, traj_step_off=traj_step_off, dhidden=dhidden, dw_lm=dw_lm)
+    ca = aux._c(T, seg.n_traj, dev) if aux is not None else None
     if dhidden is None:
         dhidden = torch.empty_like(hidden)
     if dw_lm is None:
-        dw_lm = torch.empty((H, V), dtype=torch.float32, device=hidden.device)
-    _dev(dhidden, "dhidden")
-    _dev(dw_lm, "dw_lm")
+        dw_lm = torch.empty((H, V), dtype=torch.float32, device=dev)
     need = ws_bytes(T, H, V, sched, seg.n_traj)
-    workspace = _workspace(workspace, need, hidden.device)
-    loss_out = _loss_out(loss_out, hidden.device)
-    ca = aux._c(T, seg.n_traj) if aux is not None else None
+    workspace = _workspace(workspace, need, dev)
+    loss_out = _loss_out(loss_out, dev)
     st = getattr(_lib.load(), entry)(
-        _ptr(hidden), _ptr(w_lm), T, H, V, int(sched), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
-        _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
-        _ptr(loss_out), _ptr(dhidden), _ptr(dw_lm), int(bool(accumulate_dw)),
+        _ptr(hidden), _ptr(w_lm), T, H, V, int(sched), _ptr(actions), _ptr(behave_logp), _ptr(prox_logp), _ptr(adv),
+        ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dhidden), _ptr(dw_lm), int(bool(accumulate_dw)),
         ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace), _stream(stream), *extra)
     _check(st, entry)
     return loss_out, dhidden, dw_lm
@@ -346,23 +407,13 @@ def grpo_token_logp(logits: torch.Tensor, actions: torch.Tensor, *, V: int | Non
     ``logits`` is [T, ld] (bf16 or fp32, unit column stride); V defaults to the column count.
     ``error_flags`` (int32 [1], optional) receives GRPO_FLAG_* bits.  Returns (logp, entropy or None).
     """
-    if logits.dim() != 2 or logits.stride(1) != 1:
-        raise ValueError("logits must be [T, ld] with unit column stride")
-    if not logits.is_cuda:
-        raise ValueError("logits must be a GPU tensor (no CPU path)")
-    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
-    if dt is None:
-        raise TypeError("logits must be bfloat16 or float32")
-    T = logits.shape[0]
-    ld = logits.stride(0) if T > 0 else logits.shape[1]
+    dt, T, ld = _logits2d(logits)
     Vv = logits.shape[1] if V is None else int(V)
-    _dev(actions, "actions")
-    if actions.dtype != torch.int32:
-        raise TypeError("actions must be int32")
+    _meta(actions, "actions", torch.int32, n=T)
+    _meta(error_flags, "error_flags", torch.int32, n=1, optional=True)
+    _placed(logits.device, strided=("logits",), logits=logits, actions=actions, error_flags=error_flags)
     logp = torch.empty(T, dtype=torch.float32, device=logits.device)
     ent = torch.empty(T, dtype=torch.float32, device=logits.device) if entropy else None
-    if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
-        raise ValueError("error_flags must be an int32 GPU tensor")
     st = _lib.load().grpo_token_logp(_ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(logp), _ptr(ent),
                                      _ptr(error_flags), _stream(stream))
     _check(st, "grpo_token_logp")
@@ -378,24 +429,16 @@ def fused_lmhead_token_logp(hidden: torch.Tensor, w_lm: torch.Tensor, actions: t
     """Forward only from hidden states: the action's log-prob (fp32 [T]) and, if ``entropy``, the policy entropy
     (fp32 [T]) of softmax(h W) per token, without storing the logits.  Returns (token_logp, token_entropy or
     None)."""
-    _dev(hidden, "hidden")
-    _dev(w_lm, "w_lm")
-    if hidden.dtype != torch.bfloat16 or w_lm.dtype != torch.bfloat16:
-        raise TypeError("hidden and w_lm must be bfloat16")
-    T, H = hidden.shape
-    H2, V = w_lm.shape
-    if H2 != H:
-        raise ValueError("hidden and w_lm disagree on H")
-    _dev(actions, "actions")
-    if actions.dtype != torch.int32:
-        raise TypeError("actions must be int32")
-    if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
-        raise ValueError("error_flags must be an int32 GPU tensor")
+    T, H, V = _hidden_w(hidden, w_lm, "w_lm")
+    _meta(actions, "actions", torch.int32, n=T)
+    _meta(error_flags, "error_flags", torch.int32, n=1, optional=True)
+    dev = hidden.device
+    _placed(dev, hidden=hidden, w_lm=w_lm, actions=actions, error_flags=error_flags)
     lib = _lib.load()
     need = int(lib.fused_lmhead_token_logp_workspace_bytes(T, H, V))
-    workspace = _workspace(workspace, need, hidden.device)
-    logp = torch.empty(T, dtype=torch.float32, device=hidden.device)
-    ent = torch.empty(T, dtype=torch.float32, device=hidden.device) if entropy else None
+    workspace = _workspace(workspace, need, dev)
+    logp = torch.empty(T, dtype=torch.float32, device=dev)
+    ent = torch.empty(T, dtype=torch.float32, device=dev) if entropy else None
     st = lib.fused_lmhead_token_logp(_ptr(hidden), _ptr(w_lm), T, H, V, _ptr(actions), _ptr(logp), _ptr(ent),
                                      _ptr(error_flags), _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(st, "fused_lmhead_token_logp")
@@ -408,35 +451,18 @@ def vocab_stats_fields(stats: torch.Tensor):
     return f64[..., 0], f64[..., 2], f64[..., 1]
 
 
-def _logits2d(logits, name="logits"):
-    if logits.dim() != 2 or logits.stride(1) != 1:
-        raise ValueError(f"{name} must be [T, ld] with unit column stride")
-    if not logits.is_cuda:
-        raise ValueError(f"{name} must be a GPU tensor (no CPU path)")
-    dt = {torch.bfloat16: GRPO_BF16, torch.float32: GRPO_F32}.get(logits.dtype)
-    if dt is None:
-        raise TypeError(f"{name} must be bfloat16 or float32")
-    T = logits.shape[0]
-    ld = logits.stride(0) if T > 0 else logits.shape[1]
-    return dt, T, ld
-
-
 def grpo_vocab_shard_stats(logits: torch.Tensor, actions: torch.Tensor, v_begin: int, *, V: int | None = None,
                            stats: torch.Tensor | None = None, error_flags: torch.Tensor | None = None, stream=None):
     """Step 1 of the vocabulary-sharded loss: each row of the shard (global columns [v_begin, v_begin + V)) reduced
     to its record.  Returns uint8 [T, 24] records (read them with ``vocab_stats_fields``)."""
     dt, T, ld = _logits2d(logits)
     Vv = logits.shape[1] if V is None else int(V)
-    _dev(actions, "actions")
-    if actions.dtype != torch.int32:
-        raise TypeError("actions must be int32")
+    _meta(actions, "actions", torch.int32, n=T)
+    _meta(stats, "stats", torch.uint8, shape=(T, VOCAB_STATS_BYTES), optional=True)
+    _meta(error_flags, "error_flags", torch.int32, n=1, optional=True)
+    _placed(logits.device, strided=("logits",), logits=logits, actions=actions, stats=stats, error_flags=error_flags)
     if stats is None:
         stats = torch.empty((T, VOCAB_STATS_BYTES), dtype=torch.uint8, device=logits.device)
-    _dev(stats, "stats")
-    if stats.dtype != torch.uint8 or tuple(stats.shape) != (T, VOCAB_STATS_BYTES):
-        raise ValueError(f"stats must be uint8 [T, {VOCAB_STATS_BYTES}]")
-    if error_flags is not None and (error_flags.dtype != torch.int32 or not error_flags.is_cuda):
-        raise ValueError("error_flags must be an int32 GPU tensor")
     st = _lib.load().grpo_vocab_shard_stats(_ptr(logits), dt, T, Vv, ld, int(v_begin), _ptr(actions), _ptr(stats),
                                             _ptr(error_flags), _stream(stream))
     _check(st, "grpo_vocab_shard_stats")
@@ -460,33 +486,35 @@ def grpo_loss_fwd_bwd_vocab_shard(logits: torch.Tensor, stats_all: torch.Tensor,
     """
     dt, T, ld = _logits2d(logits)
     Vv = logits.shape[1] if V is None else int(V)
-    _dev(actions, "actions")
-    if actions.dtype != torch.int32:
-        raise TypeError("actions must be int32")
-    _dev(stats_all, "stats_all")
-    if stats_all.dtype != torch.uint8 or stats_all.dim() != 3 or tuple(stats_all.shape[1:]) != (T, VOCAB_STATS_BYTES):
-        raise ValueError(f"stats_all must be uint8 [n_shards, T, {VOCAB_STATS_BYTES}]")
+    _stats_all(stats_all, T)
     n_shards = stats_all.shape[0]
     seg = _segments(step_tok_off, traj_step_off, group_size)
+    _token_inputs(T, seg.n_traj, actions, behave_logp, prox_logp, adv)
     par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
-    if dlogits is True:
-        dlogits = torch.empty_like(logits)
-    elif dlogits is False:
-        dlogits = None
-    if dlogits is not None and (dlogits.shape != logits.shape or dlogits.stride() != logits.stride()
-                                or dlogits.dtype != logits.dtype):
-        raise ValueError("dlogits must match logits in shape, stride and dtype")
+    dlogits = _dlogits_arg(dlogits, logits) if dlogits is not True else True
+    _outputs_meta(T, seg.n_traj, aux, loss_out)
+    dev = logits.device
+    _placed(dev, strided=("logits", "dlogits"), logits=logits, dlogits=None if dlogits is True else dlogits,
+            stats_all=stats_all, actions=actions, behave_logp=behave_logp, prox_logp=prox_logp, adv=adv,
+            step_tok_off=step_tok_off, traj_step_off=traj_step_off)
+    ca = aux._c(T, seg.n_traj, dev) if aux is not None else None
     need = grpo_loss_workspace_bytes(T, seg.n_traj)
-    workspace = _workspace(workspace, need, logits.device)
-    loss_out = _loss_out(loss_out, logits.device)
-    ca = aux._c(T, seg.n_traj) if aux is not None else None
+    workspace = _workspace(workspace, need, dev)
+    loss_out = _loss_out(loss_out, dev)
+    dlogits = _dlogits_arg(dlogits, logits)
     st = _lib.load().grpo_loss_fwd_bwd_vocab_shard(
         _ptr(logits), dt, T, Vv, ld, int(v_begin), int(V_total), _ptr(stats_all), int(n_shards), _ptr(actions),
-        _ptr(_f32(behave_logp, "behave_logp")), _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")),
-        ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dlogits),
-        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace), _stream(stream))
+        _ptr(behave_logp), _ptr(prox_logp), _ptr(adv), ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out),
+        _ptr(dlogits), ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace),
+        _stream(stream))
     _check(st, "grpo_loss_fwd_bwd_vocab_shard")
     return loss_out, dlogits
+
+
+def _stats_all(stats_all, T):
+    _meta(stats_all, "stats_all", torch.uint8)
+    if stats_all.dim() != 3 or tuple(stats_all.shape[1:]) != (T, VOCAB_STATS_BYTES):
+        raise ValueError(f"stats_all must be uint8 [n_shards, T, {VOCAB_STATS_BYTES}]")
 
 
 def vocab_shard_logits_buffer(T: int, V_shard: int, device) -> torch.Tensor:
@@ -495,11 +523,9 @@ def vocab_shard_logits_buffer(T: int, V_shard: int, device) -> torch.Tensor:
     return torch.empty(max(n, 1), dtype=torch.float32, device=device)
 
 
-def _check_logits_buffer(buf: torch.Tensor, T: int, V_shard: int):
-    _dev(buf, "logits buffer")
+def _check_logits_buffer(buf: torch.Tensor, T: int, V_shard: int, name: str):
     need = int(_lib.load().fused_lmhead_vocab_shard_logits_bytes(int(T), int(V_shard)))
-    if buf.dtype != torch.float32 or not buf.is_contiguous() or buf.numel() * 4 < need:
-        raise ValueError(f"the logits buffer must be contiguous float32 of at least {need} bytes")
+    _meta(buf, name, torch.float32, n=(need + 3) // 4)
 
 
 def fused_lmhead_vocab_shard_stats(hidden: torch.Tensor, w_shard: torch.Tensor, actions: torch.Tensor, v_begin: int,
@@ -509,25 +535,18 @@ def fused_lmhead_vocab_shard_stats(hidden: torch.Tensor, w_shard: torch.Tensor, 
     V_shard)) reduced to its record.  Returns uint8 [T, 24] records (read them with ``vocab_stats_fields``).
     ``logits_out`` (fp32, ``fused_lmhead_vocab_shard_logits_bytes(T, V_shard) / 4`` elements, see
     ``vocab_shard_logits_buffer``) also receives the shard's logits for step 2."""
-    _dev(hidden, "hidden")
-    _dev(w_shard, "w_shard")
-    if hidden.dtype != torch.bfloat16 or w_shard.dtype != torch.bfloat16:
-        raise TypeError("hidden and w_shard must be bfloat16")
-    T, H = hidden.shape
-    H2, Vs = w_shard.shape
-    if H2 != H:
-        raise ValueError("hidden and w_shard disagree on H")
-    _dev(actions, "actions")
+    T, H, Vs = _hidden_w(hidden, w_shard, "w_shard")
+    _meta(actions, "actions", torch.int32, n=T)
+    _meta(stats, "stats", torch.uint8, shape=(T, VOCAB_STATS_BYTES), optional=True)
+    if logits_out is not None:
+        _check_logits_buffer(logits_out, T, Vs, "logits_out")
+    dev = hidden.device
+    _placed(dev, hidden=hidden, w_shard=w_shard, actions=actions, stats=stats, logits_out=logits_out)
     if stats is None:
-        stats = torch.empty((T, VOCAB_STATS_BYTES), dtype=torch.uint8, device=hidden.device)
-    _dev(stats, "stats")
-    if stats.dtype != torch.uint8 or tuple(stats.shape) != (T, VOCAB_STATS_BYTES):
-        raise ValueError(f"stats must be uint8 [T, {VOCAB_STATS_BYTES}]")
+        stats = torch.empty((T, VOCAB_STATS_BYTES), dtype=torch.uint8, device=dev)
     lib = _lib.load()
     need = lib.fused_lmhead_vocab_shard_stats_workspace_bytes(T, H, Vs)
-    workspace = _workspace(workspace, need, hidden.device)
-    if logits_out is not None:
-        _check_logits_buffer(logits_out, T, Vs)
+    workspace = _workspace(workspace, need, dev)
     st = lib.fused_lmhead_vocab_shard_stats(_ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), _ptr(actions),
                                             _ptr(stats), _ptr(logits_out), _ptr(workspace), _nbytes(workspace),
                                             _stream(stream))
@@ -550,40 +569,33 @@ def fused_lmhead_grpo_vocab_shard(hidden: torch.Tensor, w_shard: torch.Tensor, s
     [T, H], to be summed over the shards) and its dW columns (fp32 [H, V_shard]), from every shard's records
     ``stats_all`` (uint8 [n_shards, T, 24], in shard order).  With ``logits_in`` (the buffer step 1 filled), D
     comes from the kept logits instead of a recomputed product.  Returns (loss, dhidden_partial, dw_shard)."""
-    _dev(hidden, "hidden")
-    _dev(w_shard, "w_shard")
-    if hidden.dtype != torch.bfloat16 or w_shard.dtype != torch.bfloat16:
-        raise TypeError("hidden and w_shard must be bfloat16")
-    T, H = hidden.shape
-    H2, Vs = w_shard.shape
-    if H2 != H:
-        raise ValueError("hidden and w_shard disagree on H")
-    _dev(actions, "actions")
-    _dev(stats_all, "stats_all")
-    if stats_all.dtype != torch.uint8 or stats_all.dim() != 3 or tuple(stats_all.shape[1:]) != (T, VOCAB_STATS_BYTES):
-        raise ValueError(f"stats_all must be uint8 [n_shards, T, {VOCAB_STATS_BYTES}]")
+    T, H, Vs = _hidden_w(hidden, w_shard, "w_shard")
+    _stats_all(stats_all, T)
     seg = _segments(step_tok_off, traj_step_off, group_size)
+    _token_inputs(T, seg.n_traj, actions, behave_logp, prox_logp, adv)
     par = _params(norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total)
-    if dhidden_partial is None:
-        dhidden_partial = torch.empty((T, H), dtype=torch.float32, device=hidden.device)
-    if dw_shard is None:
-        dw_shard = torch.empty((H, Vs), dtype=torch.float32, device=hidden.device)
-    _dev(dhidden_partial, "dhidden_partial")
-    _dev(dw_shard, "dw_shard")
-    if dhidden_partial.dtype != torch.float32 or dw_shard.dtype != torch.float32:
-        raise TypeError("dhidden_partial and dw_shard must be float32")
+    _meta(dhidden_partial, "dhidden_partial", torch.float32, shape=(T, H), optional=True)
+    _meta(dw_shard, "dw_shard", torch.float32, n=H * Vs, optional=True)
     if logits_in is not None:
-        _check_logits_buffer(logits_in, T, Vs)
+        _check_logits_buffer(logits_in, T, Vs, "logits_in")
         vocab_chunk = (Vs + 255) // 256 * 256  # the whole shard as one chunk
+    _outputs_meta(T, seg.n_traj, aux, loss_out)
+    dev = hidden.device
+    _placed(dev, hidden=hidden, w_shard=w_shard, stats_all=stats_all, actions=actions, behave_logp=behave_logp,
+            prox_logp=prox_logp, adv=adv, step_tok_off=step_tok_off, traj_step_off=traj_step_off,
+            dhidden_partial=dhidden_partial, dw_shard=dw_shard, logits_in=logits_in)
+    ca = aux._c(T, seg.n_traj, dev) if aux is not None else None
+    if dhidden_partial is None:
+        dhidden_partial = torch.empty((T, H), dtype=torch.float32, device=dev)
+    if dw_shard is None:
+        dw_shard = torch.empty((H, Vs), dtype=torch.float32, device=dev)
     need = fused_lmhead_workspace_bytes(T, H, Vs, vocab_chunk, seg.n_traj)
-    workspace = _workspace(workspace, need, hidden.device)
-    loss_out = _loss_out(loss_out, hidden.device)
-    ca = aux._c(T, seg.n_traj) if aux is not None else None
+    workspace = _workspace(workspace, need, dev)
+    loss_out = _loss_out(loss_out, dev)
     st = _lib.load().fused_lmhead_grpo_vocab_shard(
         _ptr(hidden), _ptr(w_shard), T, H, Vs, int(v_begin), int(V_total), int(vocab_chunk), _ptr(stats_all),
-        int(stats_all.shape[0]), _ptr(actions), _ptr(_f32(behave_logp, "behave_logp")),
-        _ptr(_f32(prox_logp, "prox_logp")), _ptr(_f32(adv, "adv")), ctypes.byref(seg), ctypes.byref(par),
-        _ptr(loss_out), _ptr(dhidden_partial), _ptr(dw_shard), int(bool(accumulate_dw)),
+        int(stats_all.shape[0]), _ptr(actions), _ptr(behave_logp), _ptr(prox_logp), _ptr(adv), ctypes.byref(seg),
+        ctypes.byref(par), _ptr(loss_out), _ptr(dhidden_partial), _ptr(dw_shard), int(bool(accumulate_dw)),
         ctypes.byref(ca) if ca is not None else None, _ptr(logits_in), _ptr(workspace), _nbytes(workspace),
         _stream(stream))
     _check(st, "fused_lmhead_grpo_vocab_shard")

@@ -64,4 +64,15 @@ inline double n_groups_of(const grpo_segments* seg, const grpo_loss_params* p) {
 
 inline bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr % a) == 0; }
 
+// Compute units of the device the stream belongs to (which need not be the current device), or 0 if the
+// runtime cannot say.
+inline int stream_cu_count(hipStream_t s) {
+  hipDevice_t dev = 0;
+  int n_cu = 0;
+  if (hipStreamGetDevice(s, &dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+    return 0;
+  return n_cu;
+}
+
 }  // namespace grpo

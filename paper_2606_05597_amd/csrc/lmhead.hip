@@ -1097,15 +1097,12 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     // CU, so that each CU holds one of each: the forward product's workgroup leaves room in LDS and registers
     // for one D-pass workgroup.  ev_c: block b's rows are combined and the previous backward launch (the last
     // reader of D, D^T) is done; ev_d: block b's D pass is done.
-    int n_cu = 0;  // of the streams' device, which need not be the current one
-    hipDevice_t dev = 0;
-    if (hipStreamGetDevice(s, &dev) != hipSuccess ||
-        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      return GRPO_ERR_HIP;
+    const int n_cu = stream_cu_count(s);  // of the streams' device, which need not be the current one
+    if (n_cu < 1) return GRPO_ERR_HIP;
     hipEvent_t ev_c = nullptr, ev_d = nullptr;
     if (hipEventCreateWithFlags(&ev_c, hipEventDisableTiming) != hipSuccess) return GRPO_ERR_HIP;
     if (hipEventCreateWithFlags(&ev_d, hipEventDisableTiming) != hipSuccess) {
-      hipEventDestroy(ev_c);
+      (void)hipEventDestroy(ev_c);
       return GRPO_ERR_HIP;
     }
     bool ok = true;
@@ -1129,8 +1126,8 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     }
     ok = ok && hipGetLastError() == hipSuccess;
     // released by the runtime once the work that uses them has run
-    hipEventDestroy(ev_c);
-    hipEventDestroy(ev_d);
+    (void)hipEventDestroy(ev_c);
+    (void)hipEventDestroy(ev_d);
     if (!ok) return GRPO_ERR_HIP;
   }
   if (timed && hipEventRecord(aux->hot_end, s) != hipSuccess) return GRPO_ERR_HIP;

@@ -419,17 +419,15 @@ struct Launch {
 };
 
 static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const void* logits,
-                              const void* dlogits) {
+                              const void* dlogits, hipStream_t s) {
   const int epv = (dt == GRPO_BF16) ? 8 : 4;
   const bool vec_ok = (V % epv == 0) && (ld % epv == 0) && aligned(logits, 16) && aligned(dlogits, 16);
   if (vec_ok) {
     const int64_t nvec = V / epv;
     const int64_t nv = (nvec + 1023) / 1024;
     if (dt == GRPO_BF16 && nv >= kPipeMinNV && nv <= kPipeMaxNV && T <= kPipeMaxT) {
-      int dev = 0, n_cu = 0;
-      if (hipGetDevice(&dev) != hipSuccess ||
-          hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
-        n_cu = 256;
+      int n_cu = stream_cu_count(s);  // of the stream's device
+      if (n_cu < 1) n_cu = 256;
       const int64_t g = T < n_cu ? T : n_cu;  // one workgroup per CU (LDS bound)
       return Launch{kPipe[nv - kPipeMinNV], 1024, (unsigned)g};
     }
@@ -475,7 +473,7 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
     a.ld = ld;
     a.T = (int)T;
     a.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L, aux);
-    const Launch k = pick_row_kernel(dt, T, V, ld, logits, dlogits);
+    const Launch k = pick_row_kernel(dt, T, V, ld, logits, dlogits, s);
     const bool timed = aux && aux->hot_begin && aux->hot_end;
     if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
     if (k.k) {

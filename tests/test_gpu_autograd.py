@@ -1,5 +1,7 @@
 """The torch.autograd wrappers (GrpoLoss, FusedLmHeadGrpoLoss): loss.backward() hands back exactly the gradients
-the entry points return for the same inputs, and an upstream gradient other than 1 scales them."""
+the entry points return for the same inputs, an upstream gradient other than 1 scales them on the device (the
+default "scale" mode), and in "unit" mode the saved gradients come back as the library wrote them.  Neither mode
+reads the upstream gradient on the host."""
 import numpy as np
 import pytest
 import torch
@@ -35,6 +37,13 @@ def test_grpo_loss_autograd_matches_entry_point():
     (2.0 * grpo.GrpoLoss.apply(x2, b["actions"], b["behave"], adv, sto, tso, cfg.G, opts)).backward()
     torch.cuda.synchronize()
     assert torch.equal(x2.grad, want_dl * 2)
+    # "unit": the caller guarantees an upstream gradient of 1, the gradient is the entry point's own tensor
+    x3 = b["logits"].clone().requires_grad_(True)
+    grpo.GrpoLoss.apply(x3, b["actions"], b["behave"], adv, sto, tso, cfg.G, dict(opts, upstream="unit")).backward()
+    torch.cuda.synchronize()
+    assert torch.equal(x3.grad, want_dl)
+    with pytest.raises(ValueError, match="upstream"):
+        grpo.GrpoLoss.apply(x3, b["actions"], b["behave"], adv, sto, tso, cfg.G, dict(opts, upstream="host"))
 
 
 def test_grpo_loss_autograd_forward_only_without_grad():
@@ -72,6 +81,12 @@ def test_fused_autograd_matches_entry_point(opts):
     assert loss.item() == want_loss.item()
     assert torch.equal(h.grad, want_dh)
     assert w.grad.dtype == torch.bfloat16 and torch.equal(w.grad, want_dw.to(torch.bfloat16))
+    # an upstream gradient of 0.5 (exact) halves both gradients
+    h2 = b["hidden"].clone().requires_grad_(True)
+    w2 = b["W"].clone().requires_grad_(True)
+    (0.5 * grpo.FusedLmHeadGrpoLoss.apply(h2, w2, b["actions"], b["behave"], adv, sto, tso, cfg.G, opts)).backward()
+    torch.cuda.synchronize()
+    assert torch.equal(h2.grad, want_dh * 0.5) and torch.equal(w2.grad, (want_dw * 0.5).to(torch.bfloat16))
 
 
 def test_loss_from_rewards_equals_the_two_calls():

@@ -127,88 +127,173 @@ def test_clip_ranges(eps_low, eps_high):
         assert clipped == 0 and aux.clip_counts[0].item() == 0
 
 
+# ---------------------------------------------------------------- whole-batch oracle in row blocks
+
+def _oracle_all_rows(b, oi, norms, c=3.0, block=8192):
+    """The oracle's per-token outputs for every row of a batch too large for host memory at once, one normaliser
+    after the other: row blocks are copied to the host (the next one while the oracle works on the current one),
+    the first normaliser takes the log-softmax from the logits (loss_rows) and the others reuse its log-probs
+    (loss_from_logp).  Returns {norm: LossResult over all rows, without dlogits}."""
+    from concurrent.futures import ThreadPoolExecutor
+    cfg = b["cfg"]
+    T, V = len(oi["actions"]), b["V"]
+    parts = {n: [] for n in norms}
+    fetch = lambda r0: to_np_logits(b["logits"][r0:min(T, r0 + block)])  # noqa: E731
+    with ThreadPoolExecutor(1) as ex:
+        nxt = ex.submit(fetch, 0) if T > 0 else None
+        for r0 in range(0, T, block):
+            r1 = min(T, r0 + block)
+            zl = nxt.result()
+            if r1 < T:
+                nxt = ex.submit(fetch, r1)
+            kw = dict(k=cfg.k, dual_clip_c=c, row_begin=r0, row_end=r1)
+            first = oracle.loss_rows(zl, oi["actions"], oi["behave"], oi["prox"], oi["adv"], oi["seg"], cfg.G, V=V,
+                                     norm=norms[0], want_dlogits=False, row_offset=r0, **kw)
+            parts[norms[0]].append(first)
+            for n in norms[1:]:
+                parts[n].append(oracle.loss_from_logp(first.token_logp, oi["actions"], oi["behave"], oi["prox"],
+                                                      oi["adv"], oi["seg"], cfg.G, V=V, norm=n, **kw))
+            if (r0 // block) % 8 == 7:
+                print(f"  oracle rows {r1} of {T}", flush=True)
+    out = {}
+    n_traj = len(oi["seg"].traj_steps)
+    for n, ps in parts.items():
+        cat = lambda f, dt=np.float64: np.concatenate([getattr(q, f) for q in ps]) if ps else np.zeros(0, dt)  # noqa: E731
+        contrib = cat("token_contrib")
+        traj = np.bincount(oi["seg"].tok_traj, weights=contrib, minlength=n_traj) if T else np.zeros(n_traj)
+        out[n] = oracle.LossResult(math.fsum(contrib), traj, cat("token_logp"), contrib, cat("token_g"),
+                                   cat("token_state", np.int32), None, int(np.bitwise_or.reduce([q.flags for q in ps]))
+                                   if ps else 0)
+    return out
+
+
+def _whole_batch_checks(ref, loss, aux, oi, A64, V, ld, what):
+    """Every per-token and per-trajectory output and the whole loss against the oracle over all rows."""
+    T = len(oi["actions"])
+    kappa = ref.kappa
+    print(f"{what}: loss {loss!r} oracle {ref.loss!r} rel {abs(loss - ref.loss) / abs(ref.loss):.2e} "
+          f"kappa {kappa:.1f}", flush=True)
+    assert abs(loss - ref.loss) <= LOSS_RTOL * abs(ref.loss), (what, loss, ref.loss, kappa)
+    np.testing.assert_allclose(aux.traj_loss.cpu().numpy(), ref.traj_loss, rtol=LOSS_RTOL,
+                               atol=LOSS_RTOL * np.abs(ref.traj_loss).max(), err_msg=what)
+    assert np.abs(aux.token_logp.cpu().numpy() - ref.token_logp).max() <= LOGP_ATOL, what
+    kinks = kink_rows(ref, oi["behave"], oi["prox"], A64[oi["seg"].tok_traj], 0.2, 0.2, 3.0)
+    assert len(kinks) <= max(2, T // 1000), f"unexpectedly many kink rows: {len(kinks)}"
+    clip = aux.clip_counts.cpu().numpy()
+    assert abs(clip[0] - (ref.token_state & 1).sum()) <= len(kinks), what
+    assert abs(clip[1] - ((ref.token_state >> 1) & 1).sum()) <= len(kinks), what
+    valid = oracle.valid_tokens(oi["actions"], V, oi["seg"])
+    want = oracle.ratio_stats(ref.token_logp, oi["behave"], oi["prox"], valid)
+    got = aux.ratio_stats.cpu().numpy()
+    np.testing.assert_allclose(got[:6], want[:6], rtol=1e-5, err_msg=what)
+    assert abs(got[6] - want[6]) <= len(kinks) + 2 and got[7] == want[7], (what, got[6:], want[6:])
+    assert (aux.tok_traj.cpu().numpy() == oi["seg"].tok_traj).all()
+    assert (aux.traj_tok_off.cpu().numpy() == oi["seg"].traj_tok_off).all()
+    assert (aux.gather_idx.cpu().numpy() == oracle.gather_index(T, ld, oi["actions"])).all()
+    assert aux.error_flags.item() == ref.flags == 0
+    return kinks
+
+
+def _pipeline_rows(T, grid, rng, n_random):
+    """Rows to compare element by element: the first and last rows, each side of the first round boundaries of the
+    persistent row kernel (rows t >= grid are a workgroup's second and later rows, whose LDS part and registers were
+    loaded during the previous row's dlogits pass), the last full round, and random rows."""
+    fixed = [0, 1, grid - 1, grid, grid + 1, 2 * grid - 1, 2 * grid, 2 * grid + 1, 3 * grid + 17, 7 * grid + 100,
+             T // 2, T - grid - 1, T - grid, T - 2, T - 1]
+    rows = np.concatenate([fixed, rng.integers(0, T, n_random)])
+    return np.unique(rows[(rows >= 0) & (rows < T)])
+
+
+def _sampled_dlogits(b, dl, rows, oi, A64, norm, gs, scaled, what):
+    """dlogits of the sampled rows against the oracle's, row by row (grad_scale gs on both sides)."""
+    cfg = b["cfg"]
+    rows_t = torch.from_numpy(rows).to(dl.device)
+    zs = to_np_logits(b["logits"].index_select(0, rows_t))
+    dls = dl_to_f64(dl.index_select(0, rows_t)[:, :b["V"]])
+    worst = 0.0
+    for q, t in enumerate(rows):
+        ref = oracle.loss_rows(zs[q:q + 1], oi["actions"], oi["behave"], oi["prox"], oi["adv"], oi["seg"], cfg.G,
+                               V=b["V"], norm=norm, k=cfg.k, dual_clip_c=3.0, grad_scale=gs, row_begin=int(t),
+                               row_end=int(t) + 1, row_offset=int(t))
+        kinks = kink_rows(ref, oi["behave"][t:t + 1], None if oi["prox"] is None else oi["prox"][t:t + 1],
+                          A64[oi["seg"].tok_traj[t:t + 1]], 0.2, 0.2, 3.0)
+        worst = max(worst, check_dlogits(dls[q:q + 1], ref.dlogits, True, exempt=kinks, scaled=scaled,
+                                         what=f"{what} row {t}"))
+    return worst
+
+
 # ---------------------------------------------------------------- 32k vocabulary (bf16), full batch
 
 @pytest.mark.parametrize("norm", NORMS)
 def test_v32k_parity_full(norm):
+    # the register-resident kernel (256 threads x 16 vectors per row); every row's dlogits against the oracle's,
+    # at grad_scale 1 (absolute 2e-3) and rerun at grad_scale = 1/max|g_t| (the scaled bf16 gate)
     b = make_batch("v32k", "cuda")
     cfg = b["cfg"]
     A64, A32 = _adv(b)
     oi = oracle_inputs(b, A64)
-    zl = to_np_logits(b["logits"])
+    T, V = b["logits"].shape
+    ref = _oracle_all_rows(b, oi, [norm])[norm]
     loss, dl, aux = run_gpu(b, A32, norm=gpu_norm(norm), k=cfg.k, c=3.0)
-    T = len(oi["actions"])
-    # oracle in row blocks (fp64 dlogits of the whole batch would not fit in host memory at once)
-    contrib = np.empty(T)
-    logp = np.empty(T)
+    _whole_batch_checks(ref, loss, aux, oi, A64, V, V, f"v32k norm {norm}")
+    gs = float(np.float32(1.0 / np.abs(ref.token_g).max()))
+    loss2, dl2, _ = run_gpu(b, A32, norm=gpu_norm(norm), k=cfg.k, c=3.0, grad_scale=gs, aux=False)
+    assert loss2 == loss
+    zl = to_np_logits(b["logits"])
     worst = 0.0
     for r0 in range(0, T, 2048):
         r1 = min(T, r0 + 2048)
-        ref = oracle.loss_rows(zl[r0:r1], oi["actions"], oi["behave"], None, oi["adv"], oi["seg"], cfg.G,
-                               norm=norm, k=cfg.k, dual_clip_c=3.0, row_begin=r0, row_end=r1, row_offset=r0)
-        contrib[r0:r1] = ref.token_contrib
-        logp[r0:r1] = ref.token_logp
-        kinks = kink_rows(ref, oi["behave"][r0:r1], None, A64[oi["seg"].tok_traj[r0:r1]], 0.2, 0.2, 3.0)
-        worst = max(worst, check_dlogits(dl_to_f64(dl[r0:r1]), ref.dlogits, True, exempt=kinks, what=f"rows {r0}"))
-    total = float(np.sum(contrib))
-    assert abs(loss - total) <= LOSS_RTOL * abs(total), (loss, total)
-    assert np.abs(aux.token_logp.cpu().numpy() - logp).max() <= LOGP_ATOL
-    assert (aux.tok_traj.cpu().numpy() == oi["seg"].tok_traj).all()
-    assert aux.error_flags.item() == 0
+        blk = oracle.loss_rows(zl[r0:r1], oi["actions"], oi["behave"], None, oi["adv"], oi["seg"], cfg.G, norm=norm,
+                               k=cfg.k, dual_clip_c=3.0, row_begin=r0, row_end=r1, row_offset=r0)
+        kinks = kink_rows(blk, oi["behave"][r0:r1], None, A64[oi["seg"].tok_traj[r0:r1]], 0.2, 0.2, 3.0)
+        check_dlogits(dl_to_f64(dl[r0:r1]), blk.dlogits, True, exempt=kinks, what=f"rows {r0}")
+        worst = max(worst, check_dlogits(dl_to_f64(dl2[r0:r1]), blk.dlogits * gs, True, exempt=kinks, scaled=True,
+                                         what=f"scaled rows {r0}"))
+    print(f"v32k norm {norm}: worst scaled dlogits error {worst:.3f} of the gate", flush=True)
 
 
-# ---------------------------------------------------------------- 151,936 vocabulary, full size, sampled
+# ---------------------------------------------------------------- 151,936 vocabulary, full size
 
-def _sampled_parity(name, n_rows=48, n_traj_full=2, seed=0):
+def _full_size_parity(name, norms, n_rows=48, seed=0):
+    """The whole batch in the benchmark's launch configuration.  Every row's log-prob, every trajectory's loss,
+    the clip counts, the ratio statistics and the whole loss against the oracle over all rows; dlogits of sampled
+    rows (including rows each workgroup of the persistent kernel handles after its first) at grad_scale 1 and,
+    rerun at grad_scale = 1/max|g_t|, under the scaled bf16 gate."""
     b = make_batch(name, "cuda")
     cfg = b["cfg"]
     A64, A32 = _adv(b)
     oi = oracle_inputs(b, A64)
     T, V = b["logits"].shape
-    results = {}
-    for norm in NORMS:
+    refs = _oracle_all_rows(b, oi, norms)
+    grid = min(T, torch.cuda.get_device_properties(0).multi_processor_count)
+    rows = _pipeline_rows(T, grid, np.random.default_rng(seed), n_rows)
+    assert (rows >= grid).sum() >= n_rows // 2
+    out = {}
+    for norm in norms:
+        ref = refs[norm]
         loss, dl, aux = run_gpu(b, A32, norm=gpu_norm(norm), k=cfg.k, c=3.0)
-        results[norm] = (loss, aux)
-        rng = np.random.default_rng(seed)
-        rows = np.unique(np.concatenate([[0, T - 1], rng.integers(0, T, n_rows)]))
-        rows_t = torch.from_numpy(rows).cuda()
-        zs = to_np_logits(b["logits"].index_select(0, rows_t))
-        dls = dl_to_f64(dl.index_select(0, rows_t))
-        tl = aux.token_logp.cpu().numpy()
-        for q, t in enumerate(rows):
-            ref = oracle.loss_rows(zs[q:q + 1], oi["actions"], oi["behave"], None, oi["adv"], oi["seg"], cfg.G,
-                                   norm=norm, k=cfg.k, dual_clip_c=3.0, row_begin=int(t), row_end=int(t) + 1,
-                                   row_offset=int(t))
-            assert abs(tl[t] - ref.token_logp[0]) <= LOGP_ATOL
-            kinks = kink_rows(ref, oi["behave"][t:t + 1], None, A64[oi["seg"].tok_traj[t:t + 1]], 0.2, 0.2, 3.0)
-            check_dlogits(dls[q:q + 1], ref.dlogits, True, exempt=kinks, what=f"row {t}")
-        # whole trajectories: the oracle's per-trajectory loss against the GPU's
-        traj_loss = aux.traj_loss.cpu().numpy()
-        assert abs(loss - traj_loss.sum()) <= 1e-12 * np.abs(traj_loss).sum()
-        tto = oi["seg"].traj_tok_off
-        for i in np.random.default_rng(seed + 1).choice(len(tto) - 1, n_traj_full, replace=False):
-            t0, t1 = int(tto[i]), int(tto[i + 1])
-            zt = to_np_logits(b["logits"][t0:t1])
-            ref = oracle.loss_rows(zt, oi["actions"], oi["behave"], None, oi["adv"], oi["seg"], cfg.G,
-                                   norm=norm, k=cfg.k, dual_clip_c=3.0, row_begin=t0, row_end=t1, row_offset=t0,
-                                   want_dlogits=False)
-            assert abs(traj_loss[i] - ref.traj_loss[i]) <= LOSS_RTOL * abs(ref.traj_loss[i]), (i, traj_loss[i])
-        # integers, bit-exact at full size
-        assert (aux.tok_traj.cpu().numpy() == oi["seg"].tok_traj).all()
-        assert (aux.traj_tok_off.cpu().numpy() == oi["seg"].traj_tok_off).all()
-        assert (aux.gather_idx.cpu().numpy() == oracle.gather_index(T, V, oi["actions"])).all()
-        assert aux.error_flags.item() == 0
+        _whole_batch_checks(ref, loss, aux, oi, A64, V, V, f"{name} norm {norm}")
+        _sampled_dlogits(b, dl, rows, oi, A64, norm, 1.0, False, f"{name} norm {norm}")
         del dl
         torch.cuda.empty_cache()
-    return results
+        gs = float(np.float32(1.0 / np.abs(ref.token_g).max()))
+        loss2, dl2, _ = run_gpu(b, A32, norm=gpu_norm(norm), k=cfg.k, c=3.0, grad_scale=gs, aux=False)
+        assert loss2 == loss  # grad_scale does not touch the loss
+        worst = _sampled_dlogits(b, dl2, rows, oi, A64, norm, gs, True, f"{name} norm {norm} scaled")
+        print(f"{name} norm {norm}: worst scaled dlogits error {worst:.3f} of the gate over {len(rows)} rows",
+              flush=True)
+        del dl2
+        torch.cuda.empty_cache()
+        out[norm] = (loss, ref)
+    return out
 
 
-def test_v152k_full_size_sampled():
-    _sampled_parity("v152k")
+def test_v152k_full_size():
+    _full_size_parity("v152k", NORMS)
 
 
-def test_long_full_size_sampled():
-    _sampled_parity("long", n_rows=32, n_traj_full=1)
+def test_long_full_size():
+    _full_size_parity("long", NORMS, n_rows=32)
 
 
 # ---------------------------------------------------------------- advantages
@@ -227,12 +312,12 @@ def test_advantages_parity():
 
 # ---------------------------------------------------------------- edge cases
 
-def _edge_batch(V, dtype="bf16", n_groups=2, G=4, ld=None, seed=5):
+def _edge_batch(V, dtype="bf16", n_groups=2, G=4, ld=None, seed=5, max_tok=6):
     from synth.rollouts import Structure, add_noise, engine_logp, make_logits
     rng = np.random.default_rng(seed)
     N = n_groups * G
     steps = rng.integers(1, 4, N)
-    toks = rng.integers(0, 7, int(steps.sum()))  # empty steps allowed
+    toks = rng.integers(0, max_tok + 1, int(steps.sum()))  # empty steps allowed
     toks[0] = max(toks[0], 1)
     sto = np.concatenate([[0], np.cumsum(toks)]).astype(np.int32)
     tso = np.concatenate([[0], np.cumsum(steps)]).astype(np.int32)
@@ -258,6 +343,17 @@ def test_ragged_vocab_and_kernel_variants(V, dtype):
     # register-resident one; longer vector rows (bf16 200,000 and 262,144, fp32 100,000 and 151,936) the two
     # passes (a record per row, then the epilogue and dlogits)
     b = _edge_batch(V, dtype)
+    _full_parity(b, oracle.NORM_TRAJ_STEPS, 3.0)
+
+
+@pytest.mark.parametrize("V", [122880, 151936, 184320])
+def test_pipelined_kernel_several_rows_per_workgroup(V):
+    # T well above twice the CU count: each workgroup of the persistent kernel streams two or more rows (the next
+    # row's LDS part staged and its register part reloaded during the current row's dlogits pass), every row under
+    # the scaled bf16 gate
+    b = _edge_batch(V, "bf16", n_groups=4, G=4, seed=V % 97, max_tok=48)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert b["structure"].T > 2 * n_cu + 64, b["structure"].T
     _full_parity(b, oracle.NORM_TRAJ_STEPS, 3.0)
 
 

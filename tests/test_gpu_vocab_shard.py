@@ -144,38 +144,42 @@ def test_tiny_sharded_parity(bounds, norm, c):
 @pytest.mark.parametrize("bounds", [[0, 8000, 16000, 24000, 32000], [0, 10000, 10008, 31992, 32000],
                                     [0, 12345, 32000]])
 def test_v32k_sharded_parity(bounds):
-    _shard_parity(make_batch("v32k", "cuda"), bounds, oracle.NORM_CONST_K, 3.0, scaled=False)
+    _shard_parity(make_batch("v32k", "cuda"), bounds, oracle.NORM_CONST_K, 3.0, scaled=True)
 
 
-def test_v152k_eight_shards_full_size_sampled():
-    # the shape one device holds with the 151,936-column vocabulary split 8 ways: 18,992 columns
+def test_v152k_eight_shards_full_size():
+    # the shape one device holds with the 151,936-column vocabulary split 8 ways: 18,992 columns.  Every row's
+    # log-prob and the whole loss against the oracle over all rows; records and dlogits of sampled rows (grad_scale
+    # 1, then rerun at grad_scale = 1/max|g_t| under the scaled bf16 gate)
+    from tests.test_gpu_loss import _oracle_all_rows, _pipeline_rows, _sampled_dlogits, _whole_batch_checks
     b = make_batch("v152k", "cuda")
     cfg = b["cfg"]
     A64, A32 = _adv(b)
     oi = oracle_inputs(b, A64)
     T, V = b["logits"].shape
     bounds = [g * (V // 8) for g in range(9)]
+    ref = _oracle_all_rows(b, oi, [oracle.NORM_CONST_K])[oracle.NORM_CONST_K]
     losses, dl, auxes, stats = run_sharded(b, A32, bounds, norm=gpu_norm(oracle.NORM_CONST_K), k=cfg.k, c=3.0)
     assert len(set(losses)) == 1
-    rows = np.unique(np.concatenate([[0, T - 1], np.random.default_rng(7).integers(0, T, 40)]))
+    _whole_batch_checks(ref, losses[0], auxes[0], oi, A64, V, V, "v152k, 8 shards")
+    rows = _pipeline_rows(T, 256, np.random.default_rng(7), 40)
     rows_t = torch.from_numpy(rows).cuda()
-    zs = to_np_logits(b["logits"].index_select(0, rows_t))
-    check_stats(stats.index_select(1, rows_t), zs, oi["actions"], bounds, rows=rows)
-    dls = dl_to_f64(dl.index_select(0, rows_t))
-    tl = auxes[0].token_logp.cpu().numpy()
-    for q, t in enumerate(rows):
-        ref = oracle.loss_rows(zs[q:q + 1], oi["actions"], oi["behave"], None, oi["adv"], oi["seg"], cfg.G,
-                               norm=oracle.NORM_CONST_K, k=cfg.k, dual_clip_c=3.0, row_begin=int(t),
-                               row_end=int(t) + 1, row_offset=int(t))
-        assert abs(tl[t] - ref.token_logp[0]) <= LOGP_ATOL
-        kinks = kink_rows(ref, oi["behave"][t:t + 1], None, A64[oi["seg"].tok_traj[t:t + 1]], 0.2, 0.2, 3.0)
-        check_dlogits(dls[q:q + 1], ref.dlogits, True, exempt=kinks, what=f"row {t}")
+    check_stats(stats.index_select(1, rows_t), to_np_logits(b["logits"].index_select(0, rows_t)), oi["actions"],
+                bounds, rows=rows)
+    _sampled_dlogits(b, dl, rows, oi, A64, oracle.NORM_CONST_K, 1.0, False, "8 shards")
     del dl
     torch.cuda.empty_cache()
-    # the whole loss against the single-device path (itself held to the oracle at this size)
+    gs = float(np.float32(1.0 / np.abs(ref.token_g).max()))
+    losses2, dl2, _, _ = run_sharded(b, A32, bounds, norm=gpu_norm(oracle.NORM_CONST_K), k=cfg.k, c=3.0,
+                                     grad_scale=gs, aux=False)
+    assert losses2[0] == losses[0]
+    _sampled_dlogits(b, dl2, rows, oi, A64, oracle.NORM_CONST_K, gs, True, "8 shards scaled")
+    del dl2
+    torch.cuda.empty_cache()
+    # and the single-device path on the same batch: the same loss to rounding
     loss1, _, aux1 = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, c=3.0, dlogits=False)
     assert abs(losses[0] - loss1) <= LOSS_RTOL * abs(loss1)
-    assert np.abs(tl - aux1.token_logp.cpu().numpy()).max() <= LOGP_ATOL
+    assert np.abs(auxes[0].token_logp.cpu().numpy() - aux1.token_logp.cpu().numpy()).max() <= LOGP_ATOL
     assert auxes[0].error_flags.item() == 0
 
 
