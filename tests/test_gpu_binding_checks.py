@@ -27,7 +27,7 @@ def test_caller_buffers_checked():
     need = grpo.grpo_loss_workspace_bytes(T, N)
     with pytest.raises(ValueError, match="workspace"):
         _call(b, workspace=torch.empty(need, dtype=torch.uint8))  # host memory
-    with pytest.raises(ValueError, match="loss_out"):
+    with pytest.raises(TypeError, match="loss_out"):  # a wrong dtype is a TypeError, a wrong size or place ValueError
         _call(b, loss_out=torch.empty(1, dtype=torch.float32, device="cuda"))
     short = grpo.LossAux.alloc(T, N, "cuda")
     short.token_logp = torch.empty(T - 1, dtype=torch.float32, device="cuda")
@@ -35,7 +35,7 @@ def test_caller_buffers_checked():
         _call(b, aux=short)
     wrong = grpo.LossAux.alloc(T, N, "cuda")
     wrong.traj_loss = torch.empty(N, dtype=torch.float32, device="cuda")
-    with pytest.raises(ValueError, match="traj_loss"):
+    with pytest.raises(TypeError, match="traj_loss"):
         _call(b, aux=wrong)
 
 
@@ -57,7 +57,7 @@ def test_fused_logp_error_flags_checked():
     h = torch.randn(8, 64, device="cuda").to(torch.bfloat16)
     w = torch.randn(64, 256, device="cuda").to(torch.bfloat16)
     a = torch.zeros(8, dtype=torch.int32, device="cuda")
-    with pytest.raises(ValueError, match="error_flags"):
+    with pytest.raises(TypeError, match="error_flags"):
         grpo.fused_lmhead_token_logp(h, w, a, error_flags=torch.zeros(1, dtype=torch.int64, device="cuda"))
     flags = torch.full((1,), 7, dtype=torch.int32, device="cuda")
     grpo.fused_lmhead_token_logp(h, w, a, error_flags=flags)
@@ -80,7 +80,7 @@ def test_fused_caller_buffers_checked():
                                        loss_out=torch.empty(1, dtype=torch.float64, device="cpu"))
     aux = grpo.LossAux.alloc(300, len(e["rewards"]), "cuda")
     aux.gather_idx = torch.empty(300, dtype=torch.int32, device="cuda")
-    with pytest.raises(ValueError, match="gather_idx"):
+    with pytest.raises(TypeError, match="gather_idx"):
         grpo.fused_lmhead_grpo_blocked(*args, token_block=256, aux=aux)
     # the same call with valid buffers of the caller's
     ws = torch.empty((need + 7) // 8, dtype=torch.float64, device="cuda")
