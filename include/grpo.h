@@ -179,6 +179,30 @@ int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, i
                       const float* adv, const grpo_segments* seg, const grpo_loss_params* p, double* loss_out,
                       void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
 
+/* Size of the device scratch array behind grpo_loss_fwd_bwd_noalloc (24 MiB): the largest
+ * grpo_loss_workspace_bytes(T, n_traj) it serves, e.g. T = 262,144 tokens with n_traj up to 16,384. */
+#define GRPO_NOALLOC_SCRATCH_BYTES ((size_t)24 << 20)
+
+/*
+ * grpo_loss_fwd_bwd for callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same computation, kernels and results, with the
+ * workspace taken from a device array of GRPO_NOALLOC_SCRATCH_BYTES that the library holds on each device
+ * (reserved when the library's code is loaded on the device and kept until the process ends).  The call itself
+ * allocates and frees nothing; on its first call on a device it looks the array's address up (with that
+ * device current).  The caller still passes every input and output, as for grpo_loss_fwd_bwd.
+ * Every call on a device shares that device's array and leaves the last call's contents in it: two calls that
+ * overlap on one device (on different streams, or from different host threads without ordering) race and
+ * their results are undefined.  Calls ordered on one stream are safe.
+ * Arguments: as grpo_loss_fwd_bwd, without ws and ws_bytes.
+ * Errors: as grpo_loss_fwd_bwd; GRPO_ERR_WORKSPACE when grpo_loss_workspace_bytes(T, n_traj) exceeds
+ *   GRPO_NOALLOC_SCRATCH_BYTES (nothing is launched); GRPO_ERR_HIP when the stream's device cannot be found
+ *   or the array's address cannot be looked up.
+ */
+int grpo_loss_fwd_bwd_noalloc(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                              const int32_t* actions, const float* behave_logp, const float* prox_logp,
+                              const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
+                              double* loss_out, void* dlogits, grpo_aux* aux, hipStream_t s);
+
 /* Bytes of device workspace fused_lmhead_grpo needs. */
 size_t fused_lmhead_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t vocab_chunk, int32_t n_traj);
 

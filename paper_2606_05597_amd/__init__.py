@@ -15,10 +15,11 @@ import torch
 
 from . import _lib
 from ._lib import (GRPO_ADV_GROUP_NORM, GRPO_ADV_SUCCESS_FILTER, GRPO_BF16, GRPO_F32,  # noqa: F401
-                   GRPO_FLAG_ACTION, GRPO_FLAG_NONFINITE, GRPO_FLAG_OFFSETS, GRPO_NORM_CONST_K,
-                   GRPO_NORM_TRAJ_STEPS, GrpoError)
+                   GRPO_FLAG_ACTION, GRPO_FLAG_NONFINITE, GRPO_FLAG_OFFSETS, GRPO_NOALLOC_SCRATCH_BYTES,
+                   GRPO_NORM_CONST_K, GRPO_NORM_TRAJ_STEPS, GrpoError)
 
-__all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd", "fused_lmhead_workspace_bytes",
+__all__ = ["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes", "grpo_loss_fwd_bwd",
+           "grpo_loss_fwd_bwd_noalloc", "fused_lmhead_workspace_bytes",
            "fused_lmhead_grpo", "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked", "grpo_token_logp", "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
            "vocab_stats_fields", "fused_lmhead_vocab_shard_stats", "fused_lmhead_grpo_vocab_shard",
            "vocab_shard_logits_buffer", "GrpoLoss", "FusedLmHeadGrpoLoss", "loss",
@@ -302,6 +303,30 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
     forward only; a tensor is written in place (it may be ``logits`` itself).
     Returns (loss [1] fp64, dlogits or None).
     """
+    return _logits_loss(True, logits, actions, behave_logp, adv, step_tok_off, traj_step_off, group_size, V,
+                        prox_logp, norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total, dlogits, aux,
+                        workspace, loss_out, stream)
+
+
+def grpo_loss_fwd_bwd_noalloc(logits: torch.Tensor, actions: torch.Tensor, behave_logp: torch.Tensor,
+                              adv: torch.Tensor, step_tok_off: torch.Tensor, traj_step_off: torch.Tensor,
+                              group_size: int, *, V: int | None = None, prox_logp: torch.Tensor | None = None,
+                              norm: int = GRPO_NORM_CONST_K, k: float = 10.0, eps_low: float = 0.2,
+                              eps_high: float = 0.2, dual_clip_c: float = 0.0, grad_scale: float = 1.0,
+                              n_groups_total: float = 0.0, dlogits=True, aux: LossAux | None = None,
+                              loss_out: torch.Tensor | None = None, stream=None):
+    """grpo_loss_fwd_bwd with the library's own per-device scratch array as the workspace (the entry point allocates
+    nothing; pass ``dlogits`` and ``loss_out`` tensors for a call in which nothing is allocated at all).  Calls that
+    overlap on one device race on the array; the batch must fit it (grpo_loss_workspace_bytes(T, n_traj) <=
+    GRPO_NOALLOC_SCRATCH_BYTES).  Returns (loss [1] fp64, dlogits or None)."""
+    return _logits_loss(False, logits, actions, behave_logp, adv, step_tok_off, traj_step_off, group_size, V,
+                        prox_logp, norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total, dlogits, aux,
+                        None, loss_out, stream)
+
+
+def _logits_loss(with_ws, logits, actions, behave_logp, adv, step_tok_off, traj_step_off, group_size, V, prox_logp,
+                 norm, k, eps_low, eps_high, dual_clip_c, grad_scale, n_groups_total, dlogits, aux, workspace,
+                 loss_out, stream):
     dt, T, ld = _logits2d(logits)
     Vv = logits.shape[1] if V is None else int(V)
     seg = _segments(step_tok_off, traj_step_off, group_size)
@@ -314,15 +339,18 @@ def grpo_loss_fwd_bwd(logits: torch.Tensor, actions: torch.Tensor, behave_logp: 
             actions=actions, behave_logp=behave_logp, prox_logp=prox_logp, adv=adv, step_tok_off=step_tok_off,
             traj_step_off=traj_step_off)
     ca = aux._c(T, seg.n_traj, dev) if aux is not None else None
-    need = grpo_loss_workspace_bytes(T, seg.n_traj)
-    workspace = _workspace(workspace, need, dev)
     loss_out = _loss_out(loss_out, dev)
     dlogits = _dlogits_arg(dlogits, logits)
-    st = _lib.load().grpo_loss_fwd_bwd(
-        _ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(behave_logp), _ptr(prox_logp), _ptr(adv),
-        ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dlogits),
-        ctypes.byref(ca) if ca is not None else None, _ptr(workspace), _nbytes(workspace), _stream(stream))
-    _check(st, "grpo_loss_fwd_bwd")
+    args = (_ptr(logits), dt, T, Vv, ld, _ptr(actions), _ptr(behave_logp), _ptr(prox_logp), _ptr(adv),
+            ctypes.byref(seg), ctypes.byref(par), _ptr(loss_out), _ptr(dlogits),
+            ctypes.byref(ca) if ca is not None else None)
+    if with_ws:
+        workspace = _workspace(workspace, grpo_loss_workspace_bytes(T, seg.n_traj), dev)
+        st = _lib.load().grpo_loss_fwd_bwd(*args, _ptr(workspace), _nbytes(workspace), _stream(stream))
+        _check(st, "grpo_loss_fwd_bwd")
+    else:
+        st = _lib.load().grpo_loss_fwd_bwd_noalloc(*args, _stream(stream))
+        _check(st, "grpo_loss_fwd_bwd_noalloc")
     return loss_out, dlogits
 
 

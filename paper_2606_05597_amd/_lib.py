@@ -22,6 +22,8 @@ GRPO_NORM_CONST_K = 1
 GRPO_ADV_GROUP_NORM = 0
 GRPO_ADV_SUCCESS_FILTER = 1
 
+GRPO_NOALLOC_SCRATCH_BYTES = 24 << 20
+
 GRPO_FLAG_ACTION = 1
 GRPO_FLAG_OFFSETS = 2
 GRPO_FLAG_NONFINITE = 4
@@ -72,6 +74,8 @@ def load() -> ctypes.CDLL:
                                           ctypes.POINTER(Segments), ctypes.POINTER(LossParams), P, P,
                                           ctypes.POINTER(Aux), P, SZ, P]
         lib.grpo_loss_fwd_bwd.restype = ctypes.c_int
+        lib.grpo_loss_fwd_bwd_noalloc.argtypes = lib.grpo_loss_fwd_bwd.argtypes[:14] + [P]
+        lib.grpo_loss_fwd_bwd_noalloc.restype = ctypes.c_int
         lib.fused_lmhead_workspace_bytes.argtypes = [I64, I64, I64, I32, I32]
         lib.fused_lmhead_workspace_bytes.restype = SZ
         lib.fused_lmhead_grpo.argtypes = [P, P, I64, I64, I64, I32, P, P, P, P, ctypes.POINTER(Segments),

@@ -20,6 +20,8 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include <mutex>
+
 #include "device.h"
 #include "launch.h"
 
@@ -448,11 +450,11 @@ extern "C" size_t grpo_loss_workspace_bytes(int64_t T, int32_t n_traj) {
   return loss_ws_layout(T, n_traj).total;
 }
 
-extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
-                                 const int32_t* actions, const float* behave_logp, const float* prox_logp,
-                                 const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
-                                 double* loss_out, void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes,
-                                 hipStream_t s) {
+// Argument checks of the logits path other than the workspace's (GRPO_OK or the error).
+static int check_logits_call(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                             const int32_t* actions, const float* behave_logp, const float* adv,
+                             const grpo_segments* seg, const grpo_loss_params* p, const double* loss_out,
+                             const void* dlogits) {
   int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
   if (st != GRPO_OK) return st;
   if (dt != GRPO_BF16 && dt != GRPO_F32) return GRPO_ERR_DTYPE;
@@ -460,6 +462,16 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
   if (V < 1 || ld < V || V >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
   const size_t esz = (dt == GRPO_BF16) ? 2 : 4;
   if (!aligned(logits, esz) || !aligned(dlogits, esz)) return GRPO_ERR_ALIGN;
+  return GRPO_OK;
+}
+
+extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                                 const int32_t* actions, const float* behave_logp, const float* prox_logp,
+                                 const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
+                                 double* loss_out, void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes,
+                                 hipStream_t s) {
+  const int st = check_logits_call(logits, dt, T, V, ld, actions, behave_logp, adv, seg, p, loss_out, dlogits);
+  if (st != GRPO_OK) return st;
   const LossWs L = loss_ws_layout(T, seg->n_traj);
   if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
@@ -490,4 +502,50 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, i
   }
   if (launch_reduce(T, seg->n_traj, w, L, loss_out, aux, s) != hipSuccess) return GRPO_ERR_HIP;
   return GRPO_OK;
+}
+
+// ---- the logits path without a caller workspace ------------------------------------
+// For callers that cannot allocate device memory, the workspace is a file-scope device array of fixed size.
+// Each device the library runs on holds its own copy until the process ends; host code reaches it only through
+// the address hipGetSymbolAddress returns on that device, looked up once per device and kept.
+static __device__ __align__(256) char scratch[GRPO_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[kMaxDevices];  // device address of `scratch` per device (nullptr until its first call)
+}  // namespace
+
+// The scratch array's address on the stream's device: looked up with that device current on the device's first
+// call, then read from the table.
+static int scratch_of_stream(hipStream_t s, char** out) {
+  hipDevice_t dev = 0;
+  if (hipStreamGetDevice(s, &dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return GRPO_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return GRPO_ERR_HIP;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return GRPO_ERR_HIP;
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev && hipSetDevice(cur) != hipSuccess) return GRPO_ERR_HIP;
+    if (e != hipSuccess || !ptr) return GRPO_ERR_HIP;
+    g_scratch[dev] = static_cast<char*>(ptr);
+  }
+  *out = g_scratch[dev];
+  return GRPO_OK;
+}
+
+extern "C" int grpo_loss_fwd_bwd_noalloc(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+                                         const int32_t* actions, const float* behave_logp, const float* prox_logp,
+                                         const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
+                                         double* loss_out, void* dlogits, grpo_aux* aux, hipStream_t s) {
+  const int st = check_logits_call(logits, dt, T, V, ld, actions, behave_logp, adv, seg, p, loss_out, dlogits);
+  if (st != GRPO_OK) return st;
+  if (loss_ws_layout(T, seg->n_traj).total > (size_t)GRPO_NOALLOC_SCRATCH_BYTES) return GRPO_ERR_WORKSPACE;
+  char* ws = nullptr;
+  const int sc = scratch_of_stream(s, &ws);
+  if (sc != GRPO_OK) return sc;
+  return grpo_loss_fwd_bwd(logits, dt, T, V, ld, actions, behave_logp, prox_logp, adv, seg, p, loss_out, dlogits,
+                           aux, ws, (size_t)GRPO_NOALLOC_SCRATCH_BYTES, s);
 }

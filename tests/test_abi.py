@@ -33,7 +33,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(["grpo_advantages", "grpo_advantages_ex", "grpo_loss_workspace_bytes",
-                                           "grpo_loss_fwd_bwd",
+                                           "grpo_loss_fwd_bwd", "grpo_loss_fwd_bwd_noalloc",
                                            "fused_lmhead_workspace_bytes", "fused_lmhead_grpo", "grpo_token_logp",
                                            "fused_lmhead_blocked_workspace_bytes", "fused_lmhead_grpo_blocked",
                                            "grpo_vocab_shard_stats", "grpo_loss_fwd_bwd_vocab_shard",
@@ -134,6 +134,30 @@ def call_loss(lib, *, T=8, V=64, ld=64, dt=_lib.GRPO_BF16, n_traj=4, G=4, n_step
 ])
 def test_loss_rejects_bad_arguments(lib, kw, status):
     assert call_loss(lib, **kw) == status
+
+
+def call_loss_noalloc(lib, *, T=8, V=64, ld=64, n_traj=4, G=4, n_steps=4, logits=D, actions=D):
+    seg = _lib.Segments()
+    seg.n_traj, seg.group_size, seg.n_steps = n_traj, G, n_steps
+    seg.step_tok_off, seg.traj_step_off = D, D
+    p = _lib.LossParams()
+    p.norm, p.k, p.eps_low, p.eps_high, p.dual_clip_c, p.grad_scale, p.n_groups_total = 1, 10.0, 0.2, 0.2, 3.0, 1.0, 0.0
+    return lib.grpo_loss_fwd_bwd_noalloc(logits, _lib.GRPO_BF16, T, V, ld, actions, D, None, D, ctypes.byref(seg),
+                                         ctypes.byref(p), D, D, None, None)
+
+
+def test_noalloc_rejects_bad_arguments_and_oversized_batches(lib):
+    # the argument checks of grpo_loss_fwd_bwd, then the batch against the fixed scratch array, all on the host
+    assert call_loss_noalloc(lib, actions=None) == _lib.GRPO_ERR_ARG
+    assert call_loss_noalloc(lib, ld=63) == _lib.GRPO_ERR_SHAPE
+    assert call_loss_noalloc(lib, logits=ctypes.c_void_p(0x100001)) == _lib.GRPO_ERR_ALIGN
+    big_T = 1 << 20  # 61 bytes of scratch per token: 64 MB > 24 MiB
+    assert lib.grpo_loss_workspace_bytes(big_T, 4) > _lib.GRPO_NOALLOC_SCRATCH_BYTES
+    assert call_loss_noalloc(lib, T=big_T) == _lib.GRPO_ERR_WORKSPACE
+    many = 1 << 20  # per-trajectory tables alone exceed the array
+    assert call_loss_noalloc(lib, n_traj=many, G=1, n_steps=many) == _lib.GRPO_ERR_WORKSPACE
+    # the sizes the header states fit
+    assert lib.grpo_loss_workspace_bytes(262144, 16384) <= _lib.GRPO_NOALLOC_SCRATCH_BYTES
 
 
 def test_trajectory_normaliser_ignores_k(lib):
