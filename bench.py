@@ -105,6 +105,8 @@ def parse():
                     help="timed steps of the forward-only log-prob + entropy path (0 = skip)")
     ap.add_argument("--shard-steps", type=int, default=10,
                     help="timed steps of one device's share of the vocabulary-parallel loss (0 = skip)")
+    ap.add_argument("--config-steps", type=int, default=10,
+                    help="timed steps of each other logits-path workload: long, v32k, tiny (0 = skip)")
     ap.add_argument("--skip-logits", action="store_true", help="measure only the fused path")
     ap.add_argument("--token-block", type=int, default=8192, help="token block of the blocked fused schedule")
     ap.add_argument("--fused-schedule", choices=("all",) + FUSED_SCHEDULES, default="all",
@@ -167,23 +169,50 @@ def cpu_baseline(b: dict, adv64, budget_s: float) -> dict:
                               "sample": f"first {r1} token rows, {el1:.1f} s"}}
 
 
-def copy_ceiling(t) -> dict:
-    """A plain device copy of a tensor of the same size (the runtime's copy), read + write bytes per second."""
+def copy_ceiling(src, dst, reps: int = 3) -> dict:
+    """The memory-only ceiling of the row pass: src copied into dst -- the same logits and dlogits buffers the row
+    kernel reads and writes, so the same physical placement -- by each hand-written streaming-copy variant
+    (libgrpo_bench.so) and by torch's copy_, best of ``reps`` each, read + write bytes per second.  The ceiling is
+    the fastest hand-written variant."""
+    import ctypes
+
     import torch
-    dst = torch.empty_like(t)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    ms = []
-    for _ in range(3):
-        e0.record()
-        dst.copy_(t)
-        e1.record()
-        torch.cuda.synchronize()
-        ms.append(e0.elapsed_time(e1))
-    del dst
-    nbytes = 2.0 * t.numel() * t.element_size()
-    best = min(ms)
-    return {"GBps": nbytes / (best * 1e-3) / 1e9, "bytes": nbytes, "ms": best, "what": "torch copy_ of the logits"}
+
+    from paper_2606_05597_amd.build import BENCH_SO
+    lib = ctypes.CDLL(BENCH_SO)
+    lib.stream_copy.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.stream_copy.restype = ctypes.c_int
+    lib.stream_copy_name.argtypes = [ctypes.c_int]
+    lib.stream_copy_name.restype = ctypes.c_char_p
+    nbytes = src.numel() * src.element_size()
+    assert dst.numel() * dst.element_size() == nbytes and src.is_contiguous() and dst.is_contiguous()
+    assert nbytes % 16 == 0
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def best(run):
+        ms = []
+        for _ in range(reps):
+            e0.record(stream)
+            run()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return min(ms)
+
+    variants = []
+    for v in range(lib.stream_copy_variants()):
+        def run(v=v):
+            rc = lib.stream_copy(v, src.data_ptr(), dst.data_ptr(), nbytes // 16, ctypes.c_void_p(stream.cuda_stream))
+            assert rc == 0, rc
+        ms = best(run)
+        variants.append({"kernel": lib.stream_copy_name(v).decode(), "ms": ms, "GBps": 2.0 * nbytes / (ms * 1e-3) / 1e9})
+    tms = best(lambda: dst.copy_(src))
+    top = max(variants, key=lambda x: x["GBps"])
+    return {"GBps": top["GBps"], "ms": top["ms"], "bytes": 2.0 * nbytes, "kernel": top["kernel"],
+            "what": "hand-written streaming copy of the logits buffer into the dlogits buffer (16-byte non-temporal "
+                    "loads and stores), the fastest of the variants",
+            "variants": variants, "torch_copy_GBps": 2.0 * nbytes / (tms * 1e-3) / 1e9}
 
 
 def device_info() -> dict:
@@ -194,6 +223,86 @@ def device_info() -> dict:
     if clk:
         out["max_clock_MHz"] = clk / 1000.0
     return out
+
+
+def time_logits(b: dict, norm: int, steps: int, warmup: int, dlogits=None) -> dict:
+    """Times one logits-path step on batch b (group advantages, then grpo_loss_fwd_bwd with dlogits) under the
+    normaliser ``norm``: the whole step by the host clock, the row pass by the HIP events the library records
+    around it on its stream.  Returns the step's figures and the row pass's roofline."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    cfg, st = b["cfg"], b["structure"]
+    T, V = b["logits"].shape
+    N = len(st.rewards)
+    dev = b["logits"].device
+    sto = torch.from_numpy(st.step_tok_off).to(dev)
+    tso = torch.from_numpy(st.traj_step_off).to(dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    dl = torch.empty_like(b["logits"]) if dlogits is None else dlogits
+    ws = torch.empty(grpo.grpo_loss_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for e in ev0 + ev1:
+        e.record(stream)  # creates the underlying hipEvent_t
+    torch.cuda.synchronize()
+
+    def step(i=None):
+        grpo.grpo_advantages(b["rewards"], cfg.G, out=adv)
+        aux = None if i is None else grpo.LossAux(hot_events=(ev0[i].cuda_event, ev1[i].cuda_event))
+        grpo.grpo_loss_fwd_bwd(b["logits"], b["actions"], b["behave"], adv, sto, tso, cfg.G, V=b["V"], norm=norm,
+                               k=cfg.k, eps_low=0.2, eps_high=0.2, dual_clip_c=3.0, dlogits=dl, aux=aux,
+                               workspace=ws, loss_out=loss)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(steps)) / steps
+    esz = b["logits"].element_size()
+    alg = T * (2.0 * esz * V + 16.0)  # the row read once, dlogits written once, action + behave + weight + advantage
+    achieved = alg / (hot_ms * 1e-3) / 1e9
+    out = {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps,
+           "loss": float(loss.item()),
+           "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel_ms": hot_ms,
+                        "algorithmic_bytes_per_launch": alg}}
+    if dlogits is None:
+        del dl
+    del ws
+    return out
+
+
+def bench_logits_config(name: str, steps: int, warmup: int = 2, kernel: str = "", norms=None) -> dict:
+    """One of the other logits-path workloads, generated, timed under each normaliser, and freed."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    from synth import make_batch
+    b = make_batch(name, torch.device("cuda:0"))
+    T, V = b["logits"].shape
+    cfg = b["cfg"]
+    dt = "bf16" if b["logits"].dtype == torch.bfloat16 else "fp32"
+    norms = norms or [("1/k", grpo.GRPO_NORM_CONST_K)]
+    res = {}
+    for label, norm in norms:
+        r = time_logits(b, norm, steps, warmup)
+        r["roofline"]["kernel"] = kernel
+        res[label] = r
+    head = dict(res[norms[0][0]])
+    head["workload"] = (f"{name}: {cfg.n_groups} groups x G={cfg.G}, T={T} action tokens, V={V}, {dt} logits; "
+                        f"normaliser {norms[0][0]} (k={cfg.k:g})")
+    for label, _ in norms[1:]:
+        head[f"normaliser {label}"] = res[label]
+    del b
+    torch.cuda.empty_cache()
+    return head
 
 
 def bench_logp(b: dict, steps: int, warmup: int = 2) -> dict:
@@ -574,50 +683,19 @@ def main():
     cfg, st = b["cfg"], b["structure"]
     T, V = b["logits"].shape
     N = len(st.rewards)
-    sto = torch.from_numpy(st.step_tok_off).to(dev)
-    tso = torch.from_numpy(st.traj_step_off).to(dev)
-    adv = torch.empty(N, dtype=torch.float32, device=dev)
     dlogits = torch.empty_like(b["logits"])
-    ws = torch.empty(grpo.grpo_loss_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
-    loss = torch.empty(1, dtype=torch.float64, device=dev)
-    stream = torch.cuda.current_stream()
-    n_ev = args.steps
-    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
-    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
-    for e in ev0 + ev1:
-        e.record(stream)  # creates the underlying hipEvent_t
-    torch.cuda.synchronize()
-
-    def step(i=None):
-        grpo.grpo_advantages(b["rewards"], cfg.G, out=adv)
-        aux = None
-        if i is not None:
-            aux = grpo.LossAux(hot_events=(ev0[i].cuda_event, ev1[i].cuda_event))
-        grpo.grpo_loss_fwd_bwd(b["logits"], b["actions"], b["behave"], adv, sto, tso, cfg.G,
-                               norm=grpo.GRPO_NORM_CONST_K, k=cfg.k, eps_low=0.2, eps_high=0.2, dual_clip_c=3.0,
-                               dlogits=dlogits, aux=aux, workspace=ws, loss_out=loss)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(i)
-    torch.cuda.synchronize()
-    el = time.perf_counter() - t0
-    ms = el * 1e3 / args.steps
-    hot_ms = sum(ev0[i].elapsed_time(ev1[i]) for i in range(args.steps)) / args.steps
-    alg_bytes = T * (4.0 * V + 16.0)
-    achieved = alg_bytes / (hot_ms * 1e-3) / 1e9
-    traffic = measured_traffic(T)
+    head = time_logits(b, grpo.GRPO_NORM_CONST_K, args.steps, args.warmup, dlogits=dlogits)
+    roof = head["roofline"]
+    roof["traffic"] = measured_traffic(T)
+    roof["kernel"] = "k_rows_pipe<19, 5> (bf16, 1024 threads, one workgroup per CU)"
     out = {
         "metric": METRIC,
-        "value": T / (ms * 1e-3),
+        "value": head["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -625,18 +703,26 @@ def main():
         "data": "synthetic",
         "config": {"workload": "v152k: 16 groups x G=8 rollouts, T=120,000 action tokens, V=151,936, bf16 logits",
                    "T": T, "V": V, "n_traj": N, "n_steps": int(st.step_tok_off.shape[0] - 1),
-                   "normalizer": "1/k (k=10)", "eps": 0.2, "dual_clip_c": 3.0, "loss": float(loss.item())},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_rows_pipe<19, 5> (bf16, 1024 threads, one workgroup per CU)", "kernel_ms": hot_ms,
-                     "algorithmic_bytes_per_launch": alg_bytes},
+                   "normalizer": "1/k (k=10)", "eps": 0.2, "dual_clip_c": 3.0, "loss": head["loss"]},
+        "roofline": roof,
     }
+    # the memory-only ceiling on the same two buffers, then the row pass again, so that a placement that changes
+    # between the two would show
+    cc = copy_ceiling(b["logits"], dlogits)
+    again = time_logits(b, grpo.GRPO_NORM_CONST_K, max(3, args.steps // 2), 1, dlogits=dlogits)
+    roof["copy_ceiling_GBps"] = cc["GBps"]
+    roof["copy_ceiling_kernel"] = cc["kernel"]
+    roof["copy_variants"] = cc["variants"]
+    roof["torch_copy_GBps"] = cc["torch_copy_GBps"]
+    roof["frac_of_copy_ceiling"] = roof["achieved"] / cc["GBps"]
+    roof["kernel_ms_after_copy"] = again["roofline"]["kernel_ms"]
+    # the paper's baseline normaliser 1/|tau_i| on the same batch (Sec. 3.2; the workload names both)
+    trs = time_logits(b, grpo.GRPO_NORM_TRAJ_STEPS, max(3, args.steps // 2), 1, dlogits=dlogits)
+    trs["roofline"]["kernel"] = roof["kernel"]
+    out["normaliser_traj_steps"] = trs
     del dlogits
     torch.cuda.empty_cache()
     out["device"] = device_info()
-    cc = copy_ceiling(b["logits"])
-    out["roofline"]["copy_ceiling_GBps"] = cc["GBps"]
-    out["roofline"]["frac_of_copy_ceiling"] = achieved / cc["GBps"]
     if args.cpu_seconds > 0:
         import oracle
         A = oracle.advantages(st.rewards, cfg.G).astype(np.float32).astype(np.float64)
@@ -645,9 +731,19 @@ def main():
         out["token_logp"] = bench_logp(b, args.logp_steps)
     if args.shard_steps > 0:
         out["vocab_shard"] = bench_vocab_shard(b, args.shard_steps)
+    del b
+    torch.cuda.empty_cache()
+    if args.config_steps > 0:
+        out["long"] = bench_logits_config("long", args.config_steps, kernel=roof["kernel"])
+        out["v32k"] = bench_logits_config(
+            "v32k", args.config_steps, kernel="k_rows_resident<bf16, 256, 16> (one workgroup per row)",
+            norms=[("1/k", grpo.GRPO_NORM_CONST_K), ("1/|tau_i|", grpo.GRPO_NORM_TRAJ_STEPS)])
+        tiny = bench_logits_config(
+            "tiny", max(20, args.config_steps), kernel="k_rows_resident<fp32, 64, 4> (one workgroup per row)",
+            norms=[("1/k", grpo.GRPO_NORM_CONST_K), ("1/|tau_i|", grpo.GRPO_NORM_TRAJ_STEPS)])
+        tiny["note"] = "launch-bound: four small launches per step (advantages, segments, row pass, reduction)"
+        out["tiny"] = tiny
     if args.fused_steps > 0:
-        del b
-        torch.cuda.empty_cache()
         out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3,
                                           cpu=args.cpu_seconds > 0, token_block=args.token_block,
                                           schedules=fused_schedules(args))

@@ -58,6 +58,8 @@ typedef enum {
   GRPO_ERR_HIP = -6        /* a HIP launch returned an error                         */
 } grpo_status;
 
+/* Element types of logits and dlogits.  Entry points take the code as an int32_t `dtype` argument, so that any
+ * other value reaches their check and is refused with GRPO_ERR_DTYPE. */
 typedef enum { GRPO_F32 = 0, GRPO_BF16 = 1 } grpo_dtype;
 
 typedef enum {
@@ -152,7 +154,7 @@ size_t grpo_loss_workspace_bytes(int64_t T, int32_t n_traj);
  * The logits path: loss and dlogits of Eq. 1 (+ Eq. 2) from the policy's
  * vocabulary logits at every action token.
  *   logits       device [T, ld] of `dt`, row t = token t; columns >= V unread
- *   dt           GRPO_BF16 or GRPO_F32 (dlogits has the same dtype)
+ *   dtype        GRPO_BF16 or GRPO_F32 (dlogits has the same dtype)
  *   T >= 0, 1 <= V <= ld
  *   actions      device int32 [T]  sampled token ids a_t
  *   behave_logp  device fp32 [T]   log pi_behave(a_t), recorded at rollout
@@ -174,7 +176,7 @@ size_t grpo_loss_workspace_bytes(int64_t T, int32_t n_traj);
  *   T >= 2^31), GRPO_ERR_DTYPE, GRPO_ERR_WORKSPACE, GRPO_ERR_ALIGN (logits or
  *   dlogits not aligned to the element size), GRPO_ERR_HIP.
  */
-int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+int grpo_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                       const int32_t* actions, const float* behave_logp, const float* prox_logp,
                       const float* adv, const grpo_segments* seg, const grpo_loss_params* p, double* loss_out,
                       void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s);
@@ -198,7 +200,7 @@ int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, i
  *   GRPO_NOALLOC_SCRATCH_BYTES (nothing is launched); GRPO_ERR_HIP when the stream's device cannot be found
  *   or the array's address cannot be looked up.
  */
-int grpo_loss_fwd_bwd_noalloc(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+int grpo_loss_fwd_bwd_noalloc(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                               const int32_t* actions, const float* behave_logp, const float* prox_logp,
                               const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
                               double* loss_out, void* dlogits, grpo_aux* aux, hipStream_t s);
@@ -285,7 +287,7 @@ int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, int64_t T, i
  *   ld < V, T >= 2^31), GRPO_ERR_DTYPE, GRPO_ERR_ALIGN (logits not aligned to
  *   the element size), GRPO_ERR_HIP.
  */
-int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const int32_t* actions,
+int grpo_token_logp(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld, const int32_t* actions,
                     float* token_logp, float* token_entropy, int32_t* error_flags, hipStream_t s);
 
 /* Bytes of device workspace fused_lmhead_token_logp needs (W^T and the per-(row, 256-column tile) partials:
@@ -346,7 +348,7 @@ typedef struct {
  * Errors: GRPO_ERR_ARG (logits, actions or stats NULL), GRPO_ERR_SHAPE, GRPO_ERR_DTYPE,
  *   GRPO_ERR_ALIGN, GRPO_ERR_HIP.
  */
-int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+int grpo_vocab_shard_stats(const void* logits, int32_t dtype, int64_t T, int64_t V_shard, int64_t ld,
                            int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats, int32_t* error_flags,
                            hipStream_t s);
 
@@ -370,7 +372,7 @@ int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t T, int64_t
  * v_begin + V_shard > V_total, V_total >= 2^31 or n_shards outside 1..65536, and
  * GRPO_ERR_ARG for stats NULL with T > 0.
  */
-int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+int grpo_loss_fwd_bwd_vocab_shard(const void* logits, int32_t dtype, int64_t T, int64_t V_shard, int64_t ld,
                                   int64_t v_begin, int64_t V_total, const grpo_vocab_stats* stats, int32_t n_shards,
                                   const int32_t* actions, const float* behave_logp, const float* prox_logp,
                                   const float* adv, const grpo_segments* seg, const grpo_loss_params* p,

@@ -1,7 +1,8 @@
 """Builds libgrpo.so (HIP, gfx950) in-tree with hipcc.
 
-Every .hip under csrc/ is compiled to an object in parallel, then linked into
-paper_2606_05597_amd/libgrpo.so.  Always rebuilds when called.
+Every .hip directly under csrc/ is compiled to an object in parallel, then linked
+into paper_2606_05597_amd/libgrpo.so; csrc/bench/stream_copy.hip (the
+benchmark's copy ceiling) becomes libgrpo_bench.so.  Always rebuilds when called.
 """
 from __future__ import annotations
 
@@ -16,6 +17,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 SO = os.path.join(PKG, "libgrpo.so")
+# the benchmark's streaming-copy ceiling, a separate library outside libgrpo's ABI
+BENCH_SRC = os.path.join(CSRC, "bench", "stream_copy.hip")
+BENCH_SO = os.path.join(PKG, "libgrpo_bench.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed fp32 VALU instructions are disabled on purpose: the row kernels use
@@ -42,6 +46,9 @@ def build(jobs: int = 8) -> str:
     tmp = SO + ".tmp"
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, SO)
+    tmp = BENCH_SO + ".tmp"
+    subprocess.check_call([HIPCC, *FLAGS, "-shared", BENCH_SRC, "-o", tmp])
+    os.replace(tmp, BENCH_SO)
     return SO
 
 

@@ -911,8 +911,13 @@ static int check_fused_shapes(int64_t T, int64_t H, int64_t V) {
 
 using namespace grpo;
 
+// Sizes a fused workspace query answers (the entry points accept no larger ones); their products cannot overflow.
+static bool fused_query_sizes_ok(int64_t T, int64_t H, int64_t V) {
+  return T >= 0 && T <= kMaxFusedLen && H >= 1 && H < (1 << 30) && V >= 1 && V <= kMaxFusedLen;
+}
+
 extern "C" size_t fused_lmhead_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t vocab_chunk, int32_t n_traj) {
-  if (T < 0 || H < 1 || V < 1 || vocab_chunk < 1 || n_traj < 1) return 0;
+  if (!fused_query_sizes_ok(T, H, V) || vocab_chunk < 1 || n_traj < 1) return 0;
   return lm_ws_layout(T, H, V, vocab_chunk, n_traj).total;
 }
 
@@ -981,7 +986,9 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
 
 extern "C" size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t token_block,
                                                       int32_t n_traj) {
-  if (T < 0 || H < 1 || V < 1 || token_block < TILE || token_block % TILE != 0 || n_traj < 1) return 0;
+  if (!fused_query_sizes_ok(T, H, V) || token_block < TILE || token_block % TILE != 0 || token_block > kMaxFusedLen ||
+      n_traj < 1)
+    return 0;
   return lm_block_ws_layout(T, H, V, token_block, n_traj).total;
 }
 
@@ -1151,7 +1158,7 @@ static LmLogpWs lm_logp_ws_layout(int64_t T, int64_t H, int64_t V) {
 }
 
 extern "C" size_t fused_lmhead_token_logp_workspace_bytes(int64_t T, int64_t H, int64_t V) {
-  if (T < 0 || H < 1 || V < 1) return 0;
+  if (!fused_query_sizes_ok(T, H, V)) return 0;
   return lm_logp_ws_layout(T, H, V).total;
 }
 
@@ -1195,12 +1202,12 @@ extern "C" int fused_lmhead_token_logp(const void* hidden, const void* w_lm, int
 }
 
 extern "C" size_t fused_lmhead_vocab_shard_stats_workspace_bytes(int64_t T, int64_t H, int64_t V_shard) {
-  if (T < 0 || H < 1 || V_shard < 1) return 0;
+  if (!fused_query_sizes_ok(T, H, V_shard)) return 0;
   return lm_stats_ws_layout(T, H, V_shard).total;
 }
 
 extern "C" size_t fused_lmhead_vocab_shard_logits_bytes(int64_t T, int64_t V_shard) {
-  if (T < 0 || V_shard < 1) return 0;
+  if (!fused_query_sizes_ok(T, 1, V_shard)) return 0;
   return sizeof(float) * (size_t)((T + TILE - 1) / TILE * TILE) * (size_t)((V_shard + TILE - 1) / TILE * TILE);
 }
 
@@ -1210,7 +1217,7 @@ extern "C" int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_
                                               size_t ws_bytes, hipStream_t s) {
   int st = check_fused_shapes(T, H, V_shard);
   if (st != GRPO_OK) return st;
-  if (v_begin < 0 || v_begin + V_shard >= ((int64_t)1 << 31)) return GRPO_ERR_SHAPE;
+  if (v_begin < 0 || v_begin >= ((int64_t)1 << 31) - V_shard) return GRPO_ERR_SHAPE;  // V_shard < 2^31 here
   if (!w_shard || (T > 0 && (!hidden || !actions || !stats))) return GRPO_ERR_ARG;
   if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(stats, 8) || !aligned(logits_out, 16))
     return GRPO_ERR_ALIGN;
@@ -1259,8 +1266,8 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
   const int64_t Vsp = (V_shard + TILE - 1) / TILE * TILE;
   if (logits_in) vocab_chunk = (int32_t)Vsp;
   if (vocab_chunk < 256 || vocab_chunk % 256 != 0) return GRPO_ERR_SHAPE;
-  if (v_begin < 0 || V_total >= ((int64_t)1 << 31) || v_begin + V_shard > V_total || n_shards < 1 ||
-      n_shards > 65536)
+  if (v_begin < 0 || V_total >= ((int64_t)1 << 31) || V_shard > V_total || v_begin > V_total - V_shard ||
+      n_shards < 1 || n_shards > 65536)
     return GRPO_ERR_SHAPE;
   if (!aligned(hidden, 16) || !aligned(w_shard, 16) || !aligned(dhidden_partial, 16) || !aligned(dw_shard, 16) ||
       !aligned(stats, 8) || !aligned(logits_in, 16))

@@ -217,12 +217,13 @@ hipError_t launch_vocab_records(const void* logits, grpo_dtype dt, int64_t T, in
 
 using namespace grpo;
 
-extern "C" int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+extern "C" int grpo_token_logp(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                                const int32_t* actions, float* token_logp, float* token_entropy, int32_t* error_flags,
                                hipStream_t s) {
   if (T < 0 || T >= ((int64_t)1 << 31) || V < 1 || ld < V) return GRPO_ERR_SHAPE;
   if (T > 0 && (!logits || !actions)) return GRPO_ERR_ARG;
-  if (dt != GRPO_F32 && dt != GRPO_BF16) return GRPO_ERR_DTYPE;
+  if (dtype != GRPO_F32 && dtype != GRPO_BF16) return GRPO_ERR_DTYPE;
+  const grpo_dtype dt = static_cast<grpo_dtype>(dtype);
   const int esz = (dt == GRPO_BF16) ? 2 : 4;
   if (!aligned(logits, esz)) return GRPO_ERR_ALIGN;
   if (error_flags) hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, error_flags);
@@ -233,14 +234,16 @@ extern "C" int grpo_token_logp(const void* logits, grpo_dtype dt, int64_t T, int
   return hipGetLastError() == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
 }
 
-extern "C" int grpo_vocab_shard_stats(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+extern "C" int grpo_vocab_shard_stats(const void* logits, int32_t dtype, int64_t T, int64_t V_shard, int64_t ld,
                                       int64_t v_begin, const int32_t* actions, grpo_vocab_stats* stats,
                                       int32_t* error_flags, hipStream_t s) {
-  if (T < 0 || T >= ((int64_t)1 << 31) || V_shard < 1 || ld < V_shard || v_begin < 0 ||
-      v_begin + V_shard >= ((int64_t)1 << 31))
+  constexpr int64_t kLim = (int64_t)1 << 31;  // v_begin + V_shard < 2^31, tested without forming the sum first
+  if (T < 0 || T >= kLim || V_shard < 1 || V_shard >= kLim || ld < V_shard || v_begin < 0 ||
+      v_begin >= kLim - V_shard)
     return GRPO_ERR_SHAPE;
   if (T > 0 && (!logits || !actions || !stats)) return GRPO_ERR_ARG;
-  if (dt != GRPO_F32 && dt != GRPO_BF16) return GRPO_ERR_DTYPE;
+  if (dtype != GRPO_F32 && dtype != GRPO_BF16) return GRPO_ERR_DTYPE;
+  const grpo_dtype dt = static_cast<grpo_dtype>(dtype);
   const int esz = (dt == GRPO_BF16) ? 2 : 4;
   if (!aligned(logits, esz) || !aligned(stats, 8)) return GRPO_ERR_ALIGN;
   if (error_flags) hipLaunchKernelGGL(k_clear_flag, dim3(1), dim3(1), 0, s, error_flags);

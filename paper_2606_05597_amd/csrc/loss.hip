@@ -446,12 +446,12 @@ static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, c
 using namespace grpo;
 
 extern "C" size_t grpo_loss_workspace_bytes(int64_t T, int32_t n_traj) {
-  if (T < 0 || n_traj < 1) return 0;
+  if (T < 0 || T >= ((int64_t)1 << 31) || n_traj < 1) return 0;  // the loss entry points refuse T >= 2^31
   return loss_ws_layout(T, n_traj).total;
 }
 
 // Argument checks of the logits path other than the workspace's (GRPO_OK or the error).
-static int check_logits_call(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+static int check_logits_call(const void* logits, int32_t dt, int64_t T, int64_t V, int64_t ld,
                              const int32_t* actions, const float* behave_logp, const float* adv,
                              const grpo_segments* seg, const grpo_loss_params* p, const double* loss_out,
                              const void* dlogits) {
@@ -465,13 +465,14 @@ static int check_logits_call(const void* logits, grpo_dtype dt, int64_t T, int64
   return GRPO_OK;
 }
 
-extern "C" int grpo_loss_fwd_bwd(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+extern "C" int grpo_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t T, int64_t V, int64_t ld,
                                  const int32_t* actions, const float* behave_logp, const float* prox_logp,
                                  const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
                                  double* loss_out, void* dlogits, grpo_aux* aux, void* ws, size_t ws_bytes,
                                  hipStream_t s) {
-  const int st = check_logits_call(logits, dt, T, V, ld, actions, behave_logp, adv, seg, p, loss_out, dlogits);
+  const int st = check_logits_call(logits, dtype, T, V, ld, actions, behave_logp, adv, seg, p, loss_out, dlogits);
   if (st != GRPO_OK) return st;
+  const grpo_dtype dt = static_cast<grpo_dtype>(dtype);
   const LossWs L = loss_ws_layout(T, seg->n_traj);
   if (!ws || ws_bytes < L.total) return GRPO_ERR_WORKSPACE;
   if (!aligned(ws, kAlign)) return GRPO_ERR_ALIGN;
@@ -536,7 +537,7 @@ static int scratch_of_stream(hipStream_t s, char** out) {
   return GRPO_OK;
 }
 
-extern "C" int grpo_loss_fwd_bwd_noalloc(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
+extern "C" int grpo_loss_fwd_bwd_noalloc(const void* logits, int32_t dt, int64_t T, int64_t V, int64_t ld,
                                          const int32_t* actions, const float* behave_logp, const float* prox_logp,
                                          const float* adv, const grpo_segments* seg, const grpo_loss_params* p,
                                          double* loss_out, void* dlogits, grpo_aux* aux, hipStream_t s) {

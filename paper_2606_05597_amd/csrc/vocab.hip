@@ -147,7 +147,7 @@ hipError_t launch_shard_rows(const void* logits, void* dlogits, grpo_dtype dt, i
 
 using namespace grpo;
 
-extern "C" int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, int64_t T, int64_t V_shard, int64_t ld,
+extern "C" int grpo_loss_fwd_bwd_vocab_shard(const void* logits, int32_t dtype, int64_t T, int64_t V_shard, int64_t ld,
                                              int64_t v_begin, int64_t V_total, const grpo_vocab_stats* stats,
                                              int32_t n_shards, const int32_t* actions, const float* behave_logp,
                                              const float* prox_logp, const float* adv, const grpo_segments* seg,
@@ -155,9 +155,11 @@ extern "C" int grpo_loss_fwd_bwd_vocab_shard(const void* logits, grpo_dtype dt, 
                                              grpo_aux* aux, void* ws, size_t ws_bytes, hipStream_t s) {
   int st = check_loss_common(T, actions, behave_logp, adv, seg, p, loss_out);
   if (st != GRPO_OK) return st;
-  if (dt != GRPO_BF16 && dt != GRPO_F32) return GRPO_ERR_DTYPE;
+  if (dtype != GRPO_BF16 && dtype != GRPO_F32) return GRPO_ERR_DTYPE;
+  const grpo_dtype dt = static_cast<grpo_dtype>(dtype);
+  // V_shard <= V_total < 2^31 is established before v_begin + V_shard is formed
   if (V_shard < 1 || ld < V_shard || v_begin < 0 || V_total < 1 || V_total >= ((int64_t)1 << 31) ||
-      v_begin + V_shard > V_total || n_shards < 1 || n_shards > 65536)
+      V_shard > V_total || v_begin > V_total - V_shard || n_shards < 1 || n_shards > 65536)
     return GRPO_ERR_SHAPE;
   if (T > 0 && (!logits || !stats)) return GRPO_ERR_ARG;
   const size_t esz = (dt == GRPO_BF16) ? 2 : 4;
