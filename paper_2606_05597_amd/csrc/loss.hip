@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "device.h"
@@ -35,6 +36,7 @@ struct RowArgs {
   void* dlogits;  // nullable: forward only
   int64_t ld;     // row stride in elements
   int T;
+  int chunk;      // k_rows_pipe: consecutive rows a workgroup takes at a time (>= 1)
   TokenArgs tok;
 };
 
@@ -200,7 +202,14 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
     for (int q = 0; q < NR; ++q) dst[q] = __builtin_amdgcn_raw_buffer_load_b128(src, voff, (NP + q) * VB, kStream);
   };
 
-  int t = blockIdx.x;
+  // Rows go to workgroups in chunks of `chunk` consecutive rows, chunk c to workgroup c mod gridDim.x; a
+  // workgroup walks its chunks in order, so the row it stages next is usually the one after the row it writes.
+  const int C = a.chunk;
+  auto next_row = [&](int r) {
+    const int q = r + 1;
+    return (q % C != 0) ? q : q + ((int)gridDim.x - 1) * C;
+  };
+  int t = blockIdx.x * C;
   if (t >= a.T) return;
   u32x4 reg[NR];
   if (threadIdx.x == 64) sh_in = token_load(a.tok, t);
@@ -208,14 +217,15 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
   load_regs(reg, t, threadIdx.x * 16);
   wait_vmcnt<NR>();  // this wave's LDS part of row t has landed; the register loads may still be in flight
 
-  for (; t < a.T; t += gridDim.x) {
+  for (int t_next = 0; t < a.T; t = t_next) {
     // The thread index is laundered per row so that nothing derived from it
     // is hoisted out of the row loop and kept live across it.
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int voff = tid * 16;
     const bool last_full = tid < nvec - (NV - 1) * NT;
-    const int tn = t + gridDim.x;
+    const int tn = next_row(t);
+    t_next = tn;
     lds_barrier();  // every wave's LDS part of row t has landed, and sh_in holds row t's inputs
     const TokenIn in = sh_in;
     const int act_vec = (in.act >= 0 && in.act < a.tok.V) ? in.act / 8 : -1;
@@ -412,12 +422,13 @@ static const RowKernel kPipe[] = {
     k_rows_pipe<22, 9>,  k_rows_pipe<23, 9>,
 };  // from 15 vectors on, 14 in registers (what fits in 128 VGPRs) and the rest in LDS
 constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 14 register vectors and 9 LDS vectors per thread
-constexpr int64_t kPipeMaxT = (int64_t)1 << 30;  // t + gridDim.x stays far below 2^31
+constexpr int64_t kPipeMaxT = (int64_t)1 << 30;  // t + (gridDim.x - 1) * chunk + 1 stays far below 2^31
 
 struct Launch {
   RowKernel k;
   int nt;
   unsigned grid;
+  int chunk = 1;
 };
 
 static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, const void* logits,
@@ -430,8 +441,12 @@ static Launch pick_row_kernel(grpo_dtype dt, int64_t T, int64_t V, int64_t ld, c
     if (dt == GRPO_BF16 && nv >= kPipeMinNV && nv <= kPipeMaxNV && T <= kPipeMaxT) {
       int n_cu = stream_cu_count(s);  // of the stream's device
       if (n_cu < 1) n_cu = 256;
-      const int64_t g = T < n_cu ? T : n_cu;  // one workgroup per CU (LDS bound)
-      return Launch{kPipe[nv - kPipeMinNV], 1024, (unsigned)g};
+      // chunks of up to 8 rows (1.6-2.5% faster than single rows at 120,000 x 151,936), but at least four chunks
+      // per CU, so that small batches still spread over the chip
+      const int64_t chunk = std::max<int64_t>(1, std::min<int64_t>(8, T / (4 * (int64_t)n_cu)));
+      const int64_t n_chunks = (T + chunk - 1) / chunk;
+      const int64_t g = n_chunks < n_cu ? n_chunks : n_cu;  // one workgroup per CU (LDS bound)
+      return Launch{kPipe[nv - kPipeMinNV], 1024, (unsigned)g, (int)chunk};
     }
     for (const Variant& v : kVariants) {
       if ((int64_t)v.nt * v.nv >= nvec) return Launch{dt == GRPO_BF16 ? v.bf16 : v.f32, v.nt, (unsigned)T};
@@ -487,6 +502,7 @@ extern "C" int grpo_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t T, i
     a.T = (int)T;
     a.tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L, aux);
     const Launch k = pick_row_kernel(dt, T, V, ld, logits, dlogits, s);
+    a.chunk = k.chunk;
     const bool timed = aux && aux->hot_begin && aux->hot_end;
     if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
     if (k.k) {

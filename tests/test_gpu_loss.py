@@ -194,12 +194,14 @@ def _whole_batch_checks(ref, loss, aux, oi, A64, V, ld, what):
     return kinks
 
 
-def _pipeline_rows(T, grid, rng, n_random):
-    """Rows to compare element by element: the first and last rows, each side of the first round boundaries of the
-    persistent row kernel (rows t >= grid are a workgroup's second and later rows, whose LDS part and registers were
-    loaded during the previous row's dlogits pass), the last full round, and random rows."""
-    fixed = [0, 1, grid - 1, grid, grid + 1, 2 * grid - 1, 2 * grid, 2 * grid + 1, 3 * grid + 17, 7 * grid + 100,
-             T // 2, T - grid - 1, T - grid, T - 2, T - 1]
+def _pipeline_rows(T, grid, rng, n_random, chunk=8):
+    """Rows to compare element by element: the first and last rows, rows on each side of the persistent row kernel's
+    chunk and round boundaries (every row but a workgroup's first had its LDS part and registers loaded during the
+    previous row's dlogits pass; a chunk's first row follows the previous chunk's last, grid * chunk rows earlier),
+    and random rows."""
+    fixed = [0, 1, chunk - 1, chunk, chunk + 1, grid - 1, grid, grid + 1, grid * chunk - 1, grid * chunk,
+             grid * chunk + 1, 2 * grid * chunk + 17, 3 * grid + 17, 7 * grid + 100, T // 2, T - grid - 1, T - grid,
+             T - chunk - 1, T - 2, T - 1]
     rows = np.concatenate([fixed, rng.integers(0, T, n_random)])
     return np.unique(rows[(rows >= 0) & (rows < T)])
 
@@ -355,6 +357,17 @@ def test_pipelined_kernel_several_rows_per_workgroup(V):
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     assert b["structure"].T > 2 * n_cu + 64, b["structure"].T
     _full_parity(b, oracle.NORM_TRAJ_STEPS, 3.0)
+
+
+@pytest.mark.parametrize("V", [122880, 151936])
+def test_pipelined_kernel_row_chunks(V):
+    # T above 8 x the CU count: rows go to workgroups in chunks of two consecutive rows (a workgroup's next row is
+    # either the row after the current one or the first of its next chunk, 2 x grid rows on); every row under the
+    # scaled bf16 gate
+    b = _edge_batch(V, "bf16", n_groups=8, G=4, seed=V % 97 + 1, max_tok=72)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert b["structure"].T >= 8 * n_cu, b["structure"].T
+    _full_parity(b, oracle.NORM_CONST_K, 3.0)
 
 
 def test_padded_row_stride():
