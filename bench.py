@@ -7,19 +7,28 @@ row pass with dlogits, loss reduction).  Workload: 16 task groups x G = 8
 trajectories, T = 120,000 action tokens, V = 151,936, bf16 logits (the
 realistic-vocabulary rollout batch), synthetic and seeded.
 
-One device's share of the vocabulary-parallel loss (the same batch's vocabulary
-split 8 ways, 18,992 columns) is reported under "vocab_shard", and the
-forward-only log-prob + entropy pass under "token_logp".
+The same batch with the per-trajectory normaliser 1/|tau_i| is reported under
+"normaliser_traj_steps", one device's share of the vocabulary-parallel loss (the
+batch's vocabulary split 8 ways, 18,992 columns) under "vocab_shard", and the
+forward-only log-prob + entropy pass under "token_logp".  The other logits
+workloads run the same step: "long" (32 groups, T = 250,000, V = 151,936, 76 GB
+of logits and 76 GB of dlogits resident), "v32k" (8 groups, T of about 32,000,
+V = 32,000, bf16) and "tiny" (one group of 4, fp32 [192, 1024]), each with its
+own roofline line.
 
 The fused LM-head path is measured in the same run on its own workload
-(hidden bf16 [65,536, 3,584], W bf16 [3,584, 151,936], vocabulary chunks of
-8192) and reported under "fused_lmhead" against the bf16 dense MFMA peak, with
-the algorithmic work of three products (6 T H V flop) and the four executed.
+(hidden bf16 [65,536, 3,584], W bf16 [3,584, 151,936]) and reported under
+"fused_lmhead" against the bf16 dense MFMA peak with the algorithmic work of
+three products (6 T H V flop): token blocks of 8192 rows with each block's D
+pass on a second stream (the line's value), the same on one stream, and
+vocabulary chunks of 8192 (four products executed) beside it.
 
 Prints one JSON line.  ``value`` is tokens/s of the whole step.  ``roofline``
 reports the dominant kernel (the row pass): algorithmic bytes per launch,
 T * (4V + 16), over its average duration from HIP events recorded around it
-on its stream; ``traffic`` is the HBM traffic measured with rocprofv3 counters
+on its stream, with the copy ceiling of the same two buffers beside it (the
+fastest hand-written streaming copy of the logits into the dlogits buffer, timed
+in the same process); ``traffic`` is the HBM traffic measured with rocprofv3 counters
 (FETCH_SIZE, WRITE_SIZE) scaled by a plain copy's reading, when the committed
 measurement matches the current kernel source, else null.  ``cpu_baseline``
 times the fp64 oracle on the host on a bounded sample of the same batch.
