@@ -418,14 +418,34 @@ def test_malformed_offsets_flagged():
     assert (aux.traj_tok_off.cpu() == -1).all()
 
 
-@pytest.mark.parametrize("V,dtype", [(256, "bf16"), (200000, "bf16")])  # one pass; two passes
+@pytest.mark.parametrize("V,dtype", [(256, "bf16"), (32000, "bf16"), (151936, "bf16"), (200000, "bf16")])
 def test_nonfinite_logit_flagged(V, dtype):
+    # resident kernels (one workgroup per row), the pipelined kernel, two passes
     b = _edge_batch(V, dtype)
     b["logits"][2, 5] = float("nan")
     _, A32 = _adv(b)
     loss, dl, aux = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=4.0)
     assert aux.error_flags.item() & grpo.GRPO_FLAG_NONFINITE
     assert math.isnan(loss) and math.isnan(aux.token_logp[2].item())
+
+
+@pytest.mark.parametrize("V,dtype", [(256, "bf16"), (1024, "f32"), (32000, "bf16"), (151936, "bf16"),
+                                     (200000, "bf16")])
+def test_masked_logits(V, dtype):
+    # -inf logits (a masked vocabulary) are valid input: they carry zero probability, the row's log-sum-exp
+    # stays finite, nothing is flagged, and their dlogits are zero.  About a tenth of the columns of every
+    # row, both bf16 halves of a dword, never the action's.
+    from synth.rollouts import add_noise, engine_logp
+    b = _edge_batch(V, dtype, seed=11)
+    T = b["logits"].shape[0]
+    g = torch.Generator("cuda").manual_seed(V)
+    mask = torch.rand((T, V), generator=g, device="cuda") < 0.1
+    mask[torch.arange(T, device="cuda"), b["actions"].long()] = False
+    b["logits"][:, :V].masked_fill_(mask, float("-inf"))
+    b["behave"] = add_noise(engine_logp(b["logits"], b["actions"], V), 0.1, 11)
+    ref, loss, dl, aux = _full_parity(b, oracle.NORM_CONST_K, 0.0)
+    assert aux.error_flags.item() == 0 and math.isfinite(loss)
+    assert (dl[:, :V][mask] == 0).all()
 
 
 @pytest.mark.parametrize("V,dtype", [(4096, "bf16"), (100000, "f32")])  # one pass; two passes
