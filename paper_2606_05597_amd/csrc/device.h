@@ -54,6 +54,58 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
   return v;
 }
 
+// ---- DPP reductions -----------------------------------------------------------
+// Lane moves inside a row of 16 lanes go through the VALU (DPP) rather than the
+// LDS crossbar that __shfl_xor uses, so a step costs a few cycles instead of an
+// LDS round trip.  Every source lane of these patterns is valid.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32v(float x) { return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(x))); }
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  const uint64_t lo = dpp_u32<CTRL>((uint32_t)u), hi = dpp_u32<CTRL>((uint32_t)(u >> 32));
+  return __builtin_bit_cast(double, lo | (hi << 32));
+}
+// Max (sum) over each row of 16 lanes, in every lane of the row: swaps within
+// quads (quad_perm [1, 0, 3, 2] = 0xB1, [2, 3, 0, 1] = 0x4E), then across the
+// halves of each 8-lane group (row_half_mirror = 0x141), then across the two
+// 8-lane groups (row_mirror = 0x140).
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_f32v<0xB1>(v));
+  v = fmaxf(v, dpp_f32v<0x4E>(v));
+  v = fmaxf(v, dpp_f32v<0x141>(v));
+  return fmaxf(v, dpp_f32v<0x140>(v));
+}
+__device__ __forceinline__ double row16_sum(double v) {
+  v += dpp_f64<0xB1>(v);
+  v += dpp_f64<0x4E>(v);
+  v += dpp_f64<0x141>(v);
+  return v + dpp_f64<0x140>(v);
+}
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, lo | (hi << 32));
+}
+// Over the whole wave (all 64 lanes active), the same value in every lane.
+__device__ __forceinline__ float wave_max_dpp(float v) {
+  v = row16_max(v);
+  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+__device__ __forceinline__ double wave_sum_dpp(double v) {
+  v = row16_sum(v);
+  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+}
+
 // ---- per-token surrogate (Eq. 1 with the dual clip of Eq. 2) ----------------
 // Bits of the per-token state.
 constexpr int kStateEpsCut = 1;     // the eps clip held the term (its gradient is cut)

@@ -106,16 +106,19 @@ __device__ __forceinline__ float vec_sumexp(const u32x4& x, float nmb) {
 }
 
 // Combines every thread's (max m, sum s of exp(z - m)) into the row's (M, S),
-// valid in thread 0: within each wave, then across the NW waves by the lanes of
-// wave 0, one wave partial per lane.  The rescale factors exp(m - M) <= 1 are
-// fp32 and the sums fp64.  Ends with every wave past a barrier.
+// valid in thread 0: within each wave (DPP within rows of 16 lanes, then the
+// four rows), then across the NW <= 16 waves by the first 16 lanes of wave 0,
+// one wave partial per lane.  The rescale factors exp(m - M) <= 1 are fp32 and
+// the sums fp64.  Every lane of the workgroup takes part.  Ends with every wave
+// past a barrier.
 template <int NW>
 __device__ __forceinline__ void block_combine(float m, float s, float* sh_m, double* sh_s, double& M_out,
                                               double& S_out) {
+  static_assert(NW >= 1 && NW <= 16, "one wave partial per lane of a 16-lane row");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const float mw = wave_max(m);
+  const float mw = wave_max_dpp(m);
   const double sw =
-      wave_sum((m == -INFINITY) ? 0.0 : (double)s * (double)__builtin_amdgcn_exp2f((m - mw) * kLog2e));
+      wave_sum_dpp((m == -INFINITY) ? 0.0 : (double)s * (double)__builtin_amdgcn_exp2f((m - mw) * kLog2e));
   if (lane == 0) {
     sh_m[wv] = mw;
     sh_s[wv] = sw;
@@ -123,9 +126,9 @@ __device__ __forceinline__ void block_combine(float m, float s, float* sh_m, dou
   __syncthreads();
   if (wv == 0) {
     const float mq = lane < NW ? sh_m[lane] : -INFINITY;
-    const float M = wave_max(mq);
+    const float M = row16_max(mq);
     const double S =
-        wave_sum(mq == -INFINITY ? 0.0 : sh_s[lane < NW ? lane : 0] * (double)__builtin_amdgcn_exp2f((mq - M) * kLog2e));
+        row16_sum(mq == -INFINITY ? 0.0 : sh_s[lane < NW ? lane : 0] * (double)__builtin_amdgcn_exp2f((mq - M) * kLog2e));
     M_out = (double)M;
     S_out = S;
   }
