@@ -198,10 +198,13 @@ def _pipeline_rows(T, grid, rng, n_random, chunk=8):
     """Rows to compare element by element: the first and last rows, rows on each side of the persistent row kernel's
     chunk and round boundaries (every row but a workgroup's first had its LDS part and registers loaded during the
     previous row's dlogits pass; a chunk's first row follows the previous chunk's last, grid * chunk rows earlier),
+    the boundaries of the last rows' even split (the rows after the whole rounds, r0 on, go chunk2 to a workgroup),
     and random rows."""
+    r0 = T // (chunk * grid) * (chunk * grid)
+    c2 = max(1, -(-(T - r0) // grid))
     fixed = [0, 1, chunk - 1, chunk, chunk + 1, grid - 1, grid, grid + 1, grid * chunk - 1, grid * chunk,
              grid * chunk + 1, 2 * grid * chunk + 17, 3 * grid + 17, 7 * grid + 100, T // 2, T - grid - 1, T - grid,
-             T - chunk - 1, T - 2, T - 1]
+             T - chunk - 1, T - 2, T - 1, r0 - 1, r0, r0 + 1, r0 + c2 - 1, r0 + c2, r0 + 7 * c2 - 1, r0 + 7 * c2]
     rows = np.concatenate([fixed, rng.integers(0, T, n_random)])
     return np.unique(rows[(rows >= 0) & (rows < T)])
 
@@ -362,8 +365,8 @@ def test_pipelined_kernel_several_rows_per_workgroup(V):
 @pytest.mark.parametrize("V", [122880, 151936])
 def test_pipelined_kernel_row_chunks(V):
     # T above 8 x the CU count: rows go to workgroups in chunks of two consecutive rows (a workgroup's next row is
-    # either the row after the current one or the first of its next chunk, 2 x grid rows on); every row under the
-    # scaled bf16 gate
+    # either the row after the current one or the first of its next chunk, 2 x grid rows on), the rows after the
+    # whole rounds split evenly, one chunk per workgroup; every row under the scaled bf16 gate
     b = _edge_batch(V, "bf16", n_groups=8, G=4, seed=V % 97 + 1, max_tok=72)
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     assert b["structure"].T >= 8 * n_cu, b["structure"].T
