@@ -380,6 +380,20 @@ def test_padded_row_stride():
     _full_parity(b, oracle.NORM_CONST_K, 0.0)
 
 
+@pytest.mark.parametrize("V,ld", [(151936, 152064), (122880, 122888)])
+def test_padded_row_stride_pipelined(V, ld):
+    # the pipelined kernel on rows whose stride exceeds V (several rows per workgroup): every row under the scaled
+    # bf16 gate, and the padding columns of a caller's dlogits buffer are left as they were
+    b = _edge_batch(V, "bf16", ld=ld, n_groups=8, G=4, seed=V % 89 + 2, max_tok=40)
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert b["structure"].T >= 2 * n_cu, b["structure"].T
+    _full_parity(b, oracle.NORM_CONST_K, 3.0)
+    _, A32 = _adv(b)
+    dl = torch.full_like(b["logits"], 7.0)
+    run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=b["cfg"].k, c=3.0, dlogits=dl, aux=False)
+    assert (dl[:, V:] == 7.0).all()
+
+
 def test_empty_batch():
     # T = 0: every trajectory holds steps with no action token; the loss is 0
     N = 4
