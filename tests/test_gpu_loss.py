@@ -465,9 +465,13 @@ def test_masked_logits(V, dtype):
     assert (dl[:, :V][mask] == 0).all()
 
 
-@pytest.mark.parametrize("V,dtype", [(4096, "bf16"), (100000, "f32")])  # one pass; two passes
-def test_forward_only_and_aliasing(V, dtype):
-    b = _edge_batch(V, dtype)
+@pytest.mark.parametrize("V,dtype,big", [(4096, "bf16", False), (100000, "f32", False), (151936, "bf16", True)])
+def test_forward_only_and_aliasing(V, dtype, big):
+    # one pass (resident), two passes, and the pipelined kernel with several rows per workgroup (each row's
+    # dlogits overwrite it in place while the workgroup's next row is being loaded)
+    b = _edge_batch(V, dtype, n_groups=8, G=4, seed=13, max_tok=72) if big else _edge_batch(V, dtype)
+    if big:
+        assert b["structure"].T >= 4 * torch.cuda.get_device_properties(0).multi_processor_count
     _, A32 = _adv(b)
     l0, dl0, a0 = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=4.0, c=3.0)
     l1, dl1, a1 = run_gpu(b, A32, norm=grpo.GRPO_NORM_CONST_K, k=4.0, c=3.0, dlogits=None)
