@@ -17,6 +17,8 @@ H x V with fewer tokens, and at full size through identities that hold at any
 size: each row of dW sums to ~0 (each dlogits row sums to 0) and
 <dW, W> = <dhidden, h> (= <D, z>).
 """
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -336,6 +338,27 @@ def test_fused_invalid_action_row_zero(sched):
                            None, A64, seg, 4, norm=oracle.NORM_CONST_K, k=4.0)
     assert ref.rows.flags == oracle.ERR_ACTION
     check_fused_loss(loss, ref.rows.token_contrib, "loss with an invalid action")
+
+
+@pytest.mark.parametrize("sched", [256, Blocked(256)])
+def test_fused_nonfinite_hidden_row(sched):
+    # a NaN hidden row: its logits, log-sum-exp and log-prob are NaN and flagged and the loss is NaN, while every
+    # other row's log-prob and dhidden row are those of the clean batch bit for bit (rows stay independent through
+    # the products); dW takes the NaN row's terms
+    b = make_fused_batch(small_cfg(2, 4, 64, 1000, seed=21), "cuda")
+    A64, A32, seg, sto, tso = setup(b)
+    T = b["structure"].T
+    l0, dh0, dW0, a0 = run(b, A32, sto, tso, sched, oracle.NORM_CONST_K, 3.0)
+    assert a0.error_flags.item() == 0 and math.isfinite(l0)
+    r = T // 2
+    b["hidden"][r] = float("nan")
+    l1, dh1, dW1, a1 = run(b, A32, sto, tso, sched, oracle.NORM_CONST_K, 3.0)
+    assert a1.error_flags.item() & grpo.GRPO_FLAG_NONFINITE
+    assert math.isnan(l1) and math.isnan(a1.token_logp[r].item())
+    keep = torch.arange(T, device="cuda") != r
+    assert torch.equal(a1.token_logp[keep], a0.token_logp[keep])
+    assert np.array_equal(bits(dh1[keep]), bits(dh0[keep]))
+    assert torch.isnan(dW1).any()
 
 
 def test_fused_rejects_bad_shapes():
