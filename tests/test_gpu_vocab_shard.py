@@ -183,6 +183,27 @@ def test_v152k_eight_shards_full_size():
     assert auxes[0].error_flags.item() == 0
 
 
+@pytest.mark.parametrize("bounds", [[0, 512, 1024], [0, 100, 612, 1024]])
+def test_masked_logits_whole_shard(bounds):
+    # -inf logits (a masked vocabulary), about a tenth of the columns, and in every other row the whole of the
+    # middle shard unless the action falls there: that shard's record is then (max -inf, sum 0), which the merge
+    # must skip.  Never the action's column.
+    from synth.rollouts import add_noise, engine_logp
+    b = make_batch("tiny", "cuda")
+    T, V = b["logits"].shape
+    g = torch.Generator("cuda").manual_seed(len(bounds))
+    mask = torch.rand((T, V), generator=g, device="cuda") < 0.1
+    act = b["actions"].long()
+    lo, hi = bounds[1], bounds[2]
+    whole = (torch.arange(T, device="cuda") % 2 == 0) & ((act < lo) | (act >= hi))
+    mask[whole, lo:hi] = True
+    mask[torch.arange(T, device="cuda"), act] = False
+    b["logits"].masked_fill_(mask, float("-inf"))
+    b["behave"] = add_noise(engine_logp(b["logits"], b["actions"], V), 0.1, 3)
+    loss, dl, aux = _shard_parity(b, bounds, oracle.NORM_CONST_K, 3.0)
+    assert (dl[mask] == 0).all()
+
+
 def test_global_group_count():
     # n_groups_total as a data-parallel shard of a larger batch passes it: every w_i, the loss and dlogits scale
     b = make_batch("tiny", "cuda")
