@@ -11,6 +11,7 @@
 // log-sum-exp is m + log s and its entropy -sum p log p = log s - t / s; both
 // terms of the entropy are >= 0, so it has no cancellation even when small.
 #include <hip/hip_runtime.h>
+#include <float.h>
 #include <math.h>
 
 #include "device.h"
@@ -33,34 +34,42 @@ struct LogpArgs {
   grpo_vocab_stats* stats;  // non-null: write each row's shard record instead of logp / entropy
 };
 
-// One element folded into (s, t) at the current shift m.
-__device__ __forceinline__ void fold(float z, float m, float nmb, float& s, float& t) {
-  const float e = __builtin_amdgcn_exp2f(fmaf(z, kLog2e, nmb));
+// One element folded into (s, t) at the current shift m: s = sum e^(z - m), t = sum e^(z - m) w with
+// w = (z - m) log2(e), the argument the exp2 takes anyway (t is in log2 units; row_out converts).  A -inf logit (a
+// masked column) has e = 0 and adds no term (0 log 0 = 0): its w = -inf is clamped to -FLT_MAX in the product,
+// which is then 0, not NaN.  A NaN logit still makes e, and so s and t, NaN.
+__device__ __forceinline__ void fold(float z, float nmb, float& s, float& t) {
+  const float w = fmaf(z, kLog2e, nmb);
+  const float e = __builtin_amdgcn_exp2f(w);
   s += e;
-  t = fmaf(e, z - m, t);
+  t = fmaf(e, fmaxf(w, -FLT_MAX), t);
 }
 
 // Raises the shift to mn >= m: s and t are re-expressed relative to mn.
 __device__ __forceinline__ void rescale(float& m, float mn, float& s, float& t) {
   if (mn > m) {
     if (m != -INFINITY) {
-      const float d = mn - m, f = __builtin_amdgcn_exp2f(-d * kLog2e);
-      t = f * fmaf(-d, s, t);
+      const float dl = (mn - m) * kLog2e, f = __builtin_amdgcn_exp2f(-dl);
+      t = f * fmaf(-dl, s, t);
       s *= f;
     }
     m = mn;
   }
 }
 
-// Combines every thread's (m, s, t) into the row's (M, S, T) in fp64, valid in thread 0.
+// Combines every thread's (m, s, t) into the row's (M, S, T) in fp64, valid in thread 0 (t and T in log2 units):
+// within each wave (DPP within rows of 16 lanes, then the four rows), then across the NW <= 16 waves by the first
+// 16 lanes of wave 0.  Every lane of the workgroup takes part.
 template <int NW>
 __device__ __forceinline__ void block_combine3(float m, float s, float t, float* sh_m, double* sh_s, double* sh_t,
                                                double& M_out, double& S_out, double& T_out) {
+  static_assert(NW >= 1 && NW <= 16, "one wave partial per lane of a 16-lane row");
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const float mw = wave_max(m);
+  const double L = (double)kLog2e;
+  const float mw = wave_max_dpp(m);
   const double f = (m == -INFINITY) ? 0.0 : (double)__builtin_amdgcn_exp2f((m - mw) * kLog2e);
-  const double sw = wave_sum(f * (double)s);
-  const double tw = wave_sum(m == -INFINITY ? 0.0 : f * ((double)t + ((double)m - (double)mw) * (double)s));
+  const double sw = wave_sum_dpp(f * (double)s);
+  const double tw = wave_sum_dpp(m == -INFINITY ? 0.0 : f * ((double)t + ((double)m - (double)mw) * L * (double)s));
   if (lane == 0) {
     sh_m[wv] = mw;
     sh_s[wv] = sw;
@@ -69,11 +78,11 @@ __device__ __forceinline__ void block_combine3(float m, float s, float t, float*
   __syncthreads();
   if (wv == 0) {
     const float mq = lane < NW ? sh_m[lane] : -INFINITY;
-    const float M = wave_max(mq);
+    const float M = row16_max(mq);
     const double g = (mq == -INFINITY) ? 0.0 : exp((double)mq - (double)M);
     const int q = lane < NW ? lane : 0;
-    const double S = wave_sum(g * sh_s[q]);
-    const double T = wave_sum(mq == -INFINITY ? 0.0 : g * (sh_t[q] + ((double)mq - (double)M) * sh_s[q]));
+    const double S = row16_sum(g * sh_s[q]);
+    const double T = row16_sum(mq == -INFINITY ? 0.0 : g * (sh_t[q] + ((double)mq - (double)M) * L * sh_s[q]));
     M_out = (double)M;
     S_out = S;
     T_out = T;
@@ -105,7 +114,8 @@ __device__ __forceinline__ void row_out(const LogpArgs& a, int t, double M, doub
   }
   const double lse = M + log(S);
   if (a.logp) a.logp[t] = act_ok ? (float)(za - lse) : 0.f;
-  if (a.entropy) a.entropy[t] = (float)(log(S) - Tsum / S);
+  // Tsum is in log2 units: sum e^(z - M) (z - M) = Tsum / log2(e)
+  if (a.entropy) a.entropy[t] = (float)(log(S) - Tsum / ((double)kLog2e * S));
   if (a.flags) {
     if (!act_ok) atomicOr(a.flags, GRPO_FLAG_ACTION);
     if (!isfinite(lse)) atomicOr(a.flags, GRPO_FLAG_NONFINITE);
@@ -139,8 +149,7 @@ __global__ __launch_bounds__(NT) void k_logp_vec(const LogpArgs a) {
     for (int u = 0; u < U; ++u) {
       const int vi = base + u * NT;
       if (vi < nvec) {
-#pragma unroll
-        for (int e = 0; e < EPV; ++e) cm = fmaxf(cm, elem<Tin>(x[u], e));
+        cm = vec_max<Tin>(x[u], cm);
         if (vi == act_vec) sh_za = elem<Tin>(x[u], act % EPV);
       }
     }
@@ -151,7 +160,7 @@ __global__ __launch_bounds__(NT) void k_logp_vec(const LogpArgs a) {
       const int vi = base + u * NT;
       if (vi < nvec) {
 #pragma unroll
-        for (int e = 0; e < EPV; ++e) fold(elem<Tin>(x[u], e), m, nmb, s, tt);
+        for (int e = 0; e < EPV; ++e) fold(elem<Tin>(x[u], e), nmb, s, tt);
       }
     }
   }
@@ -180,7 +189,7 @@ __global__ __launch_bounds__(256) void k_logp_generic(const LogpArgs a) {
   const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
   float s = 0.f, tt = 0.f;
   if (m != -INFINITY)
-    for (int64_t v = tid; v < a.V; v += NT) fold(load_one<Tin>(row + v), m, nmb, s, tt);
+    for (int64_t v = tid; v < a.V; v += NT) fold(load_one<Tin>(row + v), nmb, s, tt);
   double M, S, Tsum;
   block_combine3<NW>(m, s, tt, sh_m, sh_s, sh_t, M, S, Tsum);
   if (tid == 0) {

@@ -67,30 +67,6 @@ __device__ __forceinline__ float vec_elem(const u32x4& x, int e) {
   }
 }
 
-// max(a, b, c) in one instruction.  Written as asm because the compiler otherwise canonicalises every loaded
-// value before an fmaxf (two more instructions per dword of logits).  In IEEE mode a quiet NaN operand is
-// ignored, as by fmaxf, and a signalling NaN makes the result NaN; either way a NaN logit also makes the row's
-// sum of exponentials NaN, so the row is flagged as before.
-__device__ __forceinline__ float max3f(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
-
-// Maximum of m and the vector's elements (the exp shift of the row).
-template <typename Tin>
-__device__ __forceinline__ float vec_max(const u32x4& x, float m) {
-  if constexpr (sizeof(Tin) == 2) {
-    const float a = max3f(bf16_lo(x[0]), bf16_hi(x[0]), bf16_lo(x[1]));
-    const float b = max3f(bf16_hi(x[1]), bf16_lo(x[2]), bf16_hi(x[2]));
-    const float c = max3f(bf16_lo(x[3]), bf16_hi(x[3]), m);
-    return max3f(a, b, c);
-  } else {
-    return max3f(max3f(m, __uint_as_float(x[0]), __uint_as_float(x[1])), __uint_as_float(x[2]),
-                 __uint_as_float(x[3]));
-  }
-}
-
 // sum of exp(z - m) over the vector, with nmb = -m*log2(e)
 template <typename Tin>
 __device__ __forceinline__ float vec_sumexp(const u32x4& x, float nmb) {

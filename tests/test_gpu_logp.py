@@ -91,6 +91,26 @@ def test_vocab_sizes_strides_and_kernels(V, dtype, ld):
     assert flags == 0
 
 
+@pytest.mark.parametrize("V,dtype,ld", [(7, torch.float32, None), (4096, torch.bfloat16, None),
+                                        (151936, torch.bfloat16, None), (1000, torch.float32, 1003)])
+def test_masked_logits(V, dtype, ld):
+    # -inf logits (a masked vocabulary): zero probability, no term in the entropy (0 log 0 = 0), nothing flagged;
+    # about a third of the columns, never the action's, on the element-wise and the vector kernels
+    g = torch.Generator("cuda").manual_seed(V + 1)
+    T = 37
+    full = torch.randn((T, ld or V), generator=g, device="cuda") * 2.0
+    actions = torch.randint(0, V, (T,), generator=g, device="cuda", dtype=torch.int32)
+    mask = torch.rand((T, V), generator=g, device="cuda") < 0.3
+    mask[torch.arange(T, device="cuda"), actions.long()] = False
+    full[:, :V].masked_fill_(mask, float("-inf"))
+    logits = full.to(dtype)
+    logp, ent, flags = run(logits, actions, V=V)
+    ref = oracle.logp_entropy(to_np_logits(logits), actions.cpu().numpy(), V=V)
+    assert np.isfinite(ref.token_entropy).all() and ref.flags == 0
+    check(logp, ent, ref, f"masked V={V}")
+    assert flags == 0
+
+
 def test_constant_and_peaked_rows():
     V = 4096
     logits = torch.zeros((3, V), dtype=torch.bfloat16, device="cuda")
