@@ -38,19 +38,22 @@ struct LogpArgs {
 // w = (z - m) log2(e), the argument the exp2 takes anyway (t is in log2 units; row_out converts).  A -inf logit (a
 // masked column) has e = 0 and adds no term (0 log 0 = 0): its w = -inf is clamped to -FLT_MAX in the product,
 // which is then 0, not NaN.  A NaN logit still makes e, and so s and t, NaN.
+// ENT = false: s only (t stays 0), for the calls that want no entropy.
+template <bool ENT = true>
 __device__ __forceinline__ void fold(float z, float nmb, float& s, float& t) {
   const float w = fmaf(z, kLog2e, nmb);
   const float e = __builtin_amdgcn_exp2f(w);
   s += e;
-  t = fmaf(e, fmaxf(w, -FLT_MAX), t);
+  if constexpr (ENT) t = fmaf(e, fmaxf(w, -FLT_MAX), t);
 }
 
 // Raises the shift to mn >= m: s and t are re-expressed relative to mn.
+template <bool ENT = true>
 __device__ __forceinline__ void rescale(float& m, float mn, float& s, float& t) {
   if (mn > m) {
     if (m != -INFINITY) {
       const float dl = (mn - m) * kLog2e, f = __builtin_amdgcn_exp2f(-dl);
-      t = f * fmaf(-dl, s, t);
+      if constexpr (ENT) t = f * fmaf(-dl, s, t);
       s *= f;
     }
     m = mn;
@@ -122,8 +125,9 @@ __device__ __forceinline__ void row_out(const LogpArgs& a, int t, double M, doub
   }
 }
 
-// Rows of 16-byte vectors (V a multiple of the vector width, 16-byte aligned rows).
-template <typename Tin, int NT, int U>
+// Rows of 16-byte vectors (V a multiple of the vector width, 16-byte aligned rows).  ENT: the entropy moment
+// is accumulated (not for a shard's records or a call without an entropy output).
+template <typename Tin, int NT, int U, bool ENT>
 __global__ __launch_bounds__(NT) void k_logp_vec(const LogpArgs a) {
   constexpr int EPV = 16 / sizeof(Tin), NW = NT / 64;
   __shared__ float sh_m[NW];
@@ -153,14 +157,14 @@ __global__ __launch_bounds__(NT) void k_logp_vec(const LogpArgs a) {
         if (vi == act_vec) sh_za = elem<Tin>(x[u], act % EPV);
       }
     }
-    rescale(m, cm, s, tt);
+    rescale<ENT>(m, cm, s, tt);
     const float nmb = (m == -INFINITY) ? 0.f : -m * kLog2e;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int vi = base + u * NT;
       if (vi < nvec) {
 #pragma unroll
-        for (int e = 0; e < EPV; ++e) fold(elem<Tin>(x[u], e), nmb, s, tt);
+        for (int e = 0; e < EPV; ++e) fold<ENT>(elem<Tin>(x[u], e), nmb, s, tt);
       }
     }
   }
@@ -206,10 +210,18 @@ static void launch_logp(const LogpArgs& a, grpo_dtype dt, hipStream_t s) {
   const int esz = (dt == GRPO_BF16) ? 2 : 4, epv = 16 / esz;
   const bool vec = a.V % epv == 0 && a.ld % epv == 0 && aligned(a.logits, 16);
   const dim3 grid((unsigned)a.T);
-  if (vec && dt == GRPO_BF16) hipLaunchKernelGGL((k_logp_vec<uint16_t, 256, 4>), grid, dim3(256), 0, s, a);
-  else if (vec) hipLaunchKernelGGL((k_logp_vec<float, 256, 4>), grid, dim3(256), 0, s, a);
-  else if (dt == GRPO_BF16) hipLaunchKernelGGL(k_logp_generic<uint16_t>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_logp_generic<float>, grid, dim3(256), 0, s, a);
+  const bool ent = a.entropy && !a.stats;
+  if (vec && dt == GRPO_BF16) {
+    if (ent) hipLaunchKernelGGL((k_logp_vec<uint16_t, 256, 4, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_logp_vec<uint16_t, 256, 4, false>), grid, dim3(256), 0, s, a);
+  } else if (vec) {
+    if (ent) hipLaunchKernelGGL((k_logp_vec<float, 256, 4, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_logp_vec<float, 256, 4, false>), grid, dim3(256), 0, s, a);
+  } else if (dt == GRPO_BF16) {
+    hipLaunchKernelGGL(k_logp_generic<uint16_t>, grid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL(k_logp_generic<float>, grid, dim3(256), 0, s, a);
+  }
 }
 
 hipError_t launch_vocab_records(const void* logits, grpo_dtype dt, int64_t T, int64_t V, int64_t ld,
