@@ -111,6 +111,27 @@ def test_masked_logits(V, dtype, ld):
     assert flags == 0
 
 
+@pytest.mark.parametrize("V,dtype,ld", [(151936, torch.bfloat16, None), (1000, torch.float32, 1003)])
+def test_masked_uniform_rows_closed_form(V, dtype, ld):
+    # k equal finite logits among V - k masked (-inf) ones: log-prob -log k and entropy log k, the uniform row of
+    # width k (the oracle's pin); k from 1 to V over the rows, the finite columns scattered, the action among them
+    g = torch.Generator("cuda").manual_seed(V)
+    T = 24
+    ks = [1, 2, 3, 7, 64, 1000, V - 1, V]
+    ks += [int(x) for x in torch.randint(1, V + 1, (T - 8,), generator=g, device="cuda")]
+    full = torch.full((T, ld or V), float("-inf"), device="cuda")
+    actions = torch.empty(T, dtype=torch.int32, device="cuda")
+    for t, k in enumerate(ks):
+        cols = torch.randperm(V, generator=g, device="cuda")[:k]
+        full[t, cols] = float(t % 5) - 2.0
+        actions[t] = cols[0]
+    logp, ent, flags = run(full.to(dtype), actions, V=V)
+    logk = np.log(np.array(ks, np.float64))
+    assert flags == 0
+    assert np.abs(logp + logk).max() <= LOGP_ATOL
+    assert (np.abs(ent - logk) <= ENT_ATOL + ENT_RTOL * logk).all()
+
+
 def test_constant_and_peaked_rows():
     V = 4096
     logits = torch.zeros((3, V), dtype=torch.bfloat16, device="cuda")

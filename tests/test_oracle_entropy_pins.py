@@ -38,6 +38,25 @@ def test_two_level_rows_closed_form():
         assert r.token_logp[0] == pytest.approx(math.log(p_hi), rel=1e-12)
 
 
+def test_masked_columns_drop_out():
+    # -inf logits carry zero probability and no entropy term (0 log 0 = 0): k equal finite logits among V - k
+    # masked ones give H = log k and log-prob -log k exactly, as the uniform row of width k does; a masked row
+    # mixed with a two-level row gives that row's closed form
+    for V, k, c in ((8, 1, 0.0), (100, 7, 2.5), (4096, 1000, -30.0)):
+        z = np.full((1, V), -np.inf)
+        z[0, V - k:] = c
+        r = oracle.logp_entropy(z, [V - 1])
+        assert r.flags == 0
+        assert r.token_entropy[0] == pytest.approx(math.log(k), abs=1e-12)
+        assert r.token_logp[0] == pytest.approx(-math.log(k), abs=1e-12)
+    z = np.array([[-np.inf, 1.0, -np.inf, 0.0, 0.0, -np.inf]])
+    Z = math.e + 2.0
+    H = -(math.e / Z * (1.0 - math.log(Z)) + 2.0 / Z * (-math.log(Z)))
+    r = oracle.logp_entropy(z, [1])
+    assert r.token_entropy[0] == pytest.approx(H, rel=1e-13)
+    assert r.token_logp[0] == pytest.approx(1.0 - math.log(Z), rel=1e-13)
+
+
 def test_two_logits_binary_entropy():
     # V = 2: H = h(sigmoid(z1 - z0)), h(q) = -q log q - (1 - q) log(1 - q)
     for d in (-6.0, -0.3, 0.0, 1.7, 9.0):
