@@ -392,6 +392,30 @@ def test_invalid_action_row_is_zero_and_flagged():
         assert r.token_contrib[t] == 0 and (r.dlogits[t] == 0).all()
 
 
+def test_masked_columns_equal_the_reduced_vocabulary():
+    # -inf logits carry zero probability: the loss, the log-probs and the dlogits of the other columns are those of
+    # the same rows with the masked columns deleted (actions re-indexed), and the masked columns' dlogits are 0
+    rng = np.random.default_rng(21)
+    T, V = 60, 300
+    z = rng.normal(0, 2, (T, V))
+    keep = np.sort(rng.choice(V, 180, replace=False))
+    actions = rng.choice(keep, T).astype(np.int32)
+    masked = z.copy()
+    masked[:, np.setdiff1d(np.arange(V), keep)] = -np.inf
+    seg = oracle.segments(T, np.array([0, 10, 25, 40, T], np.int32), np.array([0, 1, 2, 3, 4], np.int32))
+    A = np.array([1.0, -1.0, 0.5, -0.5])
+    behave = (rng.normal(-5, 1, T)).astype(np.float32)
+    full = oracle.loss_rows(masked, actions, behave, None, A, seg, 2, V=V, dual_clip_c=3.0)
+    remap = np.searchsorted(keep, actions).astype(np.int32)
+    red = oracle.loss_rows(np.ascontiguousarray(z[:, keep]), remap, behave, None, A, seg, 2, V=len(keep),
+                           dual_clip_c=3.0)
+    assert full.flags == 0 and red.flags == 0
+    assert full.loss == pytest.approx(red.loss, rel=1e-13)
+    np.testing.assert_allclose(full.token_logp, red.token_logp, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(full.dlogits[:, keep], red.dlogits, rtol=1e-12, atol=1e-16)
+    assert (full.dlogits[:, np.setdiff1d(np.arange(V), keep)] == 0).all()
+
+
 def test_malformed_offsets_make_loss_nan():
     rng = np.random.default_rng(15)
     bt = ragged_batch(rng, V=16)
