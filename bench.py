@@ -288,8 +288,61 @@ def time_logits(b: dict, norm: int, steps: int, warmup: int, dlogits=None) -> di
     return out
 
 
-def bench_logits_config(name: str, steps: int, warmup: int = 2, kernel: str = "", norms=None) -> dict:
-    """One of the other logits-path workloads, generated, timed under each normaliser, and freed."""
+def time_logits_graph(b: dict, norm: int, steps: int) -> dict:
+    """The same logits-path step (group advantages, then grpo_loss_fwd_bwd with dlogits) captured once into a HIP
+    graph and replayed: for launch-bound batches the launches, not the kernels, set the step time.  Every buffer is
+    allocated before the capture; the replays' loss is checked against an eager call's, bit for bit."""
+    import torch
+
+    import paper_2606_05597_amd as grpo
+    cfg, st = b["cfg"], b["structure"]
+    T, V = b["logits"].shape
+    N = len(st.rewards)
+    dev = b["logits"].device
+    sto = torch.from_numpy(st.step_tok_off).to(dev)
+    tso = torch.from_numpy(st.traj_step_off).to(dev)
+    adv = torch.empty(N, dtype=torch.float32, device=dev)
+    dl = torch.empty_like(b["logits"])
+    ws = torch.empty(grpo.grpo_loss_workspace_bytes(T, N), dtype=torch.uint8, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+
+    def step():
+        grpo.grpo_advantages(b["rewards"], cfg.G, out=adv)
+        grpo.grpo_loss_fwd_bwd(b["logits"], b["actions"], b["behave"], adv, sto, tso, cfg.G, V=b["V"], norm=norm,
+                               k=cfg.k, eps_low=0.2, eps_high=0.2, dual_clip_c=3.0, dlogits=dl, workspace=ws,
+                               loss_out=loss)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    eager = float(loss.item())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    loss.fill_(float("nan"))
+    for _ in range(3):
+        graph.replay()
+    torch.cuda.synchronize()
+    first = float(loss.item())
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    if not (first == eager and float(loss.item()) == eager):
+        raise RuntimeError(f"graph replay loss {first!r} / {float(loss.item())!r} differs from the eager {eager!r}")
+    del graph, dl, ws
+    return {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps, "loss": eager,
+            "note": "the same step captured once into a HIP graph and replayed (host clock around the replays)"}
+
+
+def bench_logits_config(name: str, steps: int, warmup: int = 2, kernel: str = "", norms=None,
+                        graph: bool = False) -> dict:
+    """One of the other logits-path workloads, generated, timed under each normaliser (and, with ``graph``, as a
+    captured HIP graph under the first), and freed."""
     import torch
 
     import paper_2606_05597_amd as grpo
@@ -309,6 +362,8 @@ def bench_logits_config(name: str, steps: int, warmup: int = 2, kernel: str = ""
                         f"normaliser {norms[0][0]} (k={cfg.k:g})")
     for label, _ in norms[1:]:
         head[f"normaliser {label}"] = res[label]
+    if graph:
+        head["graph_replay"] = time_logits_graph(b, norms[0][1], max(steps, 100))
     del b
     torch.cuda.empty_cache()
     return head
@@ -749,8 +804,9 @@ def main():
             norms=[("1/k", grpo.GRPO_NORM_CONST_K), ("1/|tau_i|", grpo.GRPO_NORM_TRAJ_STEPS)])
         tiny = bench_logits_config(
             "tiny", max(20, args.config_steps), kernel="k_rows_resident<fp32, 64, 4> (one workgroup per row)",
-            norms=[("1/k", grpo.GRPO_NORM_CONST_K), ("1/|tau_i|", grpo.GRPO_NORM_TRAJ_STEPS)])
-        tiny["note"] = "launch-bound: four small launches per step (advantages, segments, row pass, reduction)"
+            norms=[("1/k", grpo.GRPO_NORM_CONST_K), ("1/|tau_i|", grpo.GRPO_NORM_TRAJ_STEPS)], graph=True)
+        tiny["note"] = ("launch-bound: four small launches per step (advantages, segments, row pass, reduction); "
+                        "graph_replay: the same step as one captured HIP graph")
         out["tiny"] = tiny
     if args.fused_steps > 0:
         out["fused_lmhead"] = bench_fused(args.fused_steps, shard_steps=args.shard_steps and 3,
