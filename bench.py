@@ -800,7 +800,7 @@ def main():
     if args.config_steps > 0:
         out["long"] = bench_logits_config("long", args.config_steps, kernel=roof["kernel"])
         out["v32k"] = bench_logits_config(
-            "v32k", args.config_steps, kernel="k_rows_resident<bf16, 256, 16> (one workgroup per row)",
+            "v32k", args.config_steps, kernel="k_rows_resident<bf16, 1024, 4> (one workgroup per row)",
             norms=[("1/k", grpo.GRPO_NORM_CONST_K), ("1/|tau_i|", grpo.GRPO_NORM_TRAJ_STEPS)])
         tiny = bench_logits_config(
             "tiny", max(20, args.config_steps), kernel="k_rows_resident<fp32, 64, 4> (one workgroup per row)",
