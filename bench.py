@@ -21,7 +21,10 @@ The fused LM-head path is measured in the same run on its own workload
 "fused_lmhead" against the bf16 dense MFMA peak with the algorithmic work of
 three products (6 T H V flop): token blocks of 8192 rows with each block's D
 pass on a second stream (the line's value), the same on one stream, and
-vocabulary chunks of 8192 (four products executed) beside it.
+vocabulary chunks of 8192 (four products executed) beside it.  Under
+"library_gemm", the three products of one token block done by torch.matmul
+(hipBLASLt, no epilogue) in the same process: context for the MFMA kernels, as
+the copy ceiling is for the row pass.
 
 Prints one JSON line.  ``value`` is tokens/s of the whole step.  ``roofline``
 reports the dominant kernel (the row pass): algorithmic bytes per launch,
@@ -594,6 +597,46 @@ def bench_fused_logp(b: dict, steps: int, warmup: int = 1) -> dict:
                          "algorithmic_flop_per_launch": alg}}
 
 
+def library_gemm(b: dict, token_block: int, reps: int = 3) -> dict:
+    """Context for the fused line, as the copy ceiling is for the row pass: the three products of one token block
+    done by torch.matmul (hipBLASLt), bf16 in and out, no epilogue, operands laid out as the library's kernels read
+    them (both K-contiguous), and what the whole call's products would take at those rates."""
+    import torch
+
+    st = b["structure"]
+    T, H, V = st.T, b["H"], b["V"]
+    tb = min(token_block, T)
+    dev = b["hidden"].device
+    gen = torch.Generator(device=dev).manual_seed(7)
+    h = b["hidden"][:tb]
+    wt = b["W"].t().contiguous()                          # [V, H]
+    d = (torch.randn((tb, V), device=dev, generator=gen) * 1e-3).to(torch.bfloat16)
+    ht = h.t().contiguous()                               # [H, tb]
+    dt = d.t().contiguous()                               # [V, tb]
+    prods = {"forward z = h W": (lambda: torch.matmul(h, wt.t()), (tb, V, H)),
+             "dhidden = D W^T": (lambda: torch.matmul(d, b["W"].t()), (tb, H, V)),
+             "dW = h^T D": (lambda: torch.matmul(ht, dt.t()), (H, V, tb))}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    res, block_ms = {}, 0.0
+    for name, (fn, (m, n, k)) in prods.items():
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        block_ms += ms
+        res[name] = {"shape_mnk": [m, n, k], "ms": ms, "TFLOPs": 2.0 * m * n * k / (ms * 1e-3) / 1e12}
+    del wt, d, ht, dt
+    torch.cuda.empty_cache()
+    call_ms = block_ms * T / tb
+    return {"kernel": "torch.matmul (hipBLASLt), bf16 in and out, no epilogue", "token_block": tb,
+            "products": res, "block_ms": block_ms, "call_ms": call_ms,
+            "call_TFLOPs": 6.0 * T * H * V / (call_ms * 1e-3) / 1e12}
+
+
 FUSED_SCHEDULES = ("blocked", "blocked1", "chunked")
 
 
@@ -633,6 +676,9 @@ def bench_fused(steps: int, warmup: int = 1, shard_steps: int = 0, cpu: bool = F
              "chunked": "vocab_chunked"}
     for sch in schedules[1:]:
         out[names[sch]] = res[sch]
+    lib = library_gemm(b, token_block or 8192)
+    lib["frac_of_library_products"] = lib["call_ms"] / out["hot_ms"]
+    out["library_gemm"] = lib
     out["forward_only"] = bench_fused_logp(b, max(1, steps))
     if shard_steps > 0:
         out["vocab_shard"] = bench_fused_shard(b, adv, sto, tso, shard_steps, keep=True)

@@ -90,8 +90,11 @@ __device__ __forceinline__ void dma16(uint32_t lds_base, uint32_t voff, g_u32x4 
                : "memory", "m0");
 }
 
-__device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// The waits are builtins, not inline asm, so that the compiler's own wait insertion knows the counters have
+// drained: behind an opaque wait it assumed the last fragment reads before the barrier were still in flight, and
+// held the last MFMA group of every step back until the next slab's first reads had landed.
+__device__ __forceinline__ void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }  // lgkmcnt(0)
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <class C>
