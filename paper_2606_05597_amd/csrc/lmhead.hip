@@ -559,10 +559,19 @@ struct DwArgs {
   int c0, accumulate;
 };
 
-// One tile of the dW product: block bid of nblocks (a multiple of 8).
+// One tile of the dW product: block bid of nblocks (a multiple of 8).  The XCD-aware order walks N with 8
+// M-tiles at a time (the h^T panels shared along N) or, with N_MAJOR, walks M with 4 N-tiles at a time (the D^T
+// panels shared along M).  With K = a token block, h^T is small ([H, 8192]: 59 MB, held by the last-level cache)
+// and D^T is the whole vocabulary, so N_MAJOR reads D^T from HBM once instead of once per 8 of H's 14 tiles
+// (3-4% faster on the bare product, 0.3% on the whole blocked call); with K = the whole batch h^T is the large operand and the first order is kept.
+template <bool N_MAJOR>
 __device__ __forceinline__ void lm_dw_tile(const DwArgs& p, int bid, int nblocks, GemmSmem& sm) {
   int tm, tn;
-  if (!gemm_tile_of(bid, nblocks, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  if (N_MAJOR) {
+    if (!gemm_tile_of<4>(bid, nblocks, tiles_of(p.g.N), tiles_of(p.g.M), tn, tm)) return;
+  } else {
+    if (!gemm_tile_of(bid, nblocks, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
+  }
   const int m0 = tm * TILE, n0 = tn * TILE;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
@@ -608,7 +617,7 @@ struct DhDwArgs {
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_dw(const DhDwArgs p) {
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
   const int b = blockIdx.x;
-  if (b < p.dw_blocks) lm_dw_tile(p.dw, b, p.dw_blocks, sm);
+  if (b < p.dw_blocks) lm_dw_tile<false>(p.dw, b, p.dw_blocks, sm);
   else lm_dh_tile(p.dh, b - p.dw_blocks, (int)gridDim.x - p.dw_blocks, sm);
 }
 
@@ -625,7 +634,7 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_then_dw(const DhThenDwArgs 
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
   const int b = blockIdx.x;
   if (b < p.dh_blocks) lm_dh_tile(p.dh, b, p.dh_blocks, sm);
-  else lm_dw_tile(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
+  else lm_dw_tile<true>(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
 }
 
 // ---- token-blocked schedule: a block's stored fp32 logits -> D = g (softmax - onehot), bf16, as D and D^T ----
