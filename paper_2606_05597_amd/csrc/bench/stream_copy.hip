@@ -11,9 +11,15 @@
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <int NT, int U>
+// LDS_PAD > 0 reserves that many bytes of LDS per workgroup, so that (like the row kernel) only one workgroup fits a
+// CU; the pad is never read or written.
+template <int NT, int U, int LDS_PAD = 0>
 __global__ __launch_bounds__(NT) void k_stream_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
                                                      int64_t n) {
+  if constexpr (LDS_PAD > 0) {
+    __shared__ uint32_t pad[LDS_PAD / 4];
+    asm volatile("" ::"r"(pad));
+  }
   const int64_t stride = (int64_t)gridDim.x * NT * U;
   for (int64_t base = (int64_t)blockIdx.x * NT * U + threadIdx.x; base < n; base += stride) {
     u32x4 x[U];
@@ -32,17 +38,19 @@ __global__ __launch_bounds__(NT) void k_stream_copy(const u32x4* __restrict__ sr
 
 struct Variant {
   void (*k)(const u32x4*, u32x4*, int64_t);
-  int nt;
+  int nt, u;
   int wg_per_cu;  // workgroups per compute unit in the grid (0: one per NT*U vectors, as many as the copy needs)
   const char* name;
 };
 
 static const Variant kVariants[] = {
-    {k_stream_copy<256, 4>, 256, 0, "256 threads x 4 vectors, one workgroup per 16 KiB"},
-    {k_stream_copy<1024, 4>, 1024, 1, "1024 threads x 4 vectors, one workgroup per CU"},
-    {k_stream_copy<1024, 16>, 1024, 1, "1024 threads x 16 vectors, one workgroup per CU"},
-    {k_stream_copy<256, 16>, 256, 8, "256 threads x 16 vectors, 8 workgroups per CU"},
-    {k_stream_copy<256, 4>, 256, 4, "256 threads x 4 vectors, 4 workgroups per CU"},
+    {k_stream_copy<256, 4>, 256, 4, 0, "256 threads x 4 vectors, one workgroup per 16 KiB"},
+    {k_stream_copy<1024, 16, 100000>, 1024, 16, 0,
+     "1024 threads x 16 vectors, one workgroup per 256 KiB, one per CU at a time (LDS)"},
+    {k_stream_copy<1024, 4>, 1024, 4, 1, "1024 threads x 4 vectors, one workgroup per CU"},
+    {k_stream_copy<1024, 16>, 1024, 16, 1, "1024 threads x 16 vectors, one workgroup per CU"},
+    {k_stream_copy<256, 16>, 256, 16, 8, "256 threads x 16 vectors, 8 workgroups per CU"},
+    {k_stream_copy<256, 4>, 256, 4, 4, "256 threads x 4 vectors, 4 workgroups per CU"},
 };
 
 extern "C" int stream_copy_variants(void) { return (int)(sizeof(kVariants) / sizeof(kVariants[0])); }
@@ -60,7 +68,7 @@ extern "C" int stream_copy(int v, const void* src, void* dst, int64_t n_vec, hip
   const Variant& k = kVariants[v];
   int64_t grid;
   if (k.wg_per_cu == 0) {
-    const int64_t per_wg = (int64_t)k.nt * 4;
+    const int64_t per_wg = (int64_t)k.nt * k.u;
     grid = (n_vec + per_wg - 1) / per_wg;
     if (grid > (int64_t)1 << 30) grid = (int64_t)1 << 30;
   } else {
