@@ -517,9 +517,22 @@ __device__ __forceinline__ void lm_dh_tile(const DhArgs& p, int bid, int nblocks
   const int H = p.g.N;
   // the uniform choices (interior tile, first / last chunk) are template arguments, so
   // that the element loop has no branches
+  // Per 32-row block i: after the first chunk, the block's accumulator values are all loaded first and waited
+  // for once (element by element, every load would wait for the memory in turn).
   auto store = [&](auto full, auto first, auto last) {
 #pragma unroll
-    for (int i = 0; i < LmCfg::IB; ++i)
+    for (int i = 0; i < LmCfg::IB; ++i) {
+      float old[16][LmCfg::JB];
+      if (!first) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
+          const int64_t o = (int64_t)m * H + n0 + gemm_col<LmCfg>(wn, 0, lane);
+#pragma unroll
+          for (int j = 0; j < LmCfg::JB; ++j)
+            old[r][j] = (full || (m < p.g.M && n0 + gemm_col<LmCfg>(wn, j, lane) < H)) ? p.acc[o + 32 * j] : 0.f;
+        }
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
@@ -529,11 +542,12 @@ __device__ __forceinline__ void lm_dh_tile(const DhArgs& p, int bid, int nblocks
         for (int j = 0; j < LmCfg::JB; ++j) {
           if (!full && n0 + gemm_col<LmCfg>(wn, j, lane) >= H) continue;
           float v = acc[i][j][r];
-          if (!first) v += p.acc[o + 32 * j];
+          if (!first) v += old[r][j];
           if (last) p.dh[o + 32 * j] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
           else p.acc[o + 32 * j] = v;
         }
       }
+    }
   };
   typedef std::true_type Y;
   typedef std::false_type N;
@@ -577,9 +591,22 @@ __device__ __forceinline__ void lm_dw_tile(const DwArgs& p, int bid, int nblocks
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
   gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  // Per 32-row block i: with accumulate, all of its old values are loaded first and waited for once, then
+  // added and stored (element by element, every load would wait for the memory in turn).
   auto store = [&](auto full, auto accumulate) {
 #pragma unroll
-    for (int i = 0; i < LmCfg::IB; ++i)
+    for (int i = 0; i < LmCfg::IB; ++i) {
+      float old[16][LmCfg::JB];
+      if (accumulate) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
+          const float* o = p.dw + (int64_t)m * p.V + p.c0 + n0 + gemm_col<LmCfg>(wn, 0, lane);
+#pragma unroll
+          for (int j = 0; j < LmCfg::JB; ++j)
+            old[r][j] = (full || (m < p.g.M && n0 + gemm_col<LmCfg>(wn, j, lane) < p.g.N)) ? o[32 * j] : 0.f;
+        }
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + gemm_row<LmCfg>(wm, i, r, lane);
@@ -588,9 +615,10 @@ __device__ __forceinline__ void lm_dw_tile(const DwArgs& p, int bid, int nblocks
 #pragma unroll
         for (int j = 0; j < LmCfg::JB; ++j) {
           if (!full && n0 + gemm_col<LmCfg>(wn, j, lane) >= p.g.N) continue;
-          o[32 * j] = accumulate ? o[32 * j] + acc[i][j][r] : acc[i][j][r];
+          o[32 * j] = accumulate ? old[r][j] + acc[i][j][r] : acc[i][j][r];
         }
       }
+    }
   };
   typedef std::true_type Y;
   typedef std::false_type N;
