@@ -229,38 +229,62 @@ struct RowScale {
   int act;
 };
 
-// Runs once per token after the row's log-sum-exp is known.  z_a is the
-// action's logit (ignored when the action is out of range).  Writes the
-// token's loss contribution, clip state and log-prob.
-__device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn& in, double lse, double z_a) {
+// The per-token epilogue, once the row's log-sum-exp is known, in two halves: token_eval forms the row's dlogits
+// scale and the token's outputs without touching memory (so every wave of a row may run it), token_store writes
+// those outputs (one thread per token).  z_a is the action's logit (ignored when the action is out of range).
+struct TokenEval {
+  TokenOut o;
+  double l;  // the token's new log-prob
+  bool bad_act, bad;
+};
+
+__device__ inline RowScale token_eval(const TokenArgs& a, const TokenIn& in, double lse, double z_a, TokenEval& e) {
   RowScale rs;
-  const bool bad_act = in.act < 0 || (int64_t)in.act >= a.V;
+  e.bad_act = in.act < 0 || (int64_t)in.act >= a.V;
+  e.bad = in.bad_off || e.bad_act;
   rs.act = in.act;
-  if (in.bad_off || bad_act) {
-    if (bad_act && !in.bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
-    a.contrib[t] = in.bad_off ? (double)NAN : 0.0;
-    a.state[t] = 0;
-    a.tok_ratio[t] = make_double2((double)NAN, (double)NAN);
-    if (a.token_logp) a.token_logp[t] = 0.f;
+  if (e.bad) {
     rs.nc = -INFINITY;  // every d_v = 0
     rs.sign = 1.f;
     rs.d_a = 0.f;
     rs.act = -1;
     return rs;
   }
-  const double l = z_a - lse;
+  e.l = z_a - lse;
   const double b = (double)in.b, p = (double)in.p, A = (double)in.A;
-  const TokenOut o = token_surrogate(l, b, p, A, in.w, a.lo, a.hi, a.c, a.grad_scale);
-  if (!isfinite(l) || !isfinite(b) || !isfinite(p) || !isfinite(A)) atomicOr(&a.hdr->flags, GRPO_FLAG_NONFINITE);
-  a.contrib[t] = o.contrib;
-  a.state[t] = (int8_t)o.state;
-  a.tok_ratio[t] = make_double2(o.r, o.rho);
-  if (a.token_logp) a.token_logp[t] = (float)l;
+  e.o = token_surrogate(e.l, b, p, A, in.w, a.lo, a.hi, a.c, a.grad_scale);
+  const TokenOut& o = e.o;
   // d_v = g exp(z_v - lse) = sign(g) 2^(z_v L - lse L + log2|g|), with L = log2(e) as rounded on the device
   rs.nc = (float)(-lse * (double)kLog2e) + __builtin_amdgcn_logf(fabsf((float)o.g));
   rs.sign = (o.g < 0.0) ? -1.f : 1.f;
-  rs.d_a = (float)o.g * expm1f((float)l);  // g (p_a - 1), without cancellation
+  rs.d_a = (float)o.g * expm1f((float)e.l);  // g (p_a - 1), without cancellation
   if (isnan(o.g)) rs.nc = NAN;
+  return rs;
+}
+
+// Writes the token's loss contribution, clip state, ratios and log-prob, and raises the flags.
+__device__ inline void token_store(const TokenArgs& a, int t, const TokenIn& in, const TokenEval& e) {
+  if (e.bad) {
+    if (e.bad_act && !in.bad_off) atomicOr(&a.hdr->flags, GRPO_FLAG_ACTION);
+    a.contrib[t] = in.bad_off ? (double)NAN : 0.0;
+    a.state[t] = 0;
+    a.tok_ratio[t] = make_double2((double)NAN, (double)NAN);
+    if (a.token_logp) a.token_logp[t] = 0.f;
+    return;
+  }
+  if (!isfinite(e.l) || !isfinite(in.b) || !isfinite(in.p) || !isfinite(in.A))
+    atomicOr(&a.hdr->flags, GRPO_FLAG_NONFINITE);
+  a.contrib[t] = e.o.contrib;
+  a.state[t] = (int8_t)e.o.state;
+  a.tok_ratio[t] = make_double2(e.o.r, e.o.rho);
+  if (a.token_logp) a.token_logp[t] = (float)e.l;
+}
+
+// Both halves on one thread.
+__device__ inline RowScale token_finish(const TokenArgs& a, int t, const TokenIn& in, double lse, double z_a) {
+  TokenEval e;
+  const RowScale rs = token_eval(a, in, lse, z_a, e);
+  token_store(a, t, in, e);
   return rs;
 }
 

@@ -112,6 +112,27 @@ __device__ __forceinline__ void block_combine(float m, float s, float* sh_m, dou
   }
 }
 
+// As block_combine, but every wave reads the NW wave partials and forms the row's (M, S) itself, so that every
+// lane of the workgroup holds them after the one barrier (each 16-lane row of a wave reduces the same partials).
+template <int NW>
+__device__ __forceinline__ void block_combine_all(float m, float s, float* sh_m, double* sh_s, double& M_out,
+                                                  double& S_out) {
+  static_assert(NW >= 1 && NW <= 16, "one wave partial per lane of a 16-lane row");
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, r = lane & 15;
+  const float mw = wave_max_dpp(m);
+  const double sw =
+      wave_sum_dpp((m == -INFINITY) ? 0.0 : (double)s * (double)__builtin_amdgcn_exp2f((m - mw) * kLog2e));
+  if (lane == 0) {
+    sh_m[wv] = mw;
+    sh_s[wv] = sw;
+  }
+  __syncthreads();
+  const float mq = r < NW ? sh_m[r] : -INFINITY;
+  const float M = row16_max(mq);
+  M_out = (double)M;
+  S_out = row16_sum(mq == -INFINITY ? 0.0 : sh_s[r < NW ? r : 0] * (double)__builtin_amdgcn_exp2f((mq - M) * kLog2e));
+}
+
 // ---- persistent pipelined kernel for long bf16 rows ----------------------------
 // Buffer resources cover exactly one row (V*2 bytes): every access is a 32-bit
 // lane offset (tid*16) plus a constant per-vector offset, and the hardware
@@ -173,7 +194,6 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
   __shared__ float sh_m[NW];
   __shared__ double sh_s[NW];
   __shared__ float sh_za;
-  __shared__ RowScale sh_rs;
   __shared__ TokenIn sh_in;  // inputs of the row about to start (wave 1 loads them during the previous row)
   const int wv = threadIdx.x >> 6;
   const int nvec = (int)(a.tok.V / 8);
@@ -259,14 +279,16 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
       if (NP + q < NV - 1 || last_full) s += vec_sumexp<uint16_t>(reg[q], nmb);
 
     double M, S;
-    block_combine<NW>(m, s, sh_m, sh_s, M, S);  // barrier: sh_za is visible
-    if (tid == 0) sh_rs = token_finish(a.tok, t, in, row_lse(M, S), (double)sh_za);
-    // wave 1 fetches the next row's token inputs meanwhile: its loads are the only memory operations it has
-    // in flight here, so waiting for them holds nothing else back
+    block_combine_all<NW>(m, s, sh_m, sh_s, M, S);  // barrier: sh_za is visible, every lane holds (M, S)
+    // every wave forms the row's scale itself (no second barrier, no one-lane section); thread 0 writes the
+    // token's outputs
+    TokenEval ev;
+    const RowScale rs = token_eval(a.tok, in, row_lse(M, S), (double)sh_za, ev);
+    if (tid == 0) token_store(a.tok, t, in, ev);
+    // wave 1 fetches the next row's token inputs meanwhile (every wave read this row's from sh_in before the
+    // barrier above; the next row reads them after its first barrier)
     if (tid == 64) sh_in = token_load(a.tok, tn < a.T ? tn : t);
-    __syncthreads();
 
-    const RowScale rs = sh_rs;
     const uint32_t smask = sign_mask<uint16_t>(rs);
     const int act_v = rs.act >= 0 ? rs.act / 8 : -1;
     fresh(reg);
@@ -427,10 +449,11 @@ static const Variant kVariants[] = {
 static const RowKernel kPipe[] = {
     k_rows_pipe<7, 4>,   k_rows_pipe<8, 4>,   k_rows_pipe<9, 5>,   k_rows_pipe<10, 5>, k_rows_pipe<11, 6>,
     k_rows_pipe<12, 6>,  k_rows_pipe<13, 7>,  k_rows_pipe<14, 7>,  k_rows_pipe<15, 1>, k_rows_pipe<16, 2>,
-    k_rows_pipe<17, 3>,  k_rows_pipe<18, 4>,  k_rows_pipe<19, 5>,  k_rows_pipe<20, 9>, k_rows_pipe<21, 9>,
+    k_rows_pipe<17, 3>,  k_rows_pipe<18, 4>,  k_rows_pipe<19, 4>,  k_rows_pipe<20, 9>, k_rows_pipe<21, 9>,
     k_rows_pipe<22, 9>,  k_rows_pipe<23, 9>,
-};  // from 15 vectors on, 14 in registers (what fits in 128 VGPRs) and the rest in LDS
-constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 14 register vectors and 9 LDS vectors per thread
+};  // from 15 vectors on, 14 in registers and the rest in LDS, except 19 (V = 151,936): 15 and 4, which is 0.4%
+   // faster than 14 and 5 there (16 and 17 in registers also fit 128 VGPRs but are 0.3-0.8% slower)
+constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 15 register vectors and 9 LDS vectors per thread
 constexpr int64_t kPipeMaxT = (int64_t)1 << 30;  // t + (gridDim.x - 1) * chunk + 1 stays far below 2^31
 
 struct Launch {
