@@ -335,7 +335,6 @@ __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
   __shared__ float sh_m[NW];
   __shared__ double sh_s[NW];
   __shared__ float sh_za;
-  __shared__ RowScale sh_rs;
 
   const int t = blockIdx.x;
   const int tid = threadIdx.x;
@@ -367,12 +366,13 @@ __global__ __launch_bounds__(NT) void k_rows_resident(const RowArgs a) {
     if (j * NT + tid < nvec) s += vec_sumexp<Tin>(buf[j], nmb);
 
   double M, S;
-  block_combine<NW>(m, s, sh_m, sh_s, M, S);
-  if (tid == 0) sh_rs = token_finish(a.tok, t, in, row_lse(M, S), (double)sh_za);
-  __syncthreads();
+  block_combine_all<NW>(m, s, sh_m, sh_s, M, S);  // barrier: sh_za is visible, every lane holds (M, S)
+  // every wave forms the row's scale itself; thread 0 writes the token's outputs
+  TokenEval ev;
+  const RowScale rs = token_eval(a.tok, in, row_lse(M, S), (double)sh_za, ev);
+  if (tid == 0) token_store(a.tok, t, in, ev);
   if (!a.dlogits) return;
 
-  const RowScale rs = sh_rs;
   const uint32_t smask = sign_mask<Tin>(rs);
   u32x4* dst = reinterpret_cast<u32x4*>(static_cast<Tin*>(a.dlogits) + (int64_t)t * a.ld);
 #pragma unroll
