@@ -48,34 +48,47 @@ __device__ inline void shard_row_head(const ShardArgs& a, int t, RowScale& rs, i
 }
 
 // Rows of 16-byte vectors, one workgroup per row; U vectors per thread in flight.
+// The row's first U vectors per thread are loaded before the records are merged (the loads do not depend on
+// them), and every wave merges the records and forms the scale itself while they land: no barrier, no one-thread
+// section ahead of the loads.  Thread 0 alone writes the token's outputs.
 template <typename Tin, int NT, int U>
 __global__ __launch_bounds__(NT) void k_shard_rows_vec(const ShardArgs a) {
   constexpr int EPV = 16 / sizeof(Tin);
-  __shared__ RowScale sh_rs;
-  __shared__ int sh_act;
   const int t = blockIdx.x, tid = threadIdx.x;
-  if (tid == 0) {
-    RowScale rs;
-    int al;
-    shard_row_head(a, t, rs, al);
-    sh_rs = rs;
-    sh_act = al;
+  if (!a.dlogits) {  // forward only: the token's outputs, no row traffic
+    if (tid == 0) {
+      RowScale rs;
+      int al;
+      shard_row_head(a, t, rs, al);
+    }
+    return;
   }
-  __syncthreads();
-  if (!a.dlogits) return;
-  const RowScale rs = sh_rs;
-  const int act = sh_act;
-  const int act_vec = act >= 0 ? act / EPV : -1, act_lane = act >= 0 ? act % EPV : 0;
-  const uint32_t smask = sign_mask<Tin>(rs);
   const int nvec = (int)(a.V / EPV);
   const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const Tin*>(a.logits) + (int64_t)t * a.ld);
   u32x4* dst = reinterpret_cast<u32x4*>(static_cast<Tin*>(a.dlogits) + (int64_t)t * a.ld);
-  for (int base = tid; base < nvec; base += NT * U) {
-    u32x4 x[U];
+  u32x4 x[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int vi = base + u * NT;
-      if (vi < nvec) x[u] = __builtin_nontemporal_load(src + vi);
+  for (int u = 0; u < U; ++u) {
+    const int vi = tid + u * NT;
+    if (vi < nvec) x[u] = __builtin_nontemporal_load(src + vi);
+  }
+  double lse, za;
+  merge_vocab_stats(a.stats, a.n_shards, a.T, t, lse, za);
+  const TokenIn in = token_load(a.tok, t);
+  TokenEval ev;
+  const RowScale rs = token_eval(a.tok, in, lse, za, ev);
+  if (tid == 0) token_store(a.tok, t, in, ev);
+  const int64_t al = rs.act >= 0 ? (int64_t)rs.act - a.v_begin : -1;
+  const int act = (al >= 0 && al < a.V) ? (int)al : -1;  // the action's column in this shard, if it holds it
+  const int act_vec = act >= 0 ? act / EPV : -1, act_lane = act >= 0 ? act % EPV : 0;
+  const uint32_t smask = sign_mask<Tin>(rs);
+  for (int base = tid; base < nvec; base += NT * U) {
+    if (base != tid) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int vi = base + u * NT;
+        if (vi < nvec) x[u] = __builtin_nontemporal_load(src + vi);
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
