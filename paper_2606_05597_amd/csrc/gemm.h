@@ -80,13 +80,14 @@ __device__ __forceinline__ g_u32x4 buffer_rsrc(const void* base, uint32_t bytes)
 __device__ __forceinline__ int lds_swizzle(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
 // 16 bytes per lane from rsrc + voff into LDS at lds_base + 16 * lane (lds_base wave-uniform).  M0 carries the
-// LDS address; nothing else in these kernels uses it.
+// LDS address; nothing else in these kernels uses it.  One wait state separates the write of M0 from the LDS DMA
+// that reads it (the compiler inserts the same for its own LDS DMA; it cannot see inside this asm).
 __device__ __forceinline__ void dma16(uint32_t lds_base, uint32_t voff, g_u32x4 rsrc) {
   // the operands are wave-uniform; readfirstlane keeps them in SGPRs whatever the register allocator prefers
   lds_base = __builtin_amdgcn_readfirstlane(lds_base);
 #pragma unroll
   for (int k = 0; k < 4; ++k) rsrc[k] = __builtin_amdgcn_readfirstlane(rsrc[k]);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_base), "v"(voff), "s"(rsrc)
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(lds_base), "v"(voff), "s"(rsrc)
                : "memory", "m0");
 }
 

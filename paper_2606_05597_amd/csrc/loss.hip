@@ -147,13 +147,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int
 // 16 bytes per lane from the buffer (rsrc, voff + soff) into LDS at lds_base + 16 * lane, non-temporal.
 // Inline asm: the compiler's own handling of LDS DMA would hold every LDS read back until all LDS DMA in
 // flight has landed; the kernel orders them with explicit waits instead.  M0 carries the LDS address;
-// nothing else in this kernel uses it.
+// nothing else in this kernel uses it.  An LDS DMA must not follow the write of M0 directly: one wait state
+// between them (the compiler inserts the same for its own LDS DMA; it cannot see inside this asm).
 __device__ __forceinline__ void dma16_nt(uint32_t lds_base, uint32_t voff, uint32_t soff, u32x4 rsrc) {
   lds_base = __builtin_amdgcn_readfirstlane(lds_base);
   soff = __builtin_amdgcn_readfirstlane(soff);
 #pragma unroll
   for (int k = 0; k < 4; ++k) rsrc[k] = __builtin_amdgcn_readfirstlane(rsrc[k]);
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds" ::"s"(lds_base), "v"(voff), "s"(rsrc),
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds" ::"s"(lds_base), "v"(voff), "s"(rsrc),
                "s"(soff)
                : "memory", "m0");
 }
