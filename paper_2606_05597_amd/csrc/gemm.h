@@ -74,6 +74,10 @@ __device__ __forceinline__ g_u32x4 buffer_rsrc(const void* base, uint32_t bytes)
   return r;
 }
 
+// Byte offset of a load that must read zeros: past the range of every descriptor here (a tile's 256 rows of at
+// most 2^23 - 256 elements end at or below 2^32 - 2^17 bytes), with room for the load's 16 bytes below 2^32.
+constexpr uint32_t kOobOffset = 0xFFFF0000u;
+
 // LDS slot permutation of a slab row (eight 16-byte slots per 128-byte row).  A fragment read takes
 // one slot from each of 32 consecutive rows; the LDS serves 16 lanes (256 bytes) at a time, so every 16
 // consecutive rows must spread over the 8 slots x 2 row parities, and every 8 over the 8 slots.
@@ -119,14 +123,14 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, int m0, int n0,
       const int row = (q * C::NW + wave) * 8 + lrow, kv = (lane & 7) ^ lds_swizzle(row);
       const bool kin = k0 + kv * 8 < g.K;  // vectors past K read as zero
       dma16(la + (uint32_t)(q * C::NW * 8 * C::BK) * 2u,
-            kin ? (uint32_t)(row * g.lda + k0 + kv * 8) * 2u : 0x80000000u, ra);
+            kin ? (uint32_t)(row * g.lda + k0 + kv * 8) * 2u : kOobOffset, ra);
     }
 #pragma unroll
     for (int q = 0; q < C::QB; ++q) {
       const int row = (q * C::NW + wave) * 8 + lrow, kv = (lane & 7) ^ lds_swizzle(row);
       const bool kin = k0 + kv * 8 < g.K;
       dma16(lb + (uint32_t)(q * C::NW * 8 * C::BK) * 2u,
-            kin ? (uint32_t)(row * g.ldb + k0 + kv * 8) * 2u : 0x80000000u, rb);
+            kin ? (uint32_t)(row * g.ldb + k0 + kv * 8) * 2u : kOobOffset, rb);
     }
   };
 #pragma unroll
@@ -187,6 +191,169 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs& g, int m0, int n0,
     if (kt + 1 < nk) read(0, buf ^ 1, 0);
     mma(1);
   }
+}
+
+
+// ---- the same core with B's fragments loaded from memory straight into registers ------------------------------
+// B in the fragment-packed layout: for every 32 rows of B (n-block nb) and every 16 columns of K (k-block kb) one
+// 1 KB chunk, the 32 x 16 operand of one MFMA as its 64 lanes read it: lane l's 16 bytes are
+// B[32 nb + l % 32][16 kb + 8 (l / 32) .. + 7].  Chunk (nb, kb) sits at ((nb * kb_count) + kb) KB, kb_count =
+// 16-column blocks of K rounded up to whole 64-deep slabs, and rows past N and columns past K hold zeros.  A wave
+// then fetches each of its B fragments with one fully coalesced 16-byte-per-lane load, one slab ahead, so the LDS
+// carries only A (a third of the LDS traffic of the LDS-staged core goes away: A's slab writes and fragment reads
+// stay, B's go).
+__host__ __device__ constexpr int64_t packed_kb_count(int64_t K) { return (K + 63) / 64 * 4; }
+__host__ __device__ constexpr int64_t packed_bytes(int64_t N, int64_t K) {
+  return (N + 31) / 32 * packed_kb_count(K) * 1024;
+}
+
+// vmcnt(N) with the other counters left alone
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// One B fragment: 16 bytes per lane from rsrc + voff into v.  Inline asm, so that the compiler leaves the wait to
+// the explicit vmcnt below (it cannot count the LDS DMA, which is asm too, and would wait for the wrong load); the
+// register is an in-out operand so that the load writes the register the MFMAs read, with no copy in between.
+__device__ __forceinline__ void frag_load(g_bf16x8& v, uint32_t voff, g_u32x4 rsrc) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) rsrc[k] = __builtin_amdgcn_readfirstlane(rsrc[k]);
+  asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen" : "+v"(v) : "v"(voff), "s"(rsrc) : "memory");
+}
+
+// C[m, n] = sum_k A[m, k] B[n, k] with g.A as in gemm_mainloop and g.B the packed B of an N x K matrix (g.ldb
+// unused).  Same tile, waves, accumulator layout and order of the K sum as gemm_mainloop, so the accumulators are
+// bit-identical to its.  LDS: two A slabs, C::BM * C::BK * 2 elements.
+template <class C>
+__device__ __forceinline__ void gemm_mainloop_packed(const GemmArgs& g, int m0, int n0,
+                                                     g_f32x16 (&acc)[C::IB][C::JB], uint16_t* lds) {
+  constexpr int STA = C::BM * C::BK;  // elements per A slab buffer
+  static_assert(C::WTN % 32 == 0 && C::BN % 32 == 0, "whole n-blocks per wave and tile");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
+  const int rows_a = min(C::BM, g.M - m0);
+  const g_u32x4 ra = buffer_rsrc(g.A + (int64_t)m0 * g.lda, (uint32_t)(((int64_t)(rows_a - 1) * g.lda + g.K) * 2));
+  // the tile's n-blocks: its own descriptor, so that n-blocks past N and loads past the last slab of the last
+  // n-block read as zero
+  const int64_t kbc = packed_kb_count(g.K);
+  const int nb_tile = (int)min((int64_t)C::BN / 32, ((int64_t)g.N + 31) / 32 - n0 / 32);
+  const g_u32x4 rbp = buffer_rsrc(reinterpret_cast<const char*>(g.B) + (int64_t)(n0 / 32) * kbc * 1024,
+                                  (uint32_t)(nb_tile * kbc * 1024));
+  const int lrow = lane >> 3;
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)lds);
+  auto issue = [&](int buf, int k0) {
+    const uint32_t la = lds0 + (uint32_t)(buf * STA + wave * 8 * C::BK) * 2u;
+#pragma unroll
+    for (int q = 0; q < C::QA; ++q) {
+      const int row = (q * C::NW + wave) * 8 + lrow, kv = (lane & 7) ^ lds_swizzle(row);
+      const bool kin = k0 + kv * 8 < g.K;
+      dma16(la + (uint32_t)(q * C::NW * 8 * C::BK) * 2u,
+            kin ? (uint32_t)(row * g.lda + k0 + kv * 8) * 2u : kOobOffset, ra);
+    }
+  };
+  uint32_t boff[C::JB];
+#pragma unroll
+  for (int j = 0; j < C::JB; ++j) boff[j] = (uint32_t)((wn * C::WTN / 32 + j) * kbc * 1024) + lane * 16u;
+  g_bf16x8 fb[4][C::JB];  // B fragments of one slab: k-substep, n-block
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int j = 0; j < C::JB; ++j) fb[s][j] = g_bf16x8{};
+  auto bload = [&](int s, int kt) {
+#pragma unroll
+    for (int j = 0; j < C::JB; ++j) frag_load(fb[s][j], boff[j] + (uint32_t)(4 * kt + s) * 1024u, rbp);
+  };
+#pragma unroll
+  for (int i = 0; i < C::IB; ++i)
+#pragma unroll
+    for (int j = 0; j < C::JB; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int fr = lane & 31, hi = lane >> 5;
+  const int arow = (wm * C::WTM + fr) * C::BK;
+  int sw[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) sw[ks] = ((2 * ks + hi) ^ lds_swizzle(fr)) * 8;
+  g_bf16x8 fa[2][C::IB];
+  auto read = [&](int f, int buf, int ks) {
+    const uint16_t* s = lds + buf * STA;
+#pragma unroll
+    for (int i = 0; i < C::IB; ++i) fa[f][i] = *reinterpret_cast<const g_bf16x8*>(s + arow + i * 32 * C::BK + sw[ks]);
+  };
+  // the MFMAs of k-substep s with the A reads of the next substep interleaved (one read, one MFMA)
+  auto mma = [&](int f, int s) {
+#pragma unroll
+    for (int i = 0; i < C::IB; ++i)
+#pragma unroll
+      for (int j = 0; j < C::JB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[f][i], fb[s][j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int x = 0; x < C::IB; ++x) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, C::IB * C::JB - C::IB, 0);
+  };
+  // Per wave and slab kt the vector-memory queue gets, oldest first: B(kt+1, s) for s = 0, 1, 2, each after the
+  // MFMAs of substep s (which were the last readers of those registers), the A DMA of slab kt+2 after the
+  // barrier, B(kt+1, 3) after substep 3.  Counters drain in order, so substep s of slab kt, which needs B(kt, s),
+  // leaves WB younger operations in flight, and the barrier, which needs this wave's DMA of slab kt+1, WD.  Loads
+  // past the last slab are issued as well (they read zeros or values nobody uses) so that the counts are the same
+  // on every slab; the sched_barriers keep the compiler from moving MFMAs above a wait it cannot see the reason for.
+  constexpr int WB = 3 * C::JB + C::QA, WD = 4 * C::JB;
+  const int nk = (g.K + C::BK - 1) / C::BK;
+  issue(0, 0);
+  issue(1, C::BK);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) bload(s, 0);
+  wait_vm0();
+  wait_lgkm0();  // also publishes what the caller stored to LDS before the mainloop
+  barrier();
+  read(0, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    wait_vm<WB>();
+    __builtin_amdgcn_sched_barrier(0);
+    read(1, buf, 1);
+    mma(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    bload(0, kt + 1);
+    wait_vm<WB>();
+    __builtin_amdgcn_sched_barrier(0);
+    read(0, buf, 2);
+    mma(1, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    bload(1, kt + 1);
+    wait_vm<WB>();
+    __builtin_amdgcn_sched_barrier(0);
+    read(1, buf, 3);
+    mma(0, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    bload(2, kt + 1);
+    wait_lgkm0();  // this wave's reads of slab kt are done
+    wait_vm<WD>();  // this wave's DMA of slab kt + 1 has landed
+    barrier();      // ... and every wave's
+    issue(buf, (kt + 2) * C::BK);
+    wait_vm<WB>();
+    __builtin_amdgcn_sched_barrier(0);
+    read(0, buf ^ 1, 0);
+    mma(1, 3);
+    __builtin_amdgcn_sched_barrier(0);
+    bload(3, kt + 1);
+  }
+  // The last slab's loads of the next one are still in flight.  The compiler cannot see them (asm), so the wait
+  // names every fragment register: they stay allocated until the data has landed, and nothing of the caller's
+  // can be given a register that a late load would then overwrite.  The barrier then keeps any wave from reusing
+  // the LDS before every wave's last (zero) DMA has landed in it.
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int j = 0; j < C::JB; ++j) asm volatile("s_waitcnt vmcnt(0)" : "+v"(fb[s][j])::"memory");
+  barrier();
 }
 
 }  // namespace grpo

@@ -87,7 +87,9 @@ template <bool ENT>
 __device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x16 (&acc)[LmCfg::IB][LmCfg::JB],
                                                     int m0, int n0, int tn, GemmSmem& sm);
 
-template <bool STORE_Z>
+// PACKED: B is W^T in the fragment-packed layout (gemm_mainloop_packed); the accumulators, and so every output,
+// are bit-identical to the LDS-staged core's.
+template <bool STORE_Z, bool PACKED = false>
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
   int tm, tn;
@@ -96,7 +98,8 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  if constexpr (PACKED) gemm_mainloop_packed<LmCfg>(p.g, m0, n0, acc, sm.s);
+  else gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
   if constexpr (STORE_Z) {
     // Rows and columns past M and N hold zeros (their operand rows read as zero).  Accumulators 4g..4g+3 of a
     // lane are four consecutive rows of one column; a 4 x 4 transpose within each quad of lanes (two DPP
@@ -233,7 +236,7 @@ struct CombineArgs {
   TokenArgs tok;
   const float2* part;
   const uint16_t* h;   // [T, H]
-  const uint16_t* WT;  // [V, H]
+  const uint16_t* WT;  // [V, H], or with PACKED W^T in the fragment-packed layout
   RowScale* rs;        // [Tp]; rows >= T get the zero scale
   int T, H, n_tiles;
   int t0;              // row of blockIdx.x 0; part holds rows from t0 on
@@ -246,6 +249,16 @@ struct RowStatsSmem {
   float m[4];
   double s[4], z[4];
 };
+// Elements 8 q .. 8 q + 7 of row `row` of a matrix with K = H columns: 16 contiguous bytes in either layout.
+template <bool PACKED>
+__device__ __forceinline__ const uint16_t* row_piece(const uint16_t* B, int64_t row, int q, int H) {
+  if constexpr (PACKED)  // chunk (row / 32, q / 2), lane 32 (q % 2) + row % 32
+    return B + ((row >> 5) * packed_kb_count(H) + (q >> 1)) * 512 + ((q & 1) * 32 + (row & 31)) * 8;
+  else
+    return B + row * H + 8 * q;
+}
+
+template <bool PACKED = false>
 __device__ inline void lm_row_stats(const float2* pr, int n_tiles, const uint16_t* hr, const uint16_t* WT, int act,
                                     int H, RowStatsSmem& sh, float& M_out, double& S_out, double& z_out) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -254,10 +267,9 @@ __device__ inline void lm_row_stats(const float2* pr, int n_tiles, const uint16_
   m = wave_max(m);
   double z = 0.0;
   if (act >= 0) {
-    const uint16_t* wr = WT + (int64_t)act * H;
     for (int k = tid * 8; k < H; k += 256 * 8) {
       const u32x4 x = *reinterpret_cast<const u32x4*>(hr + k);
-      const u32x4 y = *reinterpret_cast<const u32x4*>(wr + k);
+      const u32x4 y = *reinterpret_cast<const u32x4*>(row_piece<PACKED>(WT, act, k / 8, H));
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         z += (double)bf16_lo(x[q]) * (double)bf16_lo(y[q]);
@@ -286,6 +298,7 @@ __device__ inline void lm_row_stats(const float2* pr, int n_tiles, const uint16_
   z_out = sh.z[0] + sh.z[1] + sh.z[2] + sh.z[3];
 }
 
+template <bool PACKED = false>
 __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   __shared__ RowStatsSmem sh;
   const int t = a.t0 + (int)blockIdx.x, tid = threadIdx.x;
@@ -297,8 +310,8 @@ __global__ __launch_bounds__(256) void k_lm_combine(const CombineArgs a) {
   const bool ok = act >= 0 && (int64_t)act < a.tok.V;
   float M;
   double S, za;
-  lm_row_stats(a.part + (int64_t)(t - a.t0) * a.n_tiles, a.n_tiles, a.h + (int64_t)t * a.H, a.WT, ok ? act : -1, a.H,
-               sh, M, S, za);
+  lm_row_stats<PACKED>(a.part + (int64_t)(t - a.t0) * a.n_tiles, a.n_tiles, a.h + (int64_t)t * a.H, a.WT,
+                       ok ? act : -1, a.H, sh, M, S, za);
   if (tid == 0) {
     const TokenIn in = token_load(a.tok, t);
     a.rs[t] = token_finish(a.tok, t, in, row_lse((double)M, S), za);
@@ -500,12 +513,14 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dlogits(const DlogitsArgs p) {
 // ---- pass 2b: dhidden += D_c W_c^T --------------------------------------------------
 struct DhArgs {
   GemmArgs g;        // A = the pair buffer (M = T, K = the pair's width), B = W[:, pair] as [H, K], ldb = V
+                     // (with PACKED: W packed as an H x V matrix)
   float* acc;        // [Tp, H] fp32 accumulator (unused with a single chunk)
   uint16_t* dh;      // [T, H] bf16 output
   int first, last;
 };
 
 // One tile of the dhidden product: block bid of nblocks (a multiple of 8, for the XCD order).
+template <bool PACKED = false>
 __device__ __forceinline__ void lm_dh_tile(const DhArgs& p, int bid, int nblocks, GemmSmem& sm) {
   int tm, tn;
   if (!gemm_tile_of(bid, nblocks, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
@@ -513,7 +528,8 @@ __device__ __forceinline__ void lm_dh_tile(const DhArgs& p, int bid, int nblocks
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  if constexpr (PACKED) gemm_mainloop_packed<LmCfg>(p.g, m0, n0, acc, sm.s);
+  else gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
   const int H = p.g.N;
   // the uniform choices (interior tile, first / last chunk) are template arguments, so
   // that the element loop has no branches
@@ -567,7 +583,7 @@ __device__ __forceinline__ void lm_dh_tile(const DhArgs& p, int bid, int nblocks
 
 // ---- pass 2c: dW[:, chunks] = h^T D -------------------------------------------------
 struct DwArgs {
-  GemmArgs g;     // A = h^T [H, Tp], B = D^T of the pair [width, Tp], K = Tp
+  GemmArgs g;     // A = h^T [H, Tp], B = D^T of the pair [width, Tp], K = Tp (with PACKED: D^T packed)
   float* dw;      // [H, V]
   int64_t V;
   int c0, accumulate;
@@ -578,7 +594,7 @@ struct DwArgs {
 // panels shared along M).  With K = a token block, h^T is small ([H, 8192]: 59 MB, held by the last-level cache)
 // and D^T is the whole vocabulary, so N_MAJOR reads D^T from HBM once instead of once per 8 of H's 14 tiles
 // (3-4% faster on the bare product, 0.3% on the whole blocked call); with K = the whole batch h^T is the large operand and the first order is kept.
-template <bool N_MAJOR>
+template <bool N_MAJOR, bool PACKED = false>
 __device__ __forceinline__ void lm_dw_tile(const DwArgs& p, int bid, int nblocks, GemmSmem& sm) {
   int tm, tn;
   if (N_MAJOR) {
@@ -590,7 +606,8 @@ __device__ __forceinline__ void lm_dw_tile(const DwArgs& p, int bid, int nblocks
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
-  gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
+  if constexpr (PACKED) gemm_mainloop_packed<LmCfg>(p.g, m0, n0, acc, sm.s);
+  else gemm_mainloop<LmCfg>(p.g, m0, n0, acc, sm.s);
   // Per 32-row block i: with accumulate, all of its old values are loaded first and waited for once, then
   // added and stored (element by element, every load would wait for the memory in turn).
   auto store = [&](auto full, auto accumulate) {
@@ -651,7 +668,8 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_dw(const DhDwArgs p) {
 
 // The token-blocked schedule's backward launch: the dhidden tiles (K = the whole vocabulary) first, then the dW
 // tiles (K = the block's rows).  A dhidden tile is then the longest unit by far; dispatched first, the long tiles
-// spread over the CUs and the many short dW tiles fill the time the last of them leave.
+// spread over the CUs and the many short dW tiles fill the time the last of them leave.  Both B operands (W and
+// D^T) come in the fragment-packed layout.
 struct DhThenDwArgs {
   DhArgs dh;
   DwArgs dw;
@@ -661,8 +679,8 @@ struct DhThenDwArgs {
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_then_dw(const DhThenDwArgs p) {
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
   const int b = blockIdx.x;
-  if (b < p.dh_blocks) lm_dh_tile(p.dh, b, p.dh_blocks, sm);
-  else lm_dw_tile<true>(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
+  if (b < p.dh_blocks) lm_dh_tile<true>(p.dh, b, p.dh_blocks, sm);
+  else lm_dw_tile<true, true>(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
 }
 
 // ---- token-blocked schedule: a block's stored fp32 logits -> D = g (softmax - onehot), bf16, as D and D^T ----
@@ -670,9 +688,10 @@ struct BlockDArgs {
   const float* z;      // [rows, ld] the block's logits
   const RowScale* rs;  // [rows] the block's row scales
   uint16_t* D;         // [rows, ld]
-  uint16_t* DT;        // [ld, rows]
+  uint16_t* DT;        // [ld, rows], or with packed_dt D^T in the fragment-packed layout (N = ld, K = rows)
   int64_t ld;          // a multiple of 64; columns V..ld get D = 0
   int V, rows;         // rows: a multiple of 64
+  int packed_dt;
 };
 constexpr int kBlockDStrip = 512;  // columns per work item: eight 64 x 64 tiles
 constexpr int64_t kBlockDMaxGrid = 1 << 20;  // workgroups per launch at most; they loop over the rest
@@ -690,7 +709,8 @@ static unsigned block_d_grid(int64_t rows, int64_t ld, int grid) {
 // 2 x 4 pieces (rows 2p, 2p + 1 of four columns, p = tid / 16 and p + 16): two 16-byte logit loads each; the D
 // rows go out as 8-byte stores (16 lanes fill a 128-byte line); for D^T every column's row pair is packed into
 // one 32-bit LDS word (stride 33 words per column), read back as four words = eight rows, and stored 16 bytes
-// at a time (8 lanes per 128-byte column piece).  Two LDS buffers, one barrier per tile.
+// at a time (8 lanes per 128-byte column piece, or with packed_dt one packed lane's 16 bytes, 8 lanes of
+// consecutive columns side by side).  Two LDS buffers, one barrier per tile.
 __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
   constexpr int kLdw = 33;
   __shared__ uint32_t tu[2][64 * kLdw];
@@ -705,9 +725,6 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
     if (tid < 64) srs[tid] = a.rs[r0 + tid];
     __syncthreads();
     const int cq = tid & 15, rp = tid >> 4;
-    RowScale rs[4];  // rows 2 rp, 2 rp + 1, 2 rp + 32, 2 rp + 33
-#pragma unroll
-    for (int k = 0; k < 4; ++k) rs[k] = srs[2 * rp + (k & 1) + 32 * (k >> 1)];
     const int ntiles = (int)min((int64_t)(kBlockDStrip / 64), (a.ld - cs) / 64);
     for (int it = 0; it < ntiles; ++it) {
       const int64_t c = cs + it * 64 + 4 * cq;
@@ -718,12 +735,15 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
         const float* zr = a.z + (int64_t)(r0 + row) * a.ld + c;
         const f32x4 x0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr));
         const f32x4 x1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + a.ld));
+        // the row scales are read from LDS where they are used (per element; the reads are merged): kept in
+        // registers they take the pass past the 80 VGPRs that fit beside a forward-product workgroup (2 x 216 of
+        // a SIMD's 512)
         float d0[4], d1[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int64_t v = c + e;
-          const RowScale& s0 = rs[2 * u];
-          const RowScale& s1 = rs[2 * u + 1];
+          const RowScale& s0 = srs[row];
+          const RowScale& s1 = srs[row + 1];
           d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : s0.sign * __builtin_amdgcn_exp2f(fmaf(x0[e], kLog2e, s0.nc));
           d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : s1.sign * __builtin_amdgcn_exp2f(fmaf(x1[e], kLog2e, s1.nc));
         }
@@ -744,7 +764,11 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
         const int col = (tid >> 3) + 32 * q, rc = tid & 7;
         const uint32_t* src = t + col * kLdw + 4 * rc;
         const u32x4 v = {src[0], src[1], src[2], src[3]};
-        *reinterpret_cast<u32x4*>(a.DT + (cs + it * 64 + col) * a.rows + r0 + 8 * rc) = v;
+        const int64_t vc = cs + it * 64 + col;
+        const int t8 = (r0 >> 3) + rc;  // rows 8 t8 .. 8 t8 + 7 of column vc: one packed lane's 16 bytes
+        uint16_t* dst = a.packed_dt ? a.DT + ((vc >> 5) * (a.rows >> 4) + (t8 >> 1)) * 512 + ((t8 & 1) * 32 + (vc & 31)) * 8
+                                    : a.DT + vc * a.rows + 8 * t8;
+        *reinterpret_cast<u32x4*>(dst) = v;
       }
     }
   }
@@ -778,6 +802,58 @@ __global__ __launch_bounds__(256) void k_transpose_bf16(const uint16_t* __restri
       v[e] = (uint32_t)tile[tx * 8 + 2 * e][cc] | ((uint32_t)tile[tx * 8 + 2 * e + 1][cc] << 16);
     *reinterpret_cast<u32x4*>(dst + (int64_t)c * ldd + r) = v;
   }
+}
+
+// ---- fragment-packed operands (gemm_mainloop_packed) -----------------------------------
+// dst = src^T packed: src [R, Cc] (row stride lds_), its transpose an Cc x R matrix (N = Cc, K = R).  One 64 x 64
+// tile of src per workgroup, staged in LDS as in k_transpose_bf16; it makes the chunks of n-blocks c0 / 32 and
+// c0 / 32 + 1 (those that exist) and k-blocks r0 / 16 .. + 3, each lane's 16 bytes taken down a column of the
+// tile.  Rows past R give zeros.
+__global__ __launch_bounds__(256) void k_pack_t(const uint16_t* __restrict__ src, int64_t lds_, int R, int Cc,
+                                                uint16_t* __restrict__ dst) {
+  __shared__ uint16_t tile[64][64 + 2];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int tid = threadIdx.x, ty = tid >> 3, tx = tid & 7;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int rr = ty + 32 * q, r = r0 + rr, c = c0 + tx * 8;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < R && c < Cc) v = *reinterpret_cast<const u32x4*>(src + (int64_t)r * lds_ + c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tile[rr][tx * 8 + 2 * e] = (uint16_t)(v[e] & 0xffffu);
+      tile[rr][tx * 8 + 2 * e + 1] = (uint16_t)(v[e] >> 16);
+    }
+  }
+  __syncthreads();
+  const int64_t kbc = packed_kb_count(R), n_nb = ((int64_t)Cc + 31) / 32;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int piece = tid + 256 * q, chunk = piece >> 6, l = piece & 63;  // chunk = 4 n-block + k-block
+    const int64_t nb = c0 / 32 + (chunk >> 2);
+    if (nb >= n_nb) continue;
+    const int cc = 32 * (chunk >> 2) + (l & 31), rr = 16 * (chunk & 3) + 8 * (l >> 5);
+    u32x4 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = (uint32_t)tile[rr + 2 * e][cc] | ((uint32_t)tile[rr + 2 * e + 1][cc] << 16);
+    *reinterpret_cast<u32x4*>(dst + (nb * kbc + r0 / 16 + (chunk & 3)) * 512 + l * 8) = v;
+  }
+}
+
+// dst = src packed: src [R, Cc] (row stride lds_, Cc a multiple of 8) as an R x Cc matrix (N = R, K = Cc).  A
+// workgroup makes the four chunks of n-block blockIdx.y and k-blocks 4 blockIdx.x .. + 3: each lane copies 16
+// bytes of one row, and the workgroup reads 128 contiguous bytes of each of its 32 rows.  Columns past Cc and rows
+// past R give zeros.
+__global__ __launch_bounds__(256) void k_pack_rows(const uint16_t* __restrict__ src, int64_t lds_, int R, int Cc,
+                                                   uint16_t* __restrict__ dst) {
+  const int64_t kbc = packed_kb_count(Cc), nb = blockIdx.y;
+  const int tid = threadIdx.x, kb = 4 * (int)blockIdx.x + (tid >> 6), l = tid & 63;
+  const int64_t row = nb * 32 + (l & 31);
+  const int col = kb * 16 + 8 * (l >> 5);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (row < R && col < Cc) v = *reinterpret_cast<const u32x4*>(src + row * lds_ + col);
+  *reinterpret_cast<u32x4*>(dst + (nb * kbc + kb) * 512 + l * 8) = v;
 }
 
 __global__ void k_fill_f32(float* p, int64_t n, float v) {
@@ -893,11 +969,12 @@ static void lm_pass2(const Pass2& q, hipStream_t s) {
   }
 }
 
-// The token-blocked schedule's workspace: the fp32 logits of two blocks (the next block's forward product runs
-// while the D pass reads the previous block's when a second stream is given), the D and D^T of one block.
+// The token-blocked schedule's workspace: W^T and W in the fragment-packed layout (the B operands of the forward
+// and dhidden products), h^T, the fp32 logits of two blocks (the next block's forward product runs while the D
+// pass reads the previous block's when a second stream is given), the D and the packed D^T of one block.
 struct LmBlockWs {
   LossWs loss;
-  size_t wt, ht, part, rs, z, d, dt, total;
+  size_t wt, wp, ht, part, rs, z, d, dt, total;
   int64_t Tp, Tbp, ldz;
   int n_tiles;
 };
@@ -909,13 +986,14 @@ static LmBlockWs lm_block_ws_layout(int64_t T, int64_t H, int64_t V, int32_t Tb,
   l.n_tiles = (int)((V + TILE - 1) / TILE);
   l.ldz = (int64_t)l.n_tiles * TILE;
   size_t o = l.loss.total;
-  l.wt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(V * H));
+  l.wt = o;   o = align_up(o + (size_t)packed_bytes(V, H));
+  l.wp = o;   o = align_up(o + (size_t)packed_bytes(H, V));
   l.ht = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(H * l.Tp));
   l.part = o; o = align_up(o + sizeof(float2) * (size_t)(l.Tbp * l.n_tiles));
   l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
   l.z = o;    o = align_up(o + sizeof(float) * (size_t)(l.Tbp * l.ldz) * (l.Tp > l.Tbp ? 2 : 1));
   l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tbp * l.ldz));
-  l.dt = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(l.ldz * l.Tbp));
+  l.dt = o;   o = align_up(o + (size_t)packed_bytes(l.ldz, l.Tbp));
   l.total = o;
   return l;
 }
@@ -1010,7 +1088,7 @@ extern "C" int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T
   ca.H = (int)H;
   ca.n_tiles = L.n_tiles;
   ca.t0 = 0;
-  hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)Tp), dim3(256), 0, s, ca);
+  hipLaunchKernelGGL(k_lm_combine<false>, dim3((unsigned)Tp), dim3(256), 0, s, ca);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   lm_pass2(Pass2{h16, W16, WT, hT, rs, D, DT, acc, static_cast<uint16_t*>(dhidden), dw_lm, T, H, V, Tp,
                  vocab_chunk, accumulate_dw},
@@ -1056,7 +1134,8 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   char* w = static_cast<char*>(ws);
   const uint16_t* h16 = static_cast<const uint16_t*>(hidden);
   const uint16_t* W16 = static_cast<const uint16_t*>(w_lm);
-  uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);
+  uint16_t* WT = reinterpret_cast<uint16_t*>(w + L.wt);  // packed
+  uint16_t* WP = reinterpret_cast<uint16_t*>(w + L.wp);  // packed
   uint16_t* hT = reinterpret_cast<uint16_t*>(w + L.ht);
   float2* part = reinterpret_cast<float2*>(w + L.part);
   RowScale* rs = reinterpret_cast<RowScale*>(w + L.rs);
@@ -1072,7 +1151,11 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
     return launch_reduce(T, seg->n_traj, w, L.loss, loss_out, aux, s) == hipSuccess ? GRPO_OK : GRPO_ERR_HIP;
   }
-  lm_transpose(W16, h16, T, H, V, Tp, WT, hT, s);
+  lm_transpose(W16, h16, T, H, V, Tp, nullptr, hT, s);
+  hipLaunchKernelGGL(k_pack_t, dim3((unsigned)((V + 63) / 64), (unsigned)((H + 63) / 64)), dim3(256), 0, s, W16, V,
+                     (int)H, (int)V, WT);
+  hipLaunchKernelGGL(k_pack_rows, dim3((unsigned)(packed_kb_count(V) / 4), (unsigned)((H + 31) / 32)), dim3(256), 0,
+                     s, W16, V, (int)H, (int)V, WP);
   if (hipGetLastError() != hipSuccess) return GRPO_ERR_HIP;
   const bool timed = aux && aux->hot_begin && aux->hot_end;
   if (timed && hipEventRecord(aux->hot_begin, s) != hipSuccess) return GRPO_ERR_HIP;
@@ -1085,13 +1168,13 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     const int64_t t0 = (int64_t)b * L.Tbp;
     const int rows = rows_of(b), rows_p = (rows + TILE - 1) / TILE * TILE;
     PartialArgs pa;
-    pa.g = GemmArgs{h16 + t0 * H, WT, H, H, rows, (int)V, (int)H};
+    pa.g = GemmArgs{h16 + t0 * H, WT, H, 0, rows, (int)V, (int)H};
     pa.part = part;
     pa.n_tiles = L.n_tiles;
     pa.z = z_of(b);
     pa.ldz = L.ldz;
     pa.part_t = nullptr;
-    hipLaunchKernelGGL(k_lm_partial<true>, gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
+    hipLaunchKernelGGL((k_lm_partial<true, true>), gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
     CombineArgs ca;
     ca.tok = tok;
     ca.part = part;
@@ -1102,12 +1185,12 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     ca.H = (int)H;
     ca.n_tiles = L.n_tiles;
     ca.t0 = (int)t0;
-    hipLaunchKernelGGL(k_lm_combine, dim3((unsigned)rows_p), dim3(256), 0, s, ca);
+    hipLaunchKernelGGL(k_lm_combine<true>, dim3((unsigned)rows_p), dim3(256), 0, s, ca);
   };
   // block b's D and D^T from its stored logits; `grid` workgroups (0: one per work item)
   auto dpass = [&](int b, hipStream_t st, int grid) {
     const int rows_p = (rows_of(b) + TILE - 1) / TILE * TILE;
-    const BlockDArgs da{z_of(b), rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V, rows_p};
+    const BlockDArgs da{z_of(b), rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V, rows_p, 1};
     hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(rows_p, L.ldz, grid)), dim3(256), 0, st, da);
   };
   // block b's dhidden rows = D W^T (K = V) and dW (+)= h^T D (K = the block's rows, zero-padded), on s
@@ -1115,12 +1198,12 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     const int64_t t0 = (int64_t)b * L.Tbp;
     const int rows = rows_of(b), rows_p = (rows + TILE - 1) / TILE * TILE;
     DhThenDwArgs ba;
-    ba.dh.g = GemmArgs{D, W16, L.ldz, V, rows, (int)H, (int)V};
+    ba.dh.g = GemmArgs{D, WP, L.ldz, 0, rows, (int)H, (int)V};
     ba.dh.acc = nullptr;
     ba.dh.dh = dh16 + t0 * H;
     ba.dh.first = 1;
     ba.dh.last = 1;
-    ba.dw.g = GemmArgs{hT + t0, DT, Tp, rows_p, (int)H, (int)V, rows_p};
+    ba.dw.g = GemmArgs{hT + t0, DT, Tp, 0, (int)H, (int)V, rows_p};
     ba.dw.dw = dw_lm;
     ba.dw.V = V;
     ba.dw.c0 = 0;
@@ -1346,7 +1429,7 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
   if (logits_in) {
     // D, D^T of the whole shard from its stored logits, then dW (K = Tp) and the fp32 partial dhidden (K = V_shard)
     // in one launch, the long dW tiles first
-    const BlockDArgs da{logits_in, rs, D, DT, Vsp, (int)V_shard, Tp};
+    const BlockDArgs da{logits_in, rs, D, DT, Vsp, (int)V_shard, Tp, 0};
     hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(Tp, Vsp, 0)), dim3(256), 0, s, da);
     DhDwArgs ba;
     ba.dh.g = GemmArgs{D, W16, Vsp, V_shard, (int)T, (int)H, (int)V_shard};

@@ -6,7 +6,14 @@ instruction put into its data registers; the compiler inserts no wait state ther
 dlogits stores therefore carry two wait states each.  This test compiles every kernel source to gfx950 assembly
 (no GPU needed) and fails if any store in the library is followed that closely by a write to its data registers,
 so a change of code or compiler that brings the pattern back is caught before it runs.
+
+Two more checks of the same assembly.  The packed-operand GEMM core loads B fragments with inline asm, which the
+compiler cannot count: no instruction may write a register that such a load is still filling before a
+vmcnt(0) wait (a late load would overwrite it; an index overwritten this way once sent a load to a wild
+address).  And the token-blocked schedule runs its D pass beside the forward product on every CU, which needs
+both workgroups' registers and LDS to fit one CU together.
 """
+import functools
 import os
 import re
 import shutil
@@ -70,14 +77,103 @@ def test_scanner_finds_the_pattern():
     assert scan(ok_nop) == [] and scan(ok_load) == [] and scan(ok_far) == []
 
 
-@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not installed")
-@pytest.mark.parametrize("src", sorted(f for f in os.listdir(CSRC) if f.endswith(".hip")) + ["bench/stream_copy.hip"])
-def test_no_store_data_overwrite(src, tmp_path):
-    out = tmp_path / (os.path.basename(src) + ".s")
+def _instructions(asm: str) -> list:
+    fn, insts = None, []
+    for line in asm.splitlines():
+        if re.match(r"^[_A-Za-z][\w.$]*:", line) and not line.startswith(".L"):
+            fn = line.split(":")[0]
+        s = line.split(";")[0].strip()
+        if s and not s.startswith(".") and not s.endswith(":"):
+            insts.append((fn, s))
+    return insts
+
+
+def scan_late_loads(asm: str) -> list:
+    """(function, load, offending instruction) for every 16-byte buffer load into registers (not into LDS) whose
+    destination a later instruction of the same function writes before a vmcnt(0) wait, in program order (which
+    also covers the path out of a loop after its last iteration)."""
+    insts, hits = _instructions(asm), []
+    for i, (fn, s) in enumerate(insts):
+        op = s.split()[0]
+        if op != "buffer_load_dwordx4" or s.endswith(" lds"):
+            continue
+        dst = _vregs(s[len(op):].split(",")[0].strip())
+        for fn2, s2 in insts[i + 1:]:
+            op2 = s2.split()[0]
+            if fn2 != fn or op2 == "s_endpgm" or (op2 == "s_waitcnt" and "vmcnt(0)" in s2):
+                break
+            if not op2.startswith(("v_", "ds_read", "global_load", "buffer_load", "flat_load", "scratch_load")):
+                continue
+            if op2.startswith(("v_cmp", "v_readlane", "v_readfirstlane")):
+                continue
+            if _vregs(s2[len(op2):].split(",")[0].strip()) & dst:
+                if not op2.startswith("buffer_load"):  # the next load into the same registers is fine
+                    hits.append((fn, s, s2))
+                break
+    return hits
+
+
+def test_late_load_scanner_finds_the_pattern():
+    bad = ("k:\n\tbuffer_load_dwordx4 v[130:133], v192, s[8:11], 0 offen\n\ts_add_i32 s4, s4, 1\n"
+           "\tv_and_b32_e32 v130, 0xc0, v0\n\ts_waitcnt vmcnt(0)\n")
+    assert len(scan_late_loads(bad)) == 1
+    ok = ("k:\n\tbuffer_load_dwordx4 v[130:133], v192, s[8:11], 0 offen\n\ts_waitcnt vmcnt(0)\n"
+          "\tv_and_b32_e32 v130, 0xc0, v0\n")
+    lds = "k:\n\tbuffer_load_dwordx4 v9, s[12:15], 0 offen lds\n\tv_mov_b32_e32 v9, 0\n"
+    assert scan_late_loads(ok) == [] and scan_late_loads(lds) == []
+
+
+SOURCES = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip")) + ["bench/stream_copy.hip"]
+
+
+@functools.lru_cache(maxsize=None)
+def _assembly(src: str) -> str:
+    import tempfile
+    d = tempfile.mkdtemp()
+    out = os.path.join(d, os.path.basename(src) + ".s")
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature", "-Xclang",
            "-packed-fp32-ops", "-I" + os.path.join(ROOT, "include"), "-I" + CSRC, "--cuda-device-only", "-S",
-           os.path.join(CSRC, src), "-o", str(out)]
+           os.path.join(CSRC, src), "-o", out]
     subprocess.run(cmd, check=True, capture_output=True)
-    hits = scan(out.read_text())
+    with open(out) as f:
+        text = f.read()
+    shutil.rmtree(d, ignore_errors=True)
+    return text
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not installed")
+@pytest.mark.parametrize("src", SOURCES)
+def test_no_store_data_overwrite(src):
+    hits = scan(_assembly(src))
     assert not hits, "\n".join(f"{fn}: [{a}] then [{b}]" for fn, a, b in hits[:10])
-    shutil.rmtree(tmp_path, ignore_errors=True)
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not installed")
+@pytest.mark.parametrize("src", SOURCES)
+def test_no_register_reuse_under_a_late_load(src):
+    hits = scan_late_loads(_assembly(src))
+    assert not hits, "\n".join(f"{fn}: [{a}] then [{b}]" for fn, a, b in hits[:10])
+
+
+def _kernel_resources(asm: str) -> dict:
+    res = {}
+    for block in asm.split("  - .agpr_count:")[1:]:
+        name = re.search(r"\.name:\s+(\S+)", block).group(1)
+        res[name] = dict(vgpr=int(re.search(r"\.vgpr_count:\s+(\d+)", block).group(1)),
+                         lds=int(re.search(r"\.group_segment_fixed_size:\s+(\d+)", block).group(1)),
+                         spill=int(re.search(r"\.vgpr_spill_count:\s+(\d+)", block).group(1)))
+    return res
+
+
+@pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not installed")
+def test_d_pass_fits_beside_the_forward_product():
+    """One forward-product workgroup (8 waves, two per SIMD) and one D-pass workgroup (4 waves, one per SIMD) on
+    one CU: 512 registers per lane per SIMD, allocated 8 at a time, and 160 KB of LDS."""
+    res = _kernel_resources(_assembly("lmhead.hip"))
+    fwd = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_partialILb1ELb1E")]
+    dpass = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_block_d")]
+    assert len(fwd) == 1 and len(dpass) == 1, sorted(res)
+    alloc = lambda n: (n + 7) // 8 * 8
+    assert 2 * alloc(fwd[0]["vgpr"]) + alloc(dpass[0]["vgpr"]) <= 512, (fwd, dpass)
+    assert fwd[0]["lds"] + dpass[0]["lds"] <= 160 * 1024, (fwd, dpass)
+    assert fwd[0]["spill"] == 0 and dpass[0]["spill"] == 0
