@@ -235,24 +235,26 @@ int fused_lmhead_grpo(const void* hidden, const void* w_lm, int64_t T, int64_t H
                       float* dw_lm, int32_t accumulate_dw, grpo_aux* aux, void* ws, size_t ws_bytes,
                       hipStream_t s);
 
-/* Bytes of device workspace fused_lmhead_grpo_blocked needs: besides W^T, h^T and the per-row scales, the fp32
- * logits of two blocks (one when a single block covers T) and one block's D and D^T, (4 + 4 + 2 + 2) * B * Vp
- * bytes with B = min(token_block, T rounded up to 256) and Vp = V rounded up to 256 (16.6 GB in all at
- * T = 65,536, H = 3,584, V = 151,936, token_block = 8192).  0 for invalid sizes. */
+/* Bytes of device workspace fused_lmhead_grpo_blocked needs: besides W^T, h^T and the per-row scales, the fp16
+ * logit terms and tile partials of two blocks (one when a single block covers T) and one block's D and D^T,
+ * about (2 + 2 + 2 + 2) * B * Vp bytes with B = min(token_block, T rounded up to 256) and Vp = V rounded up to
+ * 256 (12.7 GB in all at T = 65,536, H = 3,584, V = 151,936, token_block = 8192).  0 for invalid sizes. */
 size_t fused_lmhead_blocked_workspace_bytes(int64_t T, int64_t H, int64_t V, int32_t token_block, int32_t n_traj);
 
 /*
  * The fused LM-head path of fused_lmhead_grpo, scheduled over blocks of tokens instead of vocabulary chunks, and
  * with the same results up to the order of fp32 sums.  The forward product of a block of `token_block` rows
- * (z = h W, on the matrix cores, 256-column tiles) is kept in the workspace as fp32 until the block's rows have
- * their log-sum-exp; D of the block is then formed from the stored logits instead of a second product, so three
- * products run instead of four.  The logits of the whole batch are never stored: at most two blocks at a time.
+ * (z = h W, on the matrix cores, 256-column tiles) is kept in the workspace until the block's rows have their
+ * log-sum-exp, as each logit's term exp(z - m) in fp16 (m its row's maximum over the tile: terms <= 1, relative
+ * error <= 2^-11 down to 2^-14); D of the block is then formed from the stored terms (one multiply per logit)
+ * instead of a second product, so three products run instead of four.  The logits of the whole batch are never
+ * stored: at most two blocks at a time.
  * Per block: dhidden rows = D W^T (the whole vocabulary as K, written once in bf16), dW (+)= h^T D.
  *   token_block  a positive multiple of 256, at most 8,388,352 (8192 is the tuned value)
  *   all other arguments as fused_lmhead_grpo
  *   ws, ws_bytes device workspace of at least fused_lmhead_blocked_workspace_bytes(...)
  *   s_aux        NULL (or s): everything runs on s.  Otherwise a second stream of the caller's, on the same
- *                device: each block's D pass (stored logits -> D, D^T) then runs on s_aux beside the next
+ *                device: each block's D pass (stored terms -> D, D^T) then runs on s_aux beside the next
  *                block's forward product on s.  The call orders the two streams with two HIP events it creates
  *                and releases itself; s_aux's work is joined back into s before the last launch on s, so the
  *                results are complete in s's order, as with one stream (and the call can be captured from s

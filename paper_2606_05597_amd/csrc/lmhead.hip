@@ -15,9 +15,11 @@
 // The token-blocked schedule (fused_lmhead_grpo_blocked) takes rows in blocks
 // instead and keeps a block's logits, so the forward product is not recomputed:
 //   per block of B rows:
-//     z = h_block W  -> tile partials and the fp32 logits of the block (HBM)
+//     z = h_block W  -> tile partials, and each logit's term exp(z - m) (m its row's
+//                       maximum over the 256-column tile) as fp16 (HBM)
 //     rows           combine, as above
-//     D pass         stored logits -> D, D^T (bf16), a streaming pass
+//     D pass         stored terms -> D = g e^(m - lse) exp(z - m), D^T (bf16), a
+//                    streaming pass with one multiply per logit
 //     one launch     dhidden rows = D W^T (K = V, written once), then
 //                    dW (+)= h_block^T D (K = B)
 //   With a second stream, block b's D pass runs beside block b + 1's forward
@@ -79,18 +81,23 @@ struct PartialArgs {
   float* z;      // STORE_Z: the fp32 logits [tiles_of(M) * TILE, ldz], every tile stored whole
   int64_t ldz;   // a multiple of TILE, at least n_tiles * TILE
   float* part_t; // entropy partials [T, n_tiles]: sum over the tile of e^(z - m) (z - m), m the tile's max
+  uint16_t* e16; // TERMS: every logit's term e = exp(z - m), m its row's max over the tile, fp16 [tiles_of(M) *
+                 // TILE, ldz], every tile stored whole (0 past N)
 };
 
 // The forward product's epilogue: per (row, 256-column tile) the max m and sum exp(z - m) into part, and with ENT
-// also sum exp(z - m) (z - m) into part_t (the entropy's second moment).  Columns past N are left out.
-template <bool ENT>
+// also sum exp(z - m) (z - m) into part_t (the entropy's second moment); with TERMS every logit's term exp(z - m)
+// into p.e16 as fp16 (round to nearest even; the terms are <= 1, so the relative error is at most 2^-11 for terms
+// >= 2^-14 and the absolute one at most 2^-25 below).  Columns past N are left out (their terms stored as 0).
+template <bool ENT, bool TERMS = false>
 __device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x16 (&acc)[LmCfg::IB][LmCfg::JB],
                                                     int m0, int n0, int tn, GemmSmem& sm);
 
 // PACKED: B is W^T in the fragment-packed layout (gemm_mainloop_packed); the accumulators, and so every output,
-// are bit-identical to the LDS-staged core's.
-template <bool STORE_Z, bool PACKED = false>
+// are bit-identical to the LDS-staged core's.  STORE_Z: the fp32 logits too; TERMS: the fp16 terms (p.e16).
+template <bool STORE_Z, bool PACKED = false, bool TERMS = false>
 __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
+  static_assert(!(STORE_Z && TERMS), "one kind of stored logits");
   __shared__ __attribute__((aligned(16))) GemmSmem sm;
   int tm, tn;
   if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
@@ -131,7 +138,7 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial(const PartialArgs p) {
         }
       }
   }
-  lm_partial_epilogue<false>(p, acc, m0, n0, tn, sm);
+  lm_partial_epilogue<false, TERMS>(p, acc, m0, n0, tn, sm);
 }
 
 // The forward-only fused product: tile partials with the entropy moment, no logits stored.
@@ -141,52 +148,97 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_partial_ent(const PartialArgs 
   if (!gemm_tile_of(blockIdx.x, gridDim.x, tiles_of(p.g.M), tiles_of(p.g.N), tm, tn)) return;
   g_f32x16 acc[LmCfg::IB][LmCfg::JB];
   gemm_mainloop<LmCfg>(p.g, tm * TILE, tn * TILE, acc, sm.s);
-  lm_partial_epilogue<true>(p, acc, tm * TILE, tn * TILE, tn, sm);
+  lm_partial_epilogue<true, false>(p, acc, tm * TILE, tn * TILE, tn, sm);
 }
 
-template <bool ENT>
+template <bool ENT, bool TERMS>
 __device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x16 (&acc)[LmCfg::IB][LmCfg::JB],
                                                     int m0, int n0, int tn, GemmSmem& sm) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / LmCfg::WGN, wn = wave % LmCfg::WGN;
-  // A 16-lane row of a wave holds 16 x JB columns of one output row: reduce them with
-  // DPP, then the 2 x WGN such groups of each row through LDS.
+  // A 16-lane row of a wave holds 16 x JB columns of one output row: reduce them with DPP, then the 2 x WGN such
+  // groups of each row through LDS.  First the row's maximum over the tile, then one pass of exponentials against
+  // it for the sums (and the stored terms).
   constexpr int NG = 2 * LmCfg::WGN;
-  float* sh_m = reinterpret_cast<float*>(sm.s);  // [NG][TILE]
-  float* sh_s = sh_m + NG * TILE;                 // [NG][TILE]
-  float* sh_t = sh_s + NG * TILE;                 // [NG][TILE], ENT only
+  float* sh_m = reinterpret_cast<float*>(sm.s);  // [NG][TILE] group maxima
+  float* sh_s = sh_m + NG * TILE;                 // [NG][TILE] group sums
+  float* sh_t = sh_s + NG * TILE;                 // [NG][TILE] group entropy moments, ENT only
+  float* sh_M = sh_t + NG * TILE;                 // [TILE] the rows' maxima over the tile
   const int grp = wn * 2 + ((lane >> 4) & 1);
   const int c = n0 + gemm_col<LmCfg>(wn, 0, lane);
   const bool full = n0 + TILE <= p.g.N;
+  auto logit = [&](int i, int j, int r) { return (full || c + 32 * j < p.g.N) ? acc[i][j][r] : -INFINITY; };
+#define GRPO_DPP_STEP(OP, X, CTRL) _Pragma("unroll") for (int u = 0; u < 4; ++u) X[u] = OP(X[u], dpp_f32<CTRL>(X[u]));
 #pragma unroll
   for (int i = 0; i < LmCfg::IB; ++i) {
 #pragma unroll
     for (int r0 = 0; r0 < 16; r0 += 4) {  // four rows at a time: independent DPP chains interleave
-      float v[4][LmCfg::JB], m[4], e[4], tt[4];
+      float m[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         m[u] = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < LmCfg::JB; ++j) {
-          v[u][j] = (full || c + 32 * j < p.g.N) ? acc[i][j][r0 + u] : -INFINITY;
-          m[u] = fmaxf(m[u], v[u][j]);
-        }
+        for (int j = 0; j < LmCfg::JB; ++j) m[u] = fmaxf(m[u], logit(i, j, r0 + u));
       }
-#define GRPO_DPP_STEP(OP, X, CTRL) _Pragma("unroll") for (int u = 0; u < 4; ++u) X[u] = OP(X[u], dpp_f32<CTRL>(X[u]));
       GRPO_DPP_STEP(fmaxf, m, 0xB1)
       GRPO_DPP_STEP(fmaxf, m, 0x4E)
       GRPO_DPP_STEP(fmaxf, m, 0x141)
       GRPO_DPP_STEP(fmaxf, m, 0x140)
+      if ((lane & 15) == 0)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sh_m[grp * TILE + gemm_row<LmCfg>(wm, i, r0 + u, lane)] = m[u];
+    }
+  }
+  __syncthreads();
+  if (tid < TILE) {  // rows past M: the maximum of their zero logits
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < NG; ++q) M = fmaxf(M, sh_m[q * TILE + tid]);
+    sh_M[tid] = M;
+  }
+  __syncthreads();
+  const int x = lane & 3;
+#pragma unroll
+  for (int i = 0; i < LmCfg::IB; ++i) {
+#pragma unroll
+    for (int r0 = 0; r0 < 16; r0 += 4) {
+      // accumulators r0 .. r0 + 3 of a lane: rows rb .. rb + 3
+      const int rb = wm * LmCfg::WTM + i * 32 + 2 * r0 + 4 * (lane >> 5);
+      const f32x4 Mv = *reinterpret_cast<const f32x4*>(sh_M + rb);
+      float e[4], tt[4], xs[LmCfg::JB][4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const float nm = (m[u] == -INFINITY) ? 0.f : -m[u] * kLog2e;
+        const float nm = (Mv[u] == -INFINITY) ? 0.f : -Mv[u] * kLog2e;
         e[u] = 0.f;
         tt[u] = 0.f;
 #pragma unroll
         for (int j = 0; j < LmCfg::JB; ++j) {
-          const float x = __builtin_amdgcn_exp2f(fmaf(v[u][j], kLog2e, nm));
-          e[u] += x;
-          if constexpr (ENT) tt[u] += (v[u][j] == -INFINITY) ? 0.f : x * (v[u][j] - m[u]);
+          const float v = logit(i, j, r0 + u);
+          xs[j][u] = __builtin_amdgcn_exp2f(fmaf(v, kLog2e, nm));
+          e[u] += xs[j][u];
+          if constexpr (ENT) tt[u] += (v == -INFINITY) ? 0.f : xs[j][u] * (v - Mv[u]);
+        }
+      }
+      if constexpr (TERMS) {
+        // a 4 x 4 transpose within each quad of lanes (two DPP exchanges: lanes x ^ 1, then x ^ 2) leaves lane
+        // 4a + x with row rb + x and columns 4a .. 4a + 3 of the 32-column block j: 8 bytes per lane, and the
+        // j = 0, 1 stores of a wave fill whole 128-byte row pieces
+        uint16_t* er = p.e16 + (int64_t)(m0 + rb + x) * p.ldz + n0 + wn * LmCfg::WTN + 4 * ((lane & 31) >> 2);
+#pragma unroll
+        for (int j = 0; j < LmCfg::JB; ++j) {
+          float t[4], o[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float q = dpp_f32<0xB1>(xs[j][u ^ 1]);  // lane x ^ 1's term u ^ 1
+            t[u] = ((u ^ x) & 1) ? q : xs[j][u];
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float q = dpp_f32<0x4E>(t[u ^ 2]);  // lane x ^ 2's value u ^ 2
+            o[u] = ((u ^ x) & 2) ? q : t[u];
+          }
+          __builtin_nontemporal_store(u32x2{pack_f16(o[0], o[1]), pack_f16(o[2], o[3])},
+                                      reinterpret_cast<u32x2*>(er + 32 * j));
         }
       }
       GRPO_DPP_STEP(add_f32, e, 0xB1)
@@ -199,34 +251,24 @@ __device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x
         GRPO_DPP_STEP(add_f32, tt, 0x141)
         GRPO_DPP_STEP(add_f32, tt, 0x140)
       }
-#undef GRPO_DPP_STEP
-      if ((lane & 15) == 0) {
+      if ((lane & 15) == 0)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int row = gemm_row<LmCfg>(wm, i, r0 + u, lane);
-          sh_m[grp * TILE + row] = m[u];
-          sh_s[grp * TILE + row] = e[u];
-          if constexpr (ENT) sh_t[grp * TILE + row] = tt[u];
+          sh_s[grp * TILE + rb + u] = e[u];
+          if constexpr (ENT) sh_t[grp * TILE + rb + u] = tt[u];
         }
-      }
     }
   }
+#undef GRPO_DPP_STEP
   __syncthreads();
   if (tid < TILE && m0 + tid < p.g.M) {
-    float M = -INFINITY;
-#pragma unroll
-    for (int q = 0; q < NG; ++q) M = fmaxf(M, sh_m[q * TILE + tid]);
     float S = 0.f, Tm = 0.f;
-    if (M != -INFINITY)
 #pragma unroll
-      for (int q = 0; q < NG; ++q) {
-        const float mq = sh_m[q * TILE + tid];
-        const float g = __builtin_amdgcn_exp2f((mq - M) * kLog2e);
-        S += sh_s[q * TILE + tid] * g;
-        // a group with no column in range has m = -inf and nothing to add
-        if constexpr (ENT) Tm += (mq == -INFINITY) ? 0.f : g * (sh_t[q * TILE + tid] + sh_s[q * TILE + tid] * (mq - M));
-      }
-    p.part[(int64_t)(m0 + tid) * p.n_tiles + tn] = make_float2(M, S);
+    for (int q = 0; q < NG; ++q) {
+      S += sh_s[q * TILE + tid];
+      if constexpr (ENT) Tm += sh_t[q * TILE + tid];
+    }
+    p.part[(int64_t)(m0 + tid) * p.n_tiles + tn] = make_float2(sh_M[tid], S);
     if constexpr (ENT) p.part_t[(int64_t)(m0 + tid) * p.n_tiles + tn] = Tm;
   }
 }
@@ -683,9 +725,13 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_then_dw(const DhThenDwArgs 
   else lm_dw_tile<true, true>(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
 }
 
-// ---- token-blocked schedule: a block's stored fp32 logits -> D = g (softmax - onehot), bf16, as D and D^T ----
+// ---- D = g (softmax - onehot), bf16, as D and D^T: from a block's stored fp16 terms (the token-blocked schedule) or
+// fp32 logits (a vocabulary shard's kept logits) ----
 struct BlockDArgs {
-  const float* z;      // [rows, ld] the block's logits
+  const float* z;      // [rows, ld] the block's logits, or
+  const uint16_t* e16; // [rows, ld] (when not null) their fp16 terms e = exp(z - m) with m = part[row, tile].x
+  const float2* part;  // [rows, n_tiles] the block's tile partials (with e16)
+  int n_tiles;
   const RowScale* rs;  // [rows] the block's row scales
   uint16_t* D;         // [rows, ld]
   uint16_t* DT;        // [ld, rows], or with packed_dt D^T in the fragment-packed layout (N = ld, K = rows)
@@ -732,20 +778,45 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {  // rows 2 rp + 32 u and the next one
         const int row = 2 * rp + 32 * u;
-        const float* zr = a.z + (int64_t)(r0 + row) * a.ld + c;
-        const f32x4 x0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr));
-        const f32x4 x1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + a.ld));
         // the row scales are read from LDS where they are used (per element; the reads are merged): kept in
         // registers they take the pass past the 80 VGPRs that fit beside a forward-product workgroup (2 x 216 of
         // a SIMD's 512)
         float d0[4], d1[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int64_t v = c + e;
+        if (a.e16) {  // d = e g exp(m - lse): one multiply per logit, the factor once per row and 64 columns
+          const uint16_t* er = a.e16 + (int64_t)(r0 + row) * a.ld + c;
+          const u32x2 y0 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(er));
+          const u32x2 y1 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(er + a.ld));
+          const int64_t tile = (cs + it * 64) / TILE;
           const RowScale& s0 = srs[row];
           const RowScale& s1 = srs[row + 1];
-          d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : s0.sign * __builtin_amdgcn_exp2f(fmaf(x0[e], kLog2e, s0.nc));
-          d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : s1.sign * __builtin_amdgcn_exp2f(fmaf(x1[e], kLog2e, s1.nc));
+          // a row without gradient (nc = -inf: padding past the block's rows, whose partials were never written,
+          // or a flagged row) gets the factor 0 without its partial being read
+          const float f0 = s0.nc == -INFINITY ? 0.f
+                           : s0.sign * __builtin_amdgcn_exp2f(fmaf(a.part[(int64_t)(r0 + row) * a.n_tiles + tile].x,
+                                                                   kLog2e, s0.nc));
+          const float f1 = s1.nc == -INFINITY ? 0.f
+                           : s1.sign * __builtin_amdgcn_exp2f(fmaf(a.part[(int64_t)(r0 + row + 1) * a.n_tiles + tile].x,
+                                                                   kLog2e, s1.nc));
+          const f32x2 e00 = unpack_f16(y0[0]), e01 = unpack_f16(y0[1]), e10 = unpack_f16(y1[0]), e11 = unpack_f16(y1[1]);
+          const float x0[4] = {e00[0], e00[1], e01[0], e01[1]}, x1[4] = {e10[0], e10[1], e11[0], e11[1]};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t v = c + e;
+            d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : x0[e] * f0;
+            d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : x1[e] * f1;
+          }
+        } else {
+          const float* zr = a.z + (int64_t)(r0 + row) * a.ld + c;
+          const f32x4 x0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr));
+          const f32x4 x1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + a.ld));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t v = c + e;
+            const RowScale& s0 = srs[row];
+            const RowScale& s1 = srs[row + 1];
+            d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : s0.sign * __builtin_amdgcn_exp2f(fmaf(x0[e], kLog2e, s0.nc));
+            d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : s1.sign * __builtin_amdgcn_exp2f(fmaf(x1[e], kLog2e, s1.nc));
+          }
         }
         const uint32_t p00 = pack_bf16(d0[0], d0[1]), p01 = pack_bf16(d0[2], d0[3]);
         const uint32_t p10 = pack_bf16(d1[0], d1[1]), p11 = pack_bf16(d1[2], d1[3]);
@@ -907,7 +978,7 @@ static void lm_transpose(const uint16_t* W16, const uint16_t* h16, int64_t T, in
 
 static void lm_pass1(const uint16_t* h16, const uint16_t* WT, int64_t T, int64_t H, int64_t V, float2* part,
                      int n_tiles, hipStream_t s) {
-  PartialArgs pa;
+  PartialArgs pa{};
   pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
   pa.part = part;
   pa.n_tiles = n_tiles;
@@ -989,9 +1060,10 @@ static LmBlockWs lm_block_ws_layout(int64_t T, int64_t H, int64_t V, int32_t Tb,
   l.wt = o;   o = align_up(o + (size_t)packed_bytes(V, H));
   l.wp = o;   o = align_up(o + (size_t)packed_bytes(H, V));
   l.ht = o;   o = align_up(o + sizeof(uint16_t) * (size_t)(H * l.Tp));
-  l.part = o; o = align_up(o + sizeof(float2) * (size_t)(l.Tbp * l.n_tiles));
+  const size_t nbuf = l.Tp > l.Tbp ? 2 : 1;  // the tile partials and terms of two blocks in flight
+  l.part = o; o = align_up(o + sizeof(float2) * (size_t)(l.Tbp * l.n_tiles) * nbuf);
   l.rs = o;   o = align_up(o + sizeof(RowScale) * (size_t)l.Tp);
-  l.z = o;    o = align_up(o + sizeof(float) * (size_t)(l.Tbp * l.ldz) * (l.Tp > l.Tbp ? 2 : 1));
+  l.z = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tbp * l.ldz) * nbuf);
   l.d = o;    o = align_up(o + sizeof(uint16_t) * (size_t)(l.Tbp * l.ldz));
   l.dt = o;   o = align_up(o + (size_t)packed_bytes(l.ldz, l.Tbp));
   l.total = o;
@@ -1139,7 +1211,7 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   uint16_t* hT = reinterpret_cast<uint16_t*>(w + L.ht);
   float2* part = reinterpret_cast<float2*>(w + L.part);
   RowScale* rs = reinterpret_cast<RowScale*>(w + L.rs);
-  float* z = reinterpret_cast<float*>(w + L.z);
+  uint16_t* e16 = reinterpret_cast<uint16_t*>(w + L.z);
   uint16_t* D = reinterpret_cast<uint16_t*>(w + L.d);
   uint16_t* DT = reinterpret_cast<uint16_t*>(w + L.dt);
   uint16_t* dh16 = static_cast<uint16_t*>(dhidden);
@@ -1162,22 +1234,24 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   const TokenArgs tok = make_token_args(V, actions, behave_logp, prox_logp, adv, p, w, L.loss, aux);
   const int n_blocks = (int)((T + L.Tbp - 1) / L.Tbp);
   auto rows_of = [&](int b) { return (int)(T - (int64_t)b * L.Tbp < L.Tbp ? T - (int64_t)b * L.Tbp : L.Tbp); };
-  auto z_of = [&](int b) { return z + (size_t)(b & 1) * (size_t)(L.Tbp * L.ldz); };
+  auto e_of = [&](int b) { return e16 + (size_t)(b & 1) * (size_t)(L.Tbp * L.ldz); };
+  auto part_of = [&](int b) { return part + (size_t)(b & 1) * (size_t)(L.Tbp * L.n_tiles); };
   // block b's forward product (partials, logits into its buffer) and its rows' combine, on s
   auto forward = [&](int b) {
     const int64_t t0 = (int64_t)b * L.Tbp;
     const int rows = rows_of(b), rows_p = (rows + TILE - 1) / TILE * TILE;
-    PartialArgs pa;
+    PartialArgs pa{};
     pa.g = GemmArgs{h16 + t0 * H, WT, H, 0, rows, (int)V, (int)H};
-    pa.part = part;
+    pa.part = part_of(b);
     pa.n_tiles = L.n_tiles;
-    pa.z = z_of(b);
+    pa.z = nullptr;
+    pa.e16 = e_of(b);
     pa.ldz = L.ldz;
     pa.part_t = nullptr;
-    hipLaunchKernelGGL((k_lm_partial<true, true>), gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
+    hipLaunchKernelGGL((k_lm_partial<false, true, true>), gemm_grid(rows, V), dim3(LmCfg::NT), 0, s, pa);
     CombineArgs ca;
     ca.tok = tok;
-    ca.part = part;
+    ca.part = part_of(b);
     ca.h = h16;
     ca.WT = WT;
     ca.rs = rs;
@@ -1190,7 +1264,8 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
   // block b's D and D^T from its stored logits; `grid` workgroups (0: one per work item)
   auto dpass = [&](int b, hipStream_t st, int grid) {
     const int rows_p = (rows_of(b) + TILE - 1) / TILE * TILE;
-    const BlockDArgs da{z_of(b), rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V, rows_p, 1};
+    const BlockDArgs da{nullptr, e_of(b), part_of(b), L.n_tiles, rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V,
+                        rows_p, 1};
     hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(rows_p, L.ldz, grid)), dim3(256), 0, st, da);
   };
   // block b's dhidden rows = D W^T (K = V) and dW (+)= h^T D (K = the block's rows, zero-padded), on s
@@ -1304,7 +1379,7 @@ extern "C" int fused_lmhead_token_logp(const void* hidden, const void* w_lm, int
   const int n_tiles = (int)((V + TILE - 1) / TILE);
   lm_transpose(static_cast<const uint16_t*>(w_lm), h16, T, H, V, 0, WT, nullptr, s);
   if (token_entropy) {
-    PartialArgs pa;
+    PartialArgs pa{};
     pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V, (int)H};
     pa.part = part;
     pa.n_tiles = n_tiles;
@@ -1352,7 +1427,7 @@ extern "C" int fused_lmhead_vocab_shard_stats(const void* hidden, const void* w_
   const int n_tiles = (int)((V_shard + TILE - 1) / TILE);
   lm_transpose(static_cast<const uint16_t*>(w_shard), h16, T, H, V_shard, 0, WT, nullptr, s);
   if (logits_out) {  // the shard's fp32 logits kept for the backward call
-    PartialArgs pa;
+    PartialArgs pa{};
     pa.g = GemmArgs{h16, WT, H, H, (int)T, (int)V_shard, (int)H};
     pa.part = part;
     pa.n_tiles = n_tiles;
@@ -1429,7 +1504,7 @@ extern "C" int fused_lmhead_grpo_vocab_shard(const void* hidden, const void* w_s
   if (logits_in) {
     // D, D^T of the whole shard from its stored logits, then dW (K = Tp) and the fp32 partial dhidden (K = V_shard)
     // in one launch, the long dW tiles first
-    const BlockDArgs da{logits_in, rs, D, DT, Vsp, (int)V_shard, Tp, 0};
+    const BlockDArgs da{logits_in, nullptr, nullptr, 0, rs, D, DT, Vsp, (int)V_shard, Tp, 0};
     hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(Tp, Vsp, 0)), dim3(256), 0, s, da);
     DhDwArgs ba;
     ba.dh.g = GemmArgs{D, W16, Vsp, V_shard, (int)T, (int)H, (int)V_shard};

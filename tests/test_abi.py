@@ -71,16 +71,18 @@ def test_workspace_queries(lib):
     assert f >= 2 * V * H + 2 * H * T + 2 * 2 * T * C + 4 * T * H and f % 256 == 0
     # a single chunk needs no dhidden accumulator
     assert lib.fused_lmhead_workspace_bytes(T, H, 4096, 4096, 64) < 2 * 4096 * H + 2 * H * T + 4 * T * 4096 + 4 * T * H
-    # token-blocked: W^T and W packed (V rounded to 32 and to 64), h^T, two blocks' fp32 logits, one block's D
-    # and packed D^T ((4 + 4 + 2 + 2) bytes per element of [block, V rounded to 256])
+    # token-blocked: W^T and W packed (V rounded to 32 and to 64), h^T, two blocks' fp16 logit terms and tile
+    # partials (8 bytes per row and 256-column tile), one block's D and packed D^T ((2 + 2 + 2 + 2) bytes per
+    # element of [block, V rounded to 256])
     Vp = (V + 255) // 256 * 256
     w2 = 2 * ((V + 31) // 32 * 32) * H + 2 * H * ((V + 63) // 64 * 64)
     fb = lib.fused_lmhead_blocked_workspace_bytes(T, H, V, 8192, 64)
-    assert fb >= w2 + 2 * H * T + 12 * 8192 * Vp and fb % 256 == 0
-    assert fb < w2 + 2 * H * T + 12 * 8192 * Vp + (64 << 20)
-    # one block covering T needs one logits buffer
+    parts = 2 * 8192 * (Vp // 256) * 8
+    assert fb >= w2 + 2 * H * T + 8 * 8192 * Vp + parts and fb % 256 == 0
+    assert fb < w2 + 2 * H * T + 8 * 8192 * Vp + parts + (64 << 20)
+    # one block covering T needs one buffer of terms and partials
     one = lib.fused_lmhead_blocked_workspace_bytes(8192, H, V, 8192, 64)
-    assert one < w2 + 2 * H * 8192 + 8 * 8192 * Vp + (64 << 20)
+    assert one < w2 + 2 * H * 8192 + 6 * 8192 * Vp + parts // 2 + (64 << 20)
     # a block larger than the batch is cut to the batch (rounded up to 256 rows)
     assert lib.fused_lmhead_blocked_workspace_bytes(300, H, V, 8192, 4) == \
         lib.fused_lmhead_blocked_workspace_bytes(300, H, V, 512, 4)

@@ -173,8 +173,10 @@ def test_fused_full_hv_reduced_t(sched):
 
 def test_fused_schedules_agree():
     # both schedules form the logits, their tile partials and the rows' epilogue with the same code on the same
-    # inputs: the loss and every per-token output are bit-identical; the backward products differ only in the
-    # order of their fp32 sums
+    # inputs: the loss and every per-token output are bit-identical.  The backward products differ in the order of
+    # their fp32 sums and in D: the token-blocked schedule forms it from fp16 terms exp(z - m) (relative error
+    # <= 2^-11 before D's own bf16 rounding), so about one D element in eight rounds to the neighbouring bf16
+    # value, and dW differs at the level of the oracle gate (relative Frobenius 5e-3; measured about 1e-3)
     b = make_fused_batch(small_cfg(4, 8, 256, 5000, seed=17, tok_mean=6.0, steps=(2, 9)), "cuda")
     A64, A32, seg, sto, tso = setup(b)
     l1, dh1, dW1, aux1 = run(b, A32, sto, tso, 1024, oracle.NORM_CONST_K, 3.0)
@@ -184,7 +186,9 @@ def test_fused_schedules_agree():
         assert torch.equal(getattr(aux1, f), getattr(aux2, f)), f
     dh1, dh2 = dh1.double(), dh2.double()
     assert ((dh1 - dh2).abs() <= 2.0 ** -7 * dh1.abs() + 1e-3 * dh1.abs().max()).all()
-    assert (dW1.double() - dW2.double()).norm() <= 1e-5 * dW1.double().norm()
+    rel = ((dW1.double() - dW2.double()).norm() / dW1.double().norm()).item()
+    print(f"dW between schedules: relative Frobenius {rel:.3g}")
+    assert rel <= 5e-3
 
 
 @pytest.mark.parametrize("tb,cfg_args,extras", [(256, (4, 8, 256, 5000, 18), False),

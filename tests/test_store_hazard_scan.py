@@ -170,7 +170,8 @@ def test_d_pass_fits_beside_the_forward_product():
     """One forward-product workgroup (8 waves, two per SIMD) and one D-pass workgroup (4 waves, one per SIMD) on
     one CU: 512 registers per lane per SIMD, allocated 8 at a time, and 160 KB of LDS."""
     res = _kernel_resources(_assembly("lmhead.hip"))
-    fwd = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_partialILb1ELb1E")]
+    # the token-blocked forward product: k_lm_partial<STORE_Z = false, PACKED = true, TERMS = true>
+    fwd = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_partialILb0ELb1ELb1E")]
     dpass = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_block_d")]
     assert len(fwd) == 1 and len(dpass) == 1, sorted(res)
     alloc = lambda n: (n + 7) // 8 * 8
