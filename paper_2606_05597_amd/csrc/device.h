@@ -35,15 +35,6 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// fp16 pairs: round-to-nearest-even pack of two fp32 values (v_cvt_pk_f16_f32), and the exact widening back.
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, f16x2));
-}
-__device__ __forceinline__ f32x2 unpack_f16(uint32_t w) {
-  return __builtin_convertvector(__builtin_bit_cast(f16x2, w), f32x2);
-}
-
 // ---- wave64 reductions -----------------------------------------------------
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
