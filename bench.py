@@ -551,7 +551,8 @@ def time_fused(b: dict, adv, sto, tso, steps: int, warmup: int, token_block: int
     achieved = alg / (hot_ms * 1e-3) / 1e12
     out = {"value": T / (ms * 1e-3), "unit": "tokens/s", "ms_per_step": ms, "steps": steps, "hot_ms": hot_ms,
            "loss": float(loss.item()), "workspace_bytes": need,
-           "schedule": (f"token blocks of {token_block} (their fp32 logits kept between the products; 3 products)"
+           "schedule": (f"token blocks of {token_block} (their logits kept between the products as fp16 terms exp(z - m); "
+                        f"3 products)"
                         if token_block else
                         f"vocabulary chunks of {cfg.vocab_chunk} (logits recomputed for the backward; 4 products)"),
            "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
