@@ -229,10 +229,13 @@ __device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x
         }
       }
       if constexpr (TERMS) {
-        // a 4 x 4 transpose within each quad of lanes (two DPP exchanges: lanes x ^ 1, then x ^ 2) leaves lane
-        // 4a + x with row rb + x and columns 4a .. 4a + 3 of the 32-column block j: 8 bytes per lane, and the
-        // j = 0, 1 stores of a wave fill whole 128-byte row pieces
+        // A 4 x 4 transpose within each quad of lanes (two DPP exchanges: lanes x ^ 1, then x ^ 2) leaves lane
+        // 4a + x with row rb + x and columns 4a .. 4a + 3 of each 32-column block j.  Lanes 4a + x and its
+        // partner 4(a ^ 1) + x then trade one block's 8 bytes, so that a lane with a even holds columns
+        // 4a .. 4a + 7 of block 0 and its partner the same columns of block 1: one 16-byte store per lane, and each
+        // store instruction fills the wave's whole 128-byte piece of its 8 rows.
         uint16_t* er = p.e16 + (int64_t)(m0 + rb + x) * p.ldz + n0 + wn * LmCfg::WTN + 4 * ((lane & 31) >> 2);
+        uint32_t pk[LmCfg::JB][2];
 #pragma unroll
         for (int j = 0; j < LmCfg::JB; ++j) {
           float t[4], o[4];
@@ -246,9 +249,20 @@ __device__ __forceinline__ void lm_partial_epilogue(const PartialArgs& p, g_f32x
             const float q = dpp_f32<0x4E>(t[u ^ 2]);  // lane x ^ 2's value u ^ 2
             o[u] = ((u ^ x) & 2) ? q : t[u];
           }
-          __builtin_nontemporal_store(u32x2{pack_f16(o[0], o[1]), pack_f16(o[2], o[3])},
-                                      reinterpret_cast<u32x2*>(er + 32 * j));
+          pk[j][0] = pack_f16(o[0], o[1]);
+          pk[j][1] = pack_f16(o[2], o[3]);
         }
+        static_assert(LmCfg::JB == 2, "two 32-column blocks per wave");
+        const bool even = ((lane >> 2) & 1) == 0;
+        uint32_t r[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          // lane L ^ 4: the quad reversed (quad_perm [3, 2, 1, 0] = 0x1B), then the 8-lane group mirrored (0x141)
+          const float sent = __uint_as_float(even ? pk[1][q] : pk[0][q]);
+          r[q] = __float_as_uint(dpp_f32<0x141>(dpp_f32<0x1B>(sent)));
+        }
+        const u32x4 w = even ? u32x4{pk[0][0], pk[0][1], r[0], r[1]} : u32x4{r[0], r[1], pk[1][0], pk[1][1]};
+        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(er + (even ? 0 : 32 - 4)));
       }
       GRPO_DPP_STEP(add_f32, e, 0xB1)
       GRPO_DPP_STEP(add_f32, e, 0x4E)
