@@ -798,7 +798,7 @@ def main():
     head = time_logits(b, grpo.GRPO_NORM_CONST_K, args.steps, args.warmup, dlogits=dlogits)
     roof = head["roofline"]
     roof["traffic"] = measured_traffic(T)
-    roof["kernel"] = "k_rows_pipe<19, 4> (bf16, 1024 threads, one workgroup per CU)"
+    roof["kernel"] = "k_rows_pipe<19, 6> (bf16, 1024 threads, one workgroup per CU)"
     out = {
         "metric": METRIC,
         "value": head["value"],

@@ -83,6 +83,48 @@ __device__ __forceinline__ float vec_sumexp(const u32x4& x, float nmb) {
   return s;
 }
 
+// The LDS part of a k_rows_pipe row keeps its terms: the sum pass overwrites each vector of 8 bf16 logits in the
+// thread's own LDS slot with its terms e = exp(z - m) as fp16 pairs (round to nearest even), and the dlogits pass
+// forms d = g exp(z - lse) = c e with one multiply, c = g exp(m - lse), instead of a second exponential.  The terms
+// are <= 1: relative error at most 2^-11 for e >= 2^-14, absolute at most 2^-25 below, before the bf16 rounding of
+// d.  The sum is formed from the fp32 terms in vec_sumexp's order.  (The register part cannot do the same: held in
+// place of the logits, the fp32 terms would wait for their packs in registers the row needs.)
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, f16x2));
+}
+__device__ __forceinline__ f32x2 unpack_f16(uint32_t w) {
+  return __builtin_convertvector(__builtin_bit_cast(f16x2, w), f32x2);
+}
+__device__ __forceinline__ float vec_sumexp_keep(u32x4& x, float nmb) {
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float lo = __builtin_amdgcn_exp2f(fmaf(bf16_lo(x[q]), kLog2e, nmb));
+    const float hi = __builtin_amdgcn_exp2f(fmaf(bf16_hi(x[q]), kLog2e, nmb));
+    s += lo + hi;
+    x[q] = pack_f16(lo, hi);
+  }
+  return s;
+}
+// dlogits of a vector of kept terms, bf16 round to nearest even; c carries the row's sign; the action column (when
+// it falls in this vector) replaced by d_a.
+__device__ __forceinline__ u32x4 vec_dlogits_kept(const u32x4& e, float c, bool has_act, int act_lane, float d_a) {
+  u32x4 o;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x2 f = unpack_f16(e[q]);
+    o[q] = pack_bf16(f[0] * c, f[1] * c);
+  }
+  if (has_act) {
+    const uint32_t da = pack_bf16(d_a, 0.f) & 0xffffu;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if ((act_lane >> 1) == q) o[q] = (act_lane & 1) ? ((o[q] & 0xffffu) | (da << 16)) : ((o[q] & 0xffff0000u) | da);
+  }
+  return o;
+}
+
 // Combines every thread's (max m, sum s of exp(z - m)) into the row's (M, S),
 // valid in thread 0: within each wave (DPP within rows of 16 lanes, then the
 // four rows), then across the NW <= 16 waves by the first 16 lanes of wave 0,
@@ -262,7 +304,11 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
     const float nmb1 = (m1 == -INFINITY) ? 0.f : -m1 * kLog2e;
     float s1 = 0.f;
 #pragma unroll 1
-    for (int j = 0; j < NP; ++j) s1 += vec_sumexp<uint16_t>(stage[j * NT + tid], nmb1);
+    for (int j = 0; j < NP; ++j) {  // the terms replace the logits in the thread's own LDS slots
+      u32x4 x = stage[j * NT + tid];
+      s1 += vec_sumexp_keep(x, nmb1);
+      stage[j * NT + tid] = x;
+    }
     float m = m1;
 #pragma unroll
     for (int q = 0; q < NR; ++q) {
@@ -291,6 +337,7 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
     if (tid == 64) sh_in = token_load(a.tok, tn < a.T ? tn : t);
 
     const uint32_t smask = sign_mask<uint16_t>(rs);
+    const float c1 = rs.sign * __builtin_amdgcn_exp2f(rs.nc - nmb1);  // the LDS part's terms: d = c1 e
     const int act_v = rs.act >= 0 ? rs.act / 8 : -1;
     fresh(reg);
     // forward only: a zero-sized destination, so the range check drops every store
@@ -299,7 +346,7 @@ __global__ __launch_bounds__(1024) void k_rows_pipe(const RowArgs a) {
 #pragma unroll 1
     for (int j = 0; j < NP; ++j)
       __builtin_amdgcn_raw_buffer_store_b128(
-          vec_dlogits<uint16_t>(stage[j * NT + tid], rs, smask, j * NT + tid == act_v, rs.act & 7), dst, voff, j * VB,
+          vec_dlogits_kept(stage[j * NT + tid], c1, j * NT + tid == act_v, rs.act & 7, rs.d_a), dst, voff, j * VB,
           kStream);
     lds_barrier();  // every wave is done reading stage[] (the stores read registers)
     if (tn < a.T) stage_row(tn, voff);
@@ -450,10 +497,11 @@ static const Variant kVariants[] = {
 static const RowKernel kPipe[] = {
     k_rows_pipe<7, 4>,   k_rows_pipe<8, 4>,   k_rows_pipe<9, 5>,   k_rows_pipe<10, 5>, k_rows_pipe<11, 6>,
     k_rows_pipe<12, 6>,  k_rows_pipe<13, 7>,  k_rows_pipe<14, 7>,  k_rows_pipe<15, 1>, k_rows_pipe<16, 2>,
-    k_rows_pipe<17, 3>,  k_rows_pipe<18, 4>,  k_rows_pipe<19, 4>,  k_rows_pipe<20, 9>, k_rows_pipe<21, 9>,
+    k_rows_pipe<17, 3>,  k_rows_pipe<18, 4>,  k_rows_pipe<19, 6>,  k_rows_pipe<20, 9>, k_rows_pipe<21, 9>,
     k_rows_pipe<22, 9>,  k_rows_pipe<23, 9>,
-};  // from 15 vectors on, 14 in registers and the rest in LDS, except 19 (V = 151,936): 15 and 4, which is 0.4%
-   // faster than 14 and 5 there (16 and 17 in registers also fit 128 VGPRs but are 0.3-0.8% slower)
+};  // from 15 vectors on, 14 in registers and the rest in LDS, except 19 (V = 151,936): 13 and 6, 0.3% faster
+   // than 15 and 4 (before the LDS part kept its terms, 15 and 4 was 0.4% faster than 14 and 5); 14 and 5, 12 and
+   // 7, 11 and 8 measured within 0.1% of 13 and 6
 constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 15 register vectors and 9 LDS vectors per thread
 constexpr int64_t kPipeMaxT = (int64_t)1 << 30;  // t + (gridDim.x - 1) * chunk + 1 stays far below 2^31
 

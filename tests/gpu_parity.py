@@ -11,7 +11,9 @@ targets; the rest follow from the arithmetic):
   * dlogits, absolute 2e-3 (bf16) and a scaled gate, since |dlogits| is far
     below 2e-3 at these sizes: with grad_scale = 1/max|g_t| (so rows are O(1)),
     |gpu - ref| <= 2^-8 |ref| + 1e-5 max_row|ref| for bf16 (one bf16 rounding
-    of a correct fp32 value), and <= 1e-5 max_row|ref| for fp32 outputs.
+    of a correct fp32 value; 2^-8 + 2^-11 on the rows the pipelined kernel runs,
+    whose LDS part rounds its terms to fp16 first), and <= 1e-5 max_row|ref| for
+    fp32 outputs.
 Rows whose oracle ratio sits within 1e-6 of a clip boundary or whose term
 sits within 1e-6 relative of the dual-clip floor are kinks, where either
 one-sided derivative is correct: they are counted and exempt from the dlogits
@@ -95,6 +97,11 @@ def kink_rows(ref: oracle.LossResult, behave, prox, adv_tok, eps_lo, eps_hi, c, 
     return np.nonzero(near)[0]
 
 
+# bf16 rows of 49,153 to 188,416 columns run the pipelined row kernel, whose LDS part forms dlogits from fp16 terms
+# exp(z - m) <= 1: one more relative rounding of at most 2^-11 before the bf16 one
+PIPE_TERMS_V = (49152, 188416)
+
+
 def check_dlogits(gpu: np.ndarray, ref: np.ndarray, is_bf16: bool, exempt=(), scaled: bool = False, what=""):
     """Applies the dlogits gates row by row; returns the max normalised error."""
     keep = np.ones(gpu.shape[0], bool)
@@ -105,7 +112,8 @@ def check_dlogits(gpu: np.ndarray, ref: np.ndarray, is_bf16: bool, exempt=(), sc
     if is_bf16:
         assert diff.max(initial=0) <= BF16_ABS, f"{what}: bf16 dlogits abs err {diff.max()}"
         if scaled:
-            bound = 2.0 ** -8 * np.abs(r) + 1e-5 * rowmax
+            terms = PIPE_TERMS_V[0] < r.shape[1] <= PIPE_TERMS_V[1]
+            bound = (2.0 ** -8 + (2.0 ** -11 if terms else 0.0)) * np.abs(r) + 1e-5 * rowmax
             worst = (diff / np.maximum(bound, 1e-300)).max(initial=0)
             assert worst <= 1.0, f"{what}: scaled bf16 gate exceeded by {worst}"
             return worst

@@ -344,7 +344,7 @@ def _edge_batch(V, dtype="bf16", n_groups=2, G=4, ld=None, seed=5, max_tok=6):
                                      (100000, "f32"), (151936, "f32")])
 def test_ragged_vocab_and_kernel_variants(V, dtype):
     # odd V uses the generic row kernel; bf16 rows of 56K to 188K take the pipelined kernel (122,880: one LDS
-    # vector per thread; 128,256: two; 151,936: four; 163,840 and 184,320: nine); fp32 rows up to 77,824 the
+    # vector per thread; 128,256: two; 151,936: six; 163,840 and 184,320: nine); fp32 rows up to 77,824 the
     # register-resident one; longer vector rows (bf16 200,000 and 262,144, fp32 100,000 and 151,936) the two
     # passes (a record per row, then the epilogue and dlogits)
     b = _edge_batch(V, dtype)
