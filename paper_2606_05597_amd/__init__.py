@@ -412,8 +412,8 @@ def fused_lmhead_grpo_blocked(hidden: torch.Tensor, w_lm: torch.Tensor, actions:
                               accumulate_dw: bool = False, aux: LossAux | None = None,
                               workspace: torch.Tensor | None = None, loss_out: torch.Tensor | None = None,
                               stream=None, aux_stream=None):
-    """As fused_lmhead_grpo, over blocks of `token_block` tokens whose fp32 logits are kept in the workspace
-    between the forward and backward products (three products instead of four).  With `aux_stream` (a second
+    """As fused_lmhead_grpo, over blocks of `token_block` tokens whose logits are kept in the workspace between
+    the forward and backward products, as fp16 terms exp(z - m) (three products instead of four).  With `aux_stream` (a second
     torch.cuda.Stream on the same device), each block's D pass runs on it beside the next block's forward
     product; the results are complete in `stream`'s order either way.
 
