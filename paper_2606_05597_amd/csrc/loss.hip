@@ -87,8 +87,9 @@ __device__ __forceinline__ float vec_sumexp(const u32x4& x, float nmb) {
 // thread's own LDS slot with its terms e = exp(z - m) as fp16 pairs (round to nearest even), and the dlogits pass
 // forms d = g exp(z - lse) = c e with one multiply, c = g exp(m - lse), instead of a second exponential.  The terms
 // are <= 1: relative error at most 2^-11 for e >= 2^-14, absolute at most 2^-25 below, before the bf16 rounding of
-// d.  The sum is formed from the fp32 terms in vec_sumexp's order.  (The register part cannot do the same: held in
-// place of the logits, the fp32 terms would wait for their packs in registers the row needs.)
+// d.  The sum is formed from the fp32 terms in vec_sumexp's order.  (Not the register part: kept there, the
+// compiler issued all of the part's exponentials ahead of their packs and spilled the fp32 terms; and with three
+// register vectors' terms parked in the LDS left free, the kernel ran no faster.)
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, f16x2));
@@ -500,8 +501,8 @@ static const RowKernel kPipe[] = {
     k_rows_pipe<17, 3>,  k_rows_pipe<18, 4>,  k_rows_pipe<19, 6>,  k_rows_pipe<20, 9>, k_rows_pipe<21, 9>,
     k_rows_pipe<22, 9>,  k_rows_pipe<23, 9>,
 };  // from 15 vectors on, 14 in registers and the rest in LDS, except 19 (V = 151,936): 13 and 6, 0.3% faster
-   // than 15 and 4 (before the LDS part kept its terms, 15 and 4 was 0.4% faster than 14 and 5); 14 and 5, 12 and
-   // 7, 11 and 8 measured within 0.1% of 13 and 6
+   // than 15 and 4 and 0.4% faster than 14 and 5, with 12 and 7 or 11 and 8 within 0.1% of it (before the LDS
+   // part kept its terms, 15 and 4 was 0.4% faster than 14 and 5)
 constexpr int kPipeMinNV = 7, kPipeMaxNV = 23;  // at most 15 register vectors and 9 LDS vectors per thread
 constexpr int64_t kPipeMaxT = (int64_t)1 << 30;  // t + (gridDim.x - 1) * chunk + 1 stays far below 2^31
 
