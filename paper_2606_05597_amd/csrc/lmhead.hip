@@ -748,12 +748,12 @@ __global__ __launch_bounds__(LmCfg::NT) void k_lm_dh_then_dw(const DhThenDwArgs 
   else lm_dw_tile<true, true>(p.dw, b - p.dh_blocks, (int)gridDim.x - p.dh_blocks, sm);
 }
 
-// ---- D = g (softmax - onehot), bf16, as D and D^T: from a block's stored fp16 terms (the token-blocked schedule) or
-// fp32 logits (a vocabulary shard's kept logits) ----
+// ---- D = g (softmax - onehot), bf16, as D and D^T: from fp32 logits (k_lm_block_d, a vocabulary shard's kept
+// logits) or from a block's stored fp16 terms (k_lm_block_d16, the token-blocked schedule) ----
 struct BlockDArgs {
-  const float* z;      // [rows, ld] the block's logits, or
-  const uint16_t* e16; // [rows, ld] (when not null) their fp16 terms e = exp(z - m) with m = part[row, tile].x
-  const float2* part;  // [rows, n_tiles] the block's tile partials (with e16)
+  const float* z;      // [rows, ld] the block's logits (k_lm_block_d), or
+  const uint16_t* e16; // [rows, ld] their fp16 terms e = exp(z - m) with m = part[row, tile].x (k_lm_block_d16)
+  const float2* part;  // [rows, n_tiles] the block's tile partials (k_lm_block_d16)
   int n_tiles;
   const RowScale* rs;  // [rows] the block's row scales
   uint16_t* D;         // [rows, ld]
@@ -805,41 +805,16 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
         // registers they take the pass past the 80 VGPRs that fit beside a forward-product workgroup (2 x 216 of
         // a SIMD's 512)
         float d0[4], d1[4];
-        if (a.e16) {  // d = e g exp(m - lse): one multiply per logit, the factor once per row and 64 columns
-          const uint16_t* er = a.e16 + (int64_t)(r0 + row) * a.ld + c;
-          const u32x2 y0 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(er));
-          const u32x2 y1 = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(er + a.ld));
-          const int64_t tile = (cs + it * 64) / TILE;
+        const float* zr = a.z + (int64_t)(r0 + row) * a.ld + c;
+        const f32x4 x0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr));
+        const f32x4 x1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + a.ld));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int64_t v = c + e;
           const RowScale& s0 = srs[row];
           const RowScale& s1 = srs[row + 1];
-          // a row without gradient (nc = -inf: padding past the block's rows, whose partials were never written,
-          // or a flagged row) gets the factor 0 without its partial being read
-          const float f0 = s0.nc == -INFINITY ? 0.f
-                           : s0.sign * __builtin_amdgcn_exp2f(fmaf(a.part[(int64_t)(r0 + row) * a.n_tiles + tile].x,
-                                                                   kLog2e, s0.nc));
-          const float f1 = s1.nc == -INFINITY ? 0.f
-                           : s1.sign * __builtin_amdgcn_exp2f(fmaf(a.part[(int64_t)(r0 + row + 1) * a.n_tiles + tile].x,
-                                                                   kLog2e, s1.nc));
-          const f32x2 e00 = unpack_f16(y0[0]), e01 = unpack_f16(y0[1]), e10 = unpack_f16(y1[0]), e11 = unpack_f16(y1[1]);
-          const float x0[4] = {e00[0], e00[1], e01[0], e01[1]}, x1[4] = {e10[0], e10[1], e11[0], e11[1]};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int64_t v = c + e;
-            d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : x0[e] * f0;
-            d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : x1[e] * f1;
-          }
-        } else {
-          const float* zr = a.z + (int64_t)(r0 + row) * a.ld + c;
-          const f32x4 x0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr));
-          const f32x4 x1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + a.ld));
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int64_t v = c + e;
-            const RowScale& s0 = srs[row];
-            const RowScale& s1 = srs[row + 1];
-            d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : s0.sign * __builtin_amdgcn_exp2f(fmaf(x0[e], kLog2e, s0.nc));
-            d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : s1.sign * __builtin_amdgcn_exp2f(fmaf(x1[e], kLog2e, s1.nc));
-          }
+          d0[e] = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : s0.sign * __builtin_amdgcn_exp2f(fmaf(x0[e], kLog2e, s0.nc));
+          d1[e] = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : s1.sign * __builtin_amdgcn_exp2f(fmaf(x1[e], kLog2e, s1.nc));
         }
         const uint32_t p00 = pack_bf16(d0[0], d0[1]), p01 = pack_bf16(d0[2], d0[3]);
         const uint32_t p10 = pack_bf16(d1[0], d1[1]), p11 = pack_bf16(d1[2], d1[3]);
@@ -862,6 +837,76 @@ __global__ __launch_bounds__(256) void k_lm_block_d(const BlockDArgs a) {
         const int t8 = (r0 >> 3) + rc;  // rows 8 t8 .. 8 t8 + 7 of column vc: one packed lane's 16 bytes
         uint16_t* dst = a.packed_dt ? a.DT + ((vc >> 5) * (a.rows >> 4) + (t8 >> 1)) * 512 + ((t8 & 1) * 32 + (vc & 31)) * 8
                                     : a.DT + vc * a.rows + 8 * t8;
+        *reinterpret_cast<u32x4*>(dst) = v;
+      }
+    }
+  }
+}
+
+
+// k_lm_block_d for stored fp16 terms, with each thread on one row pair and 8 columns of a 64 x 64 tile: 16-byte
+// term loads and D stores (6 vector-memory instructions per thread and tile instead of 10).
+__global__ __launch_bounds__(256) void k_lm_block_d16(const BlockDArgs a) {
+  constexpr int kLdw = 33;
+  __shared__ uint32_t tu[2][64 * kLdw];
+  __shared__ RowScale srs[64];
+  const int tid = threadIdx.x;
+  const int64_t n_rt = a.rows / 64;
+  const int64_t n_items = n_rt * ((a.ld + kBlockDStrip - 1) / kBlockDStrip);
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int r0 = (int)(item % n_rt) * 64;
+    const int64_t cs = (item / n_rt) * kBlockDStrip;
+    __syncthreads();  // the previous item's last reads of tu and srs are done
+    if (tid < 64) srs[tid] = a.rs[r0 + tid];
+    __syncthreads();
+    const int cq = tid & 7, rp = tid >> 3;  // columns 8 cq .. 8 cq + 7 of rows 2 rp, 2 rp + 1
+    const int row = 2 * rp;
+    const int ntiles = (int)min((int64_t)(kBlockDStrip / 64), (a.ld - cs) / 64);
+    for (int it = 0; it < ntiles; ++it) {
+      const int64_t c = cs + it * 64 + 8 * cq;
+      uint32_t* t = tu[it & 1];
+      const uint16_t* er = a.e16 + (int64_t)(r0 + row) * a.ld + c;
+      const u32x4 y0 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(er));
+      const u32x4 y1 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(er + a.ld));
+      const int64_t tile = (cs + it * 64) / TILE;
+      const RowScale& s0 = srs[row];
+      const RowScale& s1 = srs[row + 1];
+      const float f0 = s0.nc == -INFINITY ? 0.f
+                       : s0.sign * __builtin_amdgcn_exp2f(fmaf(a.part[(int64_t)(r0 + row) * a.n_tiles + tile].x,
+                                                               kLog2e, s0.nc));
+      const float f1 = s1.nc == -INFINITY ? 0.f
+                       : s1.sign * __builtin_amdgcn_exp2f(fmaf(a.part[(int64_t)(r0 + row + 1) * a.n_tiles + tile].x,
+                                                               kLog2e, s1.nc));
+      uint32_t p0[4], p1[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x2 e0 = unpack_f16(y0[q]), e1 = unpack_f16(y1[q]);
+        const int64_t v = c + 2 * q;
+        const float a00 = v >= a.V ? 0.f : (v == s0.act) ? s0.d_a : e0[0] * f0;
+        const float a01 = v + 1 >= a.V ? 0.f : (v + 1 == s0.act) ? s0.d_a : e0[1] * f0;
+        const float a10 = v >= a.V ? 0.f : (v == s1.act) ? s1.d_a : e1[0] * f1;
+        const float a11 = v + 1 >= a.V ? 0.f : (v + 1 == s1.act) ? s1.d_a : e1[1] * f1;
+        p0[q] = pack_bf16(a00, a01);
+        p1[q] = pack_bf16(a10, a11);
+      }
+      *reinterpret_cast<u32x4*>(a.D + (int64_t)(r0 + row) * a.ld + c) = u32x4{p0[0], p0[1], p0[2], p0[3]};
+      *reinterpret_cast<u32x4*>(a.D + (int64_t)(r0 + row + 1) * a.ld + c) = u32x4{p1[0], p1[1], p1[2], p1[3]};
+      // column 8 cq + e's word: row `row` in the low half, row + 1 in the high half
+      uint32_t* tw = t + 8 * cq * kLdw + rp;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        tw[(2 * q) * kLdw] = (p0[q] & 0xffffu) | (p1[q] << 16);
+        tw[(2 * q + 1) * kLdw] = (p0[q] >> 16) | (p1[q] & 0xffff0000u);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int col = (tid >> 3) + 32 * q, rc = tid & 7;
+        const uint32_t* src = t + col * kLdw + 4 * rc;
+        const u32x4 v = {src[0], src[1], src[2], src[3]};
+        const int64_t vc = cs + it * 64 + col;
+        const int t8 = (r0 >> 3) + rc;  // rows 8 t8 .. 8 t8 + 7 of column vc: one packed lane's 16 bytes
+        uint16_t* dst = a.DT + ((vc >> 5) * (a.rows >> 4) + (t8 >> 1)) * 512 + ((t8 & 1) * 32 + (vc & 31)) * 8;
         *reinterpret_cast<u32x4*>(dst) = v;
       }
     }
@@ -1289,7 +1334,7 @@ extern "C" int fused_lmhead_grpo_blocked(const void* hidden, const void* w_lm, i
     const int rows_p = (rows_of(b) + TILE - 1) / TILE * TILE;
     const BlockDArgs da{nullptr, e_of(b), part_of(b), L.n_tiles, rs + (int64_t)b * L.Tbp, D, DT, L.ldz, (int)V,
                         rows_p, 1};
-    hipLaunchKernelGGL(k_lm_block_d, dim3(block_d_grid(rows_p, L.ldz, grid)), dim3(256), 0, st, da);
+    hipLaunchKernelGGL(k_lm_block_d16, dim3(block_d_grid(rows_p, L.ldz, grid)), dim3(256), 0, st, da);
   };
   // block b's dhidden rows = D W^T (K = V) and dW (+)= h^T D (K = the block's rows, zero-padded), on s
   auto backward = [&](int b) {

@@ -172,7 +172,7 @@ def test_d_pass_fits_beside_the_forward_product():
     res = _kernel_resources(_assembly("lmhead.hip"))
     # the token-blocked forward product: k_lm_partial<STORE_Z = false, PACKED = true, TERMS = true>
     fwd = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_partialILb0ELb1ELb1E")]
-    dpass = [v for k, v in res.items() if k.startswith("_ZN4grpo12k_lm_block_d")]
+    dpass = [v for k, v in res.items() if k.startswith("_ZN4grpo14k_lm_block_d16")]
     assert len(fwd) == 1 and len(dpass) == 1, sorted(res)
     alloc = lambda n: (n + 7) // 8 * 8
     assert 2 * alloc(fwd[0]["vgpr"]) + alloc(dpass[0]["vgpr"]) <= 512, (fwd, dpass)
